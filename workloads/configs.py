@@ -1,0 +1,251 @@
+"""The five synthetic decode workloads and their seeded batch recipes.
+
+Model shapes follow the Llama-3 family the paper serves (decoder-only, GQA,
+RMSNorm, rotary positions, SwiGLU MLP).  Batch shapes stand in for the
+paper's serving workloads: small-batch weight-streaming decode, a shared
+few-shot prefix held once in the paged cache (the BBH-like case), a long
+prompt prefilled in chunks beside running decodes (the GSM8K-like case), and
+a heavy-tailed context-length mix (the CoQA-like case).  No benchmark item
+is used or reproduced; every value is drawn from the seeded generators.
+
+Nothing here computes any part of the decode step.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import gen
+
+BLOCK = 16  # tokens per KV block
+
+
+@dataclass(frozen=True)
+class ModelCfg:
+    name: str
+    n_layers: int
+    hidden: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    ffn: int
+    vocab: int
+    rope_theta: float = 500000.0
+    rms_eps: float = 1e-5
+    max_pos: int = 8192
+    weight_sigma: float = 0.02
+    kv_sigma: float = 1.0
+
+    @property
+    def q_dim(self):
+        return self.n_q_heads * self.head_dim
+
+    @property
+    def kv_dim(self):
+        return self.n_kv_heads * self.head_dim
+
+    @property
+    def kv_bytes_per_token_layer(self):
+        """K and V of one token at one layer, 16-bit elements."""
+        return 2 * self.kv_dim * 2
+
+    def matrix_shapes(self):
+        """Logical [out][in] shapes of the per-layer matrices."""
+        H, F = self.hidden, self.ffn
+        return {
+            "wq": (self.q_dim, H), "wk": (self.kv_dim, H), "wv": (self.kv_dim, H),
+            "wo": (H, self.q_dim), "w_gate": (F, H), "w_up": (F, H), "w_down": (H, F),
+        }
+
+    def layer_weight_bytes(self):
+        return sum(o * i for o, i in self.matrix_shapes().values()) * 2
+
+    def weight_bytes_streamed(self):
+        """Bytes of every matrix read once by one step (embedding rows excluded)."""
+        return self.n_layers * self.layer_weight_bytes() + self.vocab * self.hidden * 2
+
+
+TINY = ModelCfg("tiny-1L", 1, 256, 4, 4, 64, 1024, 1024)
+M3B = ModelCfg("3B-class-GQA", 28, 3072, 24, 8, 128, 8192, 128256)
+M8B = ModelCfg("8B-class-GQA", 32, 4096, 32, 8, 128, 14336, 128256)
+
+
+@dataclass
+class SeqSpec:
+    """One sequence of a pass.
+
+    ctx      : tokens already cached before the pass
+    q_len    : new rows of this sequence in the pass (1 for decode)
+    blocks   : physical block ids given up front (may be shorter than needed;
+               missing blocks are taken from the pool's free list)
+    content  : list of (first_pos, n_pos, content_id): which generator stream
+               fills the cached positions (shared prefixes reuse one id)
+    shared_prefix_of : index of the sequence whose first blocks this one
+               shares, with the number of shared tokens (block aligned)
+    """
+    ctx: int
+    q_len: int
+    blocks: list
+    content: list
+    logits: bool = True
+    shared_prefix: tuple | None = None
+
+
+@dataclass
+class Workload:
+    cfg_id: int
+    name: str
+    model: ModelCfg
+    seqs: list
+    n_pool_blocks: int
+    tokens: np.ndarray            # int32 [rows]
+    seed: int
+    description: str = ""
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def n_rows(self):
+        return sum(s.q_len for s in self.seqs)
+
+    @property
+    def n_seqs(self):
+        return len(self.seqs)
+
+    def logit_rows(self):
+        """Row indices whose logits the pass returns (last row of each marked seq)."""
+        out, r = [], 0
+        for s in self.seqs:
+            r += s.q_len
+            if s.logits:
+                out.append(r - 1)
+        return np.asarray(out, np.int32)
+
+    def resident_tokens(self):
+        """Logical resident tokens after the pass (sum of per-sequence kv lengths)."""
+        return sum(s.ctx + s.q_len for s in self.seqs)
+
+    def unique_resident_tokens(self):
+        """Resident tokens counting a shared prefix once."""
+        tot = 0
+        for s in self.seqs:
+            tot += s.ctx + s.q_len
+            if s.shared_prefix is not None:
+                tot -= s.shared_prefix[1]
+        return tot
+
+
+def _rng(seed, cfg_id, stream):
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, cfg_id, stream])))
+
+
+def _nblk(n_tokens):
+    return (n_tokens + BLOCK - 1) // BLOCK
+
+
+def kv_content_key(seed, model: ModelCfg, content_id, layer, kind):
+    """Generator key of the cached K (kind 0) or V (kind 1) values of one content stream.
+
+    Element index inside the stream: (pos * n_kv_heads + head) * head_dim + dim.
+    """
+    return gen.key_of(seed, "kv", model.name, content_id, layer, kind)
+
+
+def weight_key(seed, model: ModelCfg, name, layer=-1):
+    return gen.key_of(seed, "w", model.name, name, layer)
+
+
+def _decode_workload(cfg_id, name, model, ctx, seed, desc, shared=None, pool_factor=1.25):
+    """Decode batch with randomly permuted block tables (one new row per sequence)."""
+    B = len(ctx)
+    need = []
+    for c in ctx:
+        need.append(_nblk(c + 1))
+    shared_blocks = 0
+    if shared is not None:
+        shared_blocks = shared // BLOCK
+        need = [n - shared_blocks for n in need]
+    total = shared_blocks + sum(need)
+    n_pool = int(math.ceil(1.25 * total)) if pool_factor else total
+    perm = _rng(seed, cfg_id, 1).permutation(n_pool).astype(np.int32)
+    pos = 0
+    prefix_ids = list(perm[:shared_blocks])
+    pos = shared_blocks
+    seqs = []
+    for i, c in enumerate(ctx):
+        own = list(perm[pos:pos + need[i]])
+        pos += need[i]
+        if shared is not None:
+            content = [(0, shared, -1), (shared, c - shared, i)]
+            seqs.append(SeqSpec(int(c), 1, [int(b) for b in prefix_ids + own], content,
+                                shared_prefix=(0, shared) if i > 0 else None))
+        else:
+            seqs.append(SeqSpec(int(c), 1, [int(b) for b in own], [(0, int(c), i)]))
+    tokens = _rng(seed, cfg_id, 2).integers(0, model.vocab, size=B).astype(np.int32)
+    return Workload(cfg_id, name, model, seqs, n_pool, tokens, seed, desc)
+
+
+def workload(cfg_id: int, seed: int = 0, model: ModelCfg | None = None, batch: int | None = None) -> Workload:
+    """Build workload 1..5.  ``model``/``batch`` override shapes for scaled-down test runs."""
+    if cfg_id == 1:
+        m = model or TINY
+        B = batch or 4
+        ctx = _rng(seed, 1, 0).integers(32, 128, endpoint=True, size=B)
+        return _decode_workload(1, "tiny-decode-b4", m, ctx, seed,
+                                "1 layer H256 4x64 heads, batch 4, ctx U[32,128]")
+    if cfg_id == 2:
+        m = model or M3B
+        B = batch or 16
+        ctx = _rng(seed, 2, 0).integers(512, 1024, endpoint=True, size=B)
+        return _decode_workload(2, "3B-decode-b16", m, ctx, seed,
+                                "3B-class GQA, batch 16, ctx U[512,1024]")
+    if cfg_id == 3:
+        m = model or M3B
+        B = batch or 64
+        prefix = 1536
+        suf = _rng(seed, 3, 0).integers(50, 150, endpoint=True, size=B)
+        ctx = prefix + suf
+        return _decode_workload(3, "3B-shared-prefix-b64", m, ctx, seed,
+                                "3B-class GQA, batch 64, 1536-token shared prefix + U[50,150]",
+                                shared=prefix)
+    if cfg_id == 4:
+        m = model or M3B
+        n_dec = batch or 32
+        n_pre, plen = 4, 512
+        ctx = _rng(seed, 4, 0).integers(256, 2048, endpoint=True, size=n_dec)
+        need_dec = [_nblk(c + 1) for c in ctx]
+        need_pre = n_pre * _nblk(plen)
+        total = sum(need_dec) + need_pre
+        n_pool = int(math.ceil(1.25 * total))
+        perm = _rng(seed, 4, 1).permutation(n_pool).astype(np.int32)
+        seqs = []
+        pos = 0
+        # decoding sequences hold permuted blocks
+        dec = []
+        for i, c in enumerate(ctx):
+            own = [int(b) for b in perm[pos:pos + need_dec[i]]]
+            pos += need_dec[i]
+            dec.append(SeqSpec(int(c), 1, own, [(0, int(c), i)]))
+        # fresh requests get their blocks from the free list (lowest id first)
+        pre = [SeqSpec(0, plen, [], [], logits=True) for _ in range(n_pre)]
+        seqs = pre + dec
+        rng = _rng(seed, 4, 2)
+        tokens = rng.integers(0, m.vocab, size=n_pre * plen + n_dec).astype(np.int32)
+        w = Workload(4, "3B-mixed-prefill4x512-decode32", m, seqs, n_pool, tokens, seed,
+                     "3B-class GQA, chunked prefill 4x512 + 32 decodes ctx U[256,2048]")
+        # blocks that are not handed to decoders are free; prefill takes the lowest ids
+        w.extra["free_blocks"] = sorted(int(b) for b in perm[pos:])
+        return w
+    if cfg_id == 5:
+        m = model or M8B
+        B = batch or 128
+        z = _rng(seed, 5, 0).standard_normal(B)
+        ctx = np.clip(np.rint(np.exp(math.log(600.0) + 0.8 * z)), 16, 4096).astype(np.int64)
+        return _decode_workload(5, "8B-decode-b128", m, ctx, seed,
+                                "8B-class GQA, batch 128, ctx lognormal(600, 0.8) in [16,4096]")
+    raise ValueError(cfg_id)
+
+
+def token_ids_key(seed, cfg_id):
+    return gen.key_of(seed, "tokens", cfg_id)
