@@ -1,0 +1,209 @@
+/*
+ * vsk.h -- C ABI of the MI355X (gfx950) batched decode step.
+ *
+ * One forward pass of a Llama-style GQA decoder over the rows of a batch:
+ * paged-attention decode over a block-table KV cache, bf16 weight-streaming
+ * projections with a SwiGLU MLP, fused RMSNorm and rotary positions, and a
+ * greedy argmax.  This is the dense-mode pass of the paper ("Design and
+ * Implementation": dense mode runs every layer for every row; a row is one
+ * token's hidden state, one per sequence in decode and several in prefill).
+ *
+ * Conventions
+ *  - Every function returns an int status (VSK_OK or a negative VSK_E_*).
+ *    On error nothing is launched and no state changes; vsk_last_error()
+ *    holds a message.  No exceptions cross this boundary.
+ *  - "dev" pointers are device (HBM) pointers, "host" pointers are host
+ *    memory.  The library never allocates or frees device memory: every
+ *    device buffer (weights, packed weights, KV pool, batch metadata,
+ *    workspace, outputs) belongs to the caller and must outlive its use.
+ *    Host arrays are copied, never retained.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Device work is enqueued asynchronously on it; nothing synchronises,
+ *    except vsk_batch_upload, which returns once its host source can be reused.
+ *  - bf16 tensors are IEEE bfloat16 bit patterns (uint16), row-major unless
+ *    stated otherwise.  Matrices are [out][in].
+ *  - A handle is not thread-safe.  Device faults surface at the caller's
+ *    next synchronisation (and as VSK_E_HIP from a later call).
+ */
+#ifndef VSK_H
+#define VSK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  VSK_OK = 0,
+  VSK_E_ARG = -1,          /* bad argument, shape or size */
+  VSK_E_NOMEM = -2,        /* KV pool has too few free blocks */
+  VSK_E_RANGE = -3,        /* block id, slot or position out of range */
+  VSK_E_SHARED_WRITE = -4, /* a new position falls in a block shared by several sequences */
+  VSK_E_STATE = -5,        /* call out of order (unknown/duplicate sequence, nothing bound) */
+  VSK_E_HIP = -6,          /* the HIP runtime reported an error */
+  VSK_E_UNSUPPORTED = -7   /* shape this build has no kernel for */
+};
+
+/* Model shape.  block_size must be 16; head_dim 64 or 128; n_q_heads a
+ * multiple of n_kv_heads with at most 16 query heads per KV head; hidden,
+ * n_q_heads*head_dim and ffn multiples of 64; vocab a multiple of 16.
+ * max_pos bounds positions (rotary table length). */
+typedef struct vsk_model_cfg {
+  int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
+  int32_t block_size, max_pos;
+  float rope_theta, rms_eps;
+} vsk_model_cfg;
+
+typedef struct vsk_handle vsk_handle;
+
+const char* vsk_status_str(int status);
+const char* vsk_last_error(const vsk_handle* h);
+
+/* Validate cfg and create a handle (host memory only; touches no device). */
+int vsk_create(const vsk_model_cfg* cfg, vsk_handle** out);
+int vsk_destroy(vsk_handle* h);
+
+/* ----------------------------------------------------------------- weights
+ * The projections stream every weight byte once per pass; below the ridge
+ * point decode is bound by that weight bandwidth (paper, appendix "The
+ * Switching Thresholds from the Roofline", decode rule).  The library
+ * repacks each [out][in] matrix once into 1 KiB tiles laid out as the matrix
+ * cores consume them, so a pass reads each tile with one coalesced 16-byte
+ * load per lane. */
+typedef struct vsk_layer_weights {
+  const void* attn_norm; /* dev bf16 [hidden] */
+  const void* wq;        /* dev bf16 [n_q_heads*head_dim][hidden] */
+  const void* wk;        /* dev bf16 [n_kv_heads*head_dim][hidden] */
+  const void* wv;        /* dev bf16 [n_kv_heads*head_dim][hidden] */
+  const void* wo;        /* dev bf16 [hidden][n_q_heads*head_dim] */
+  const void* mlp_norm;  /* dev bf16 [hidden] */
+  const void* w_gate;    /* dev bf16 [ffn][hidden] */
+  const void* w_up;      /* dev bf16 [ffn][hidden] */
+  const void* w_down;    /* dev bf16 [hidden][ffn] */
+} vsk_layer_weights;
+
+/* Bytes of the packed weight buffer (all layers, embedding, lm_head, norms,
+ * rotary table). */
+size_t vsk_packed_weight_bytes(const vsk_model_cfg* cfg);
+/* Bind a caller-owned device buffer of at least vsk_packed_weight_bytes(). */
+int vsk_weights_bind(vsk_handle* h, void* packed_dev, size_t bytes);
+/* Repack one layer from logical [out][in] bf16 (source may be freed after
+ * the stream passes this point).  Not part of the timed pass. */
+int vsk_weights_pack_layer(vsk_handle* h, int32_t layer, const vsk_layer_weights* w, void* stream);
+/* Repack embedding [vocab][hidden], lm_head [vocab][hidden] (untied),
+ * final norm gain [hidden]; also writes the rotary cos/sin table. */
+int vsk_weights_pack_head(vsk_handle* h, const void* embed_dev, const void* lm_head_dev,
+                          const void* final_norm_dev, void* stream);
+
+/* ----------------------------------------------------------------- KV cache
+ * Paged KV cache (paper, "Invariants for Correct Mixed-Depth Execution":
+ * position t of layer l holds that layer's own K and V, Invariant 1; every
+ * row-to-memory map is rebuilt from the current row set, Invariant 2).
+ * The pool holds n_blocks blocks of 16 tokens for every layer, K and V.
+ * Its internal layout is private to the library; use vsk_kv_write /
+ * vsk_kv_read to move logical [n][n_kv_heads][head_dim] bf16 values.
+ * Position p of a sequence lives at slot table[p/16]*16 + p%16. */
+size_t vsk_kv_pool_bytes(const vsk_model_cfg* cfg, int32_t n_blocks);
+/* Bind a pool of n_blocks blocks.  pool_dev may be NULL, in which case only
+ * the host allocator exists (device calls that need the pool return
+ * VSK_E_STATE).  Resets the allocator: every block free, no sequences. */
+int vsk_kv_init(vsk_handle* h, void* pool_dev, int32_t n_blocks);
+
+int vsk_seq_create(vsk_handle* h, int64_t seq);
+/* Drop the sequence; blocks whose reference count reaches 0 become free. */
+int vsk_seq_release(vsk_handle* h, int64_t seq);
+/* Install a caller-chosen block table (host int32[n]) holding ctx_len
+ * resident tokens; each listed block gains a reference.  The same block may
+ * appear in several sequences' tables (a shared prefix).  Requires an empty
+ * sequence, distinct in-range ids and n*16 >= ctx_len. */
+int vsk_seq_set_blocks(vsk_handle* h, int64_t seq, const int32_t* blocks_host, int32_t n,
+                       int32_t ctx_len);
+/* dst (empty) shares the first n_tokens (a multiple of 16, <= src length)
+ * of src's blocks. */
+int vsk_seq_share_prefix(vsk_handle* h, int64_t dst, int64_t src, int32_t n_tokens);
+/* Append n_new positions to seq.  A position that starts a block beyond the
+ * table takes the lowest-numbered free block.  Writing into a block with more
+ * than one reference is VSK_E_SHARED_WRITE (no copy-on-write); too few free
+ * blocks is VSK_E_NOMEM.  All or nothing.  slots_host (nullable, int32[n_new])
+ * receives the new positions' slots. */
+int vsk_kv_reserve(vsk_handle* h, int64_t seq, int32_t n_new, int32_t* slots_host);
+/* Length and block table of seq: *len, *n_blocks, and up to cap ids. */
+int vsk_seq_info(const vsk_handle* h, int64_t seq, int32_t* len, int32_t* n_blocks,
+                 int32_t* blocks_host, int32_t cap);
+int vsk_kv_free_blocks(const vsk_handle* h, int32_t* n_free);
+/* Scatter logical k, v (dev bf16 [n][n_kv_heads][head_dim]) of one layer to
+ * the given slots (dev int32[n]) / gather them back.  Setup and inspection. */
+int vsk_kv_write(vsk_handle* h, int32_t layer, const int32_t* slots_dev, int32_t n,
+                 const void* k_dev, const void* v_dev, void* stream);
+int vsk_kv_read(vsk_handle* h, int32_t layer, const int32_t* slots_dev, int32_t n,
+                void* k_dev, void* v_dev, void* stream);
+
+/* ----------------------------------------------------------------- batch
+ * Per-pass metadata, rebuilt from the current row set every pass
+ * (Invariant 2).  For sequences seqs[0..n) with q_lens new rows each (the
+ * rows are the last q_len resident positions, already reserved):
+ *   block_table [n][max_blocks] int32 (unused entries -1)
+ *   kv_len [n], cu_q [n+1], and per row r: row_seq[r], pos[r], slot[r].
+ * Rows are numbered sequence by sequence.  vsk_batch_build validates and
+ * keeps the host copy in the handle; vsk_batch_host_* reads it back. */
+int vsk_batch_build(vsk_handle* h, const int64_t* seqs_host, const int32_t* q_lens_host,
+                    int32_t n_seqs);
+int vsk_batch_shape(const vsk_handle* h, int32_t* n_seqs, int32_t* n_rows, int32_t* max_blocks);
+int vsk_batch_host_copy(const vsk_handle* h, int32_t* block_table, int32_t* kv_len, int32_t* cu_q,
+                        int32_t* row_seq, int32_t* pos, int32_t* slot);
+/* Device bytes needed by vsk_batch_upload for the current batch. */
+size_t vsk_batch_device_bytes(const vsk_handle* h);
+/* Copy the metadata into caller device memory (H2D on stream) and make it
+ * the batch of the following passes.  The buffer must stay valid and
+ * unmodified while those passes run. */
+int vsk_batch_upload(vsk_handle* h, void* meta_dev, size_t bytes, void* stream);
+
+/* ----------------------------------------------------------------- passes
+ * Workspace: caller-owned device scratch sized for a capacity (max rows,
+ * sequences and resident length of any pass that will use it).
+ * vsk_workspace_init binds it to the handle and clears it on `stream`
+ * (cross-workgroup arrival counters start at zero and every pass leaves them
+ * at zero again).  Passes must then be given the bound buffer and fit its
+ * capacity.  One workspace must not serve two passes that run concurrently. */
+size_t vsk_workspace_bytes(const vsk_handle* h, int32_t max_rows, int32_t max_seqs,
+                           int32_t max_kv_len);
+int vsk_workspace_init(vsk_handle* h, void* ws_dev, size_t bytes, int32_t max_rows,
+                       int32_t max_seqs, int32_t max_kv_len, void* stream);
+
+/* One decode step over the uploaded batch (every q_len must be 1):
+ * ids_dev int32[n_rows] input tokens; writes every layer's K,V of every row
+ * at its slot; logits_dev bf16 [n_rows][vocab]; next_ids_dev (nullable)
+ * int32[n_rows] = lowest index of the maximum fp32 logit (greedy).
+ * Replaying the same batch and ids rewrites the same slots with the same
+ * bytes, so the step is idempotent. */
+int vsk_decode_step(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int32_t* next_ids_dev,
+                    void* ws_dev, size_t ws_bytes, void* stream);
+
+/* One ragged pass over the uploaded batch (any q_lens: chunked prefill rows
+ * and decode rows together).  Prefill row at position p attends to keys
+ * 0..p of its sequence; all of a layer's new K,V are written before that
+ * layer's attention reads them.  Logits (bf16 [n_logit_rows][vocab]) and
+ * next ids are produced only for the rows listed in logit_rows_dev
+ * (int32[n_logit_rows]). */
+int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logit_rows_dev,
+                      int32_t n_logit_rows, void* logits_dev, int32_t* next_ids_dev,
+                      void* ws_dev, size_t ws_bytes, void* stream);
+
+/* Greedy sampling over given logits (dtype 0 = bf16, 1 = fp32), row-major
+ * [rows][vocab]: ids_dev[r] = lowest index of the maximum; NaN never wins;
+ * an all-NaN row gives 0.  Uses no workspace beyond its arguments. */
+int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab,
+                      int32_t* ids_dev, void* stream);
+
+/* Counters of what the last pass executed (kernel variants, split factors),
+ * for attestation in tests and benchmarks.  Writes up to cap int64 values:
+ * [0] passes run, [1] gemm launches, [2] attention launches, [3] attention
+ * splits (max per row), [4] gemm K-splits of the last down projection. */
+int vsk_exec_counters(const vsk_handle* h, int64_t* out, int32_t cap);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VSK_H */

@@ -147,13 +147,17 @@ def build_batch(alloc: BlockAllocator, seqs, q_lens):
     n = len(seqs)
     if len(q_lens) != n:
         raise AllocError("ARG", "length mismatch")
+    if n == 0:
+        raise AllocError("ARG", "empty batch")
+    if len(set(seqs)) != n:
+        raise AllocError("ARG", "sequence listed twice in one pass")
     kv_len = []
     for s, q in zip(seqs, q_lens):
         if s not in alloc.seqs:
             raise AllocError("STATE", f"unknown sequence {s}")
         L = alloc.length(s)
-        if q < 0 or q > L:
-            raise AllocError("ARG", "rows exceed resident tokens")
+        if q < 1 or q > L:
+            raise AllocError("ARG", "rows of a sequence must be 1..resident length")
         kv_len.append(L)
     max_blocks = max([len(alloc.table(s)) for s in seqs] + [1])
     table = -np.ones((n, max_blocks), np.int32)

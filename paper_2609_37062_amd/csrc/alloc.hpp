@@ -1,0 +1,75 @@
+// Host-side KV block allocator and per-pass batch metadata.
+//
+// Paged KV bookkeeping of the serving engine (paper, "Invariants for
+// Correct Mixed-Depth Execution"): position t of a sequence lives at slot
+// table[t/16]*16 + t%16 of every layer's cache (Invariant 1 keeps every
+// layer's own K,V there) and the row-to-slot maps are rebuilt from the
+// current row set for every pass (Invariant 2).  Plain C++17, no HIP.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+namespace vsk {
+
+enum Status : int {
+  kOk = 0,
+  kErrArg = -1,
+  kErrNomem = -2,
+  kErrRange = -3,
+  kErrSharedWrite = -4,
+  kErrState = -5,
+  kErrHip = -6,
+  kErrUnsupported = -7,
+};
+
+struct SeqState {
+  std::vector<int32_t> blocks;
+  int32_t len = 0;
+};
+
+// Reference-counted block pool.  Free blocks are handed out lowest id first.
+// Every mutating call is all-or-nothing: on error the state is unchanged and
+// `err` says why.
+class BlockAllocator {
+ public:
+  BlockAllocator() = default;
+  explicit BlockAllocator(int32_t n_blocks, int32_t block = 16);
+
+  int seq_create(int64_t seq, std::string& err);
+  int seq_release(int64_t seq, std::string& err);
+  int seq_set_blocks(int64_t seq, const int32_t* blocks, int32_t n, int32_t ctx_len, std::string& err);
+  int seq_share_prefix(int64_t dst, int64_t src, int32_t n_tokens, std::string& err);
+  int reserve(int64_t seq, int32_t n_new, int32_t* slots_out, std::string& err);
+
+  const SeqState* find(int64_t seq) const;
+  int32_t n_blocks() const { return static_cast<int32_t>(ref_.size()); }
+  int32_t block() const { return block_; }
+  int32_t free_count() const { return free_count_; }
+
+ private:
+  // lowest free block id at or after `from`, or -1
+  int32_t next_free(int32_t from) const;
+  int32_t block_ = 16;
+  std::vector<int32_t> ref_;
+  int32_t free_count_ = 0;
+  std::unordered_map<int64_t, SeqState> seqs_;
+};
+
+// Host copy of one pass's metadata (see vsk_batch_build in vsk.h).
+struct BatchHost {
+  int32_t n_seqs = 0, n_rows = 0, max_blocks = 0, max_kv_len = 0, max_q_len = 0;
+  std::vector<int32_t> block_table;  // [n_seqs][max_blocks]
+  std::vector<int32_t> kv_len;       // [n_seqs]
+  std::vector<int32_t> cu_q;         // [n_seqs + 1]
+  std::vector<int32_t> row_seq;      // [n_rows]
+  std::vector<int32_t> pos;          // [n_rows]
+  std::vector<int32_t> slot;         // [n_rows]
+};
+
+int build_batch(const BlockAllocator& a, const int64_t* seqs, const int32_t* q_lens, int32_t n,
+                BatchHost& out, std::string& err);
+
+}  // namespace vsk

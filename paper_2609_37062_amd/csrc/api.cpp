@@ -1,0 +1,610 @@
+// The C ABI (include/vsk.h): validation, host allocator, layouts and the
+// orchestration of one forward pass over the rows of a batch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "attn.hpp"
+#include "gemm.hpp"
+#include "internal.hpp"
+#include "misc.hpp"
+
+using namespace vsk;
+
+struct vsk_handle : public Handle {};
+
+namespace vsk {
+
+PackedLayout packed_layout(const vsk_model_cfg& c) {
+  PackedLayout p;
+  const size_t H = c.hidden, F = c.ffn, Nq = static_cast<size_t>(c.n_q_heads) * c.head_dim,
+               Nkv = static_cast<size_t>(c.n_kv_heads) * c.head_dim, V = c.vocab;
+  size_t o = 0;
+  p.l.attn_norm = o; o = align_up(o + H * 2);
+  p.l.mlp_norm = o; o = align_up(o + H * 2);
+  p.l.wqkv = o; o = align_up(o + (Nq + 2 * Nkv) * H * 2);
+  p.l.wo = o; o = align_up(o + H * Nq * 2);
+  p.l.wgu = o; o = align_up(o + 2 * F * H * 2);
+  p.l.wd = o; o = align_up(o + H * F * 2);
+  p.layer_bytes = o;
+  p.head_base = p.layer_bytes * c.n_layers;
+  o = p.head_base;
+  p.final_norm = o; o = align_up(o + H * 2);
+  p.embed = o; o = align_up(o + V * H * 2);
+  p.lm_head = o; o = align_up(o + V * H * 2);
+  p.rope = o; o = align_up(o + static_cast<size_t>(c.max_pos) * (c.head_dim / 2) * 8);
+  p.total = o;
+  return p;
+}
+
+static int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// partial-buffer bytes and counter count needed by a projection over up to R rows
+static void gemm_ws_need(int N, int K, int R_max, int epi, size_t& part, size_t& cnt) {
+  for (int Rg = 1; Rg <= ceil_div(R_max, 16); ++Rg) {
+    const GemmPlan p = plan_gemm(N, K, 16 * Rg, epi);
+    const size_t tiles = static_cast<size_t>(p.m_tiles) * p.n_groups;
+    const size_t rows_per_group = p.mg <= 2 ? 16 : 64;
+    if (p.ks > 1) part = std::max(part, tiles * p.ks * rows_per_group * 16 * p.mg * 4);
+    cnt = std::max(cnt, tiles);
+  }
+}
+
+WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len) {
+  WsLayout w;
+  w.max_rows = max_rows;
+  w.max_seqs = max_seqs;
+  w.max_kv_len = max_kv_len;
+  w.Rg = ceil_div(max_rows, 16);
+  w.max_splits = attn_splits(max_kv_len);
+  const size_t H = c.hidden, F = c.ffn, Nq = static_cast<size_t>(c.n_q_heads) * c.head_dim,
+               Nkv = static_cast<size_t>(c.n_kv_heads) * c.head_dim;
+  const size_t Rp = static_cast<size_t>(w.Rg) * 16;
+  const int G = c.n_q_heads / c.n_kv_heads;
+  size_t o = 0;
+  w.x = o; o = align_up(o + static_cast<size_t>(max_rows) * H * 4);
+  w.act0 = o; o = align_up(o + Rp * std::max(H, Nq) * 2);
+  w.act1 = o; o = align_up(o + Rp * F * 2);
+  w.q = o; o = align_up(o + static_cast<size_t>(max_rows) * Nq * 2);
+  const size_t rh = static_cast<size_t>(max_rows) * c.n_kv_heads;
+  w.att_o = o; o = align_up(o + rh * w.max_splits * G * c.head_dim * 4);
+  w.att_ml = o; o = align_up(o + rh * w.max_splits * G * 8);
+  size_t part = 0, cnt = 0;
+  gemm_ws_need(static_cast<int>(Nq + 2 * Nkv), c.hidden, max_rows, EPI_QKV, part, cnt);
+  gemm_ws_need(c.hidden, static_cast<int>(Nq), max_rows, EPI_RESID, part, cnt);
+  gemm_ws_need(2 * c.ffn, c.hidden, max_rows, EPI_SWIGLU, part, cnt);
+  gemm_ws_need(c.hidden, c.ffn, max_rows, EPI_RESID, part, cnt);
+  w.gemm_part = o; o = align_up(o + part);
+  // lm_head partials: n_groups x rows
+  const GemmPlan lp = plan_gemm(c.vocab, c.hidden, max_rows, EPI_LOGITS);
+  const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
+  (void)lp;
+  w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
+  // counters last so one clear covers them
+  w.counters_begin = o;
+  w.att_cnt = o; o = align_up(o + rh * 4);
+  w.gemm_cnt = o; o = align_up(o + cnt * 4);
+  w.counters_end = o;
+  w.total = o;
+  return w;
+}
+
+}  // namespace vsk
+
+// ------------------------------------------------------------------ helpers
+static int fail(vsk_handle* h, int code, const std::string& msg) {
+  if (h) h->err = msg;
+  return code;
+}
+
+static int hip_check(vsk_handle* h, hipError_t e, const char* what) {
+  if (e == hipSuccess) return VSK_OK;
+  return fail(h, VSK_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+static bool cfg_ok(const vsk_model_cfg* c, std::string& why) {
+  if (!c) { why = "null config"; return false; }
+  if (c->n_layers < 1 || c->hidden < 64 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn < 64 ||
+      c->vocab < 16 || c->max_pos < 1) { why = "non-positive dimension"; return false; }
+  if (c->block_size != kBlock) { why = "block_size must be 16"; return false; }
+  if (c->head_dim != 64 && c->head_dim != 128) { why = "head_dim must be 64 or 128"; return false; }
+  if (c->n_q_heads % c->n_kv_heads != 0 || c->n_q_heads / c->n_kv_heads > 16) {
+    why = "n_q_heads must be a multiple of n_kv_heads, at most 16 per group"; return false;
+  }
+  if (c->hidden % 64 || (c->n_q_heads * c->head_dim) % 64 || c->ffn % 64 || c->vocab % 64) {
+    why = "hidden, n_q_heads*head_dim, ffn and vocab must be multiples of 64"; return false;
+  }
+  if (!(c->rms_eps >= 0.f) || !(c->rope_theta > 0.f)) { why = "bad eps or rope theta"; return false; }
+  return true;
+}
+
+extern "C" {
+
+const char* vsk_status_str(int s) {
+  switch (s) {
+    case VSK_OK: return "ok";
+    case VSK_E_ARG: return "bad argument";
+    case VSK_E_NOMEM: return "KV pool exhausted";
+    case VSK_E_RANGE: return "out of range";
+    case VSK_E_SHARED_WRITE: return "write into a shared block";
+    case VSK_E_STATE: return "invalid state";
+    case VSK_E_HIP: return "HIP runtime error";
+    case VSK_E_UNSUPPORTED: return "unsupported shape";
+    default: return "unknown status";
+  }
+}
+
+const char* vsk_last_error(const vsk_handle* h) { return h ? h->err.c_str() : "null handle"; }
+
+int vsk_create(const vsk_model_cfg* cfg, vsk_handle** out) {
+  if (!out) return VSK_E_ARG;
+  *out = nullptr;
+  std::string why;
+  if (!cfg_ok(cfg, why)) return VSK_E_ARG;
+  vsk_handle* h = new (std::nothrow) vsk_handle();
+  if (!h) return VSK_E_ARG;
+  h->cfg = *cfg;
+  h->pl = packed_layout(*cfg);
+  *out = h;
+  return VSK_OK;
+}
+
+int vsk_destroy(vsk_handle* h) {
+  delete h;
+  return VSK_OK;
+}
+
+size_t vsk_packed_weight_bytes(const vsk_model_cfg* cfg) {
+  std::string why;
+  if (!cfg_ok(cfg, why)) return 0;
+  return packed_layout(*cfg).total;
+}
+
+int vsk_weights_bind(vsk_handle* h, void* packed_dev, size_t bytes) {
+  if (!h) return VSK_E_ARG;
+  if (!packed_dev || bytes < h->pl.total) return fail(h, VSK_E_ARG, "packed weight buffer too small");
+  if (reinterpret_cast<uintptr_t>(packed_dev) % kAlign) return fail(h, VSK_E_ARG, "packed buffer not 256-byte aligned");
+  h->packed = static_cast<uint8_t*>(packed_dev);
+  h->packed_bytes = bytes;
+  return VSK_OK;
+}
+
+int vsk_weights_pack_layer(vsk_handle* h, int32_t layer, const vsk_layer_weights* w, void* stream) {
+  if (!h || !w) return VSK_E_ARG;
+  if (!h->packed) return fail(h, VSK_E_STATE, "no packed weight buffer bound");
+  const vsk_model_cfg& c = h->cfg;
+  if (layer < 0 || layer >= c.n_layers) return fail(h, VSK_E_RANGE, "layer out of range");
+  if (!w->attn_norm || !w->wq || !w->wk || !w->wv || !w->wo || !w->mlp_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return fail(h, VSK_E_ARG, "null weight pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* base = h->packed + h->pl.layer_bytes * layer;
+  const int H = c.hidden, F = c.ffn, d = c.head_dim, Nq = c.n_q_heads * d, Nkv = c.n_kv_heads * d;
+  auto u16 = [](const void* p) { return static_cast<const uint16_t*>(p); };
+  auto dst = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
+  hipError_t e;
+  if ((e = launch_copy_bf16(u16(w->attn_norm), dst(h->pl.l.attn_norm), H, s)) != hipSuccess) return hip_check(h, e, "pack");
+  if ((e = launch_copy_bf16(u16(w->mlp_norm), dst(h->pl.l.mlp_norm), H, s)) != hipSuccess) return hip_check(h, e, "pack");
+  if ((e = launch_pack(u16(w->wq), u16(w->wk), u16(w->wv), Nq, Nkv, Nq + 2 * Nkv, H, 1, d, Nq + Nkv,
+                       dst(h->pl.l.wqkv), s)) != hipSuccess) return hip_check(h, e, "pack qkv");
+  if ((e = launch_pack(u16(w->wo), nullptr, nullptr, H, 0, H, Nq, 0, d, 0, dst(h->pl.l.wo), s)) != hipSuccess)
+    return hip_check(h, e, "pack o");
+  if ((e = launch_pack(u16(w->w_gate), u16(w->w_up), nullptr, F, F, 2 * F, H, 2, d, 0, dst(h->pl.l.wgu), s)) !=
+      hipSuccess) return hip_check(h, e, "pack gate/up");
+  if ((e = launch_pack(u16(w->w_down), nullptr, nullptr, H, 0, H, F, 0, d, 0, dst(h->pl.l.wd), s)) != hipSuccess)
+    return hip_check(h, e, "pack down");
+  return VSK_OK;
+}
+
+int vsk_weights_pack_head(vsk_handle* h, const void* embed_dev, const void* lm_head_dev, const void* final_norm_dev,
+                          void* stream) {
+  if (!h) return VSK_E_ARG;
+  if (!h->packed) return fail(h, VSK_E_STATE, "no packed weight buffer bound");
+  if (!embed_dev || !lm_head_dev || !final_norm_dev) return fail(h, VSK_E_ARG, "null weight pointer");
+  const vsk_model_cfg& c = h->cfg;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t VH = static_cast<size_t>(c.vocab) * c.hidden;
+  auto u16 = [](const void* p) { return static_cast<const uint16_t*>(p); };
+  hipError_t e;
+  if ((e = launch_copy_bf16(u16(final_norm_dev), reinterpret_cast<uint16_t*>(h->packed + h->pl.final_norm), c.hidden,
+                            s)) != hipSuccess) return hip_check(h, e, "pack final norm");
+  if ((e = hipMemcpyAsync(h->packed + h->pl.embed, embed_dev, VH * 2, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+    return hip_check(h, e, "copy embedding");
+  if ((e = launch_pack(u16(lm_head_dev), nullptr, nullptr, c.vocab, 0, c.vocab, c.hidden, 0, c.head_dim, 0,
+                       reinterpret_cast<uint16_t*>(h->packed + h->pl.lm_head), s)) != hipSuccess)
+    return hip_check(h, e, "pack lm_head");
+  // rotary table: (cos, sin) of pos * theta^(-2j/d) in double, stored as float
+  const int half = c.head_dim / 2;
+  std::vector<float> tab(static_cast<size_t>(c.max_pos) * half * 2);
+  for (int p = 0; p < c.max_pos; ++p)
+    for (int j = 0; j < half; ++j) {
+      const double inv = std::pow(static_cast<double>(c.rope_theta), -2.0 * j / c.head_dim);
+      const double ang = static_cast<double>(p) * inv;
+      tab[(static_cast<size_t>(p) * half + j) * 2 + 0] = static_cast<float>(std::cos(ang));
+      tab[(static_cast<size_t>(p) * half + j) * 2 + 1] = static_cast<float>(std::sin(ang));
+    }
+  if ((e = hipMemcpyAsync(h->packed + h->pl.rope, tab.data(), tab.size() * 4, hipMemcpyHostToDevice, s)) != hipSuccess)
+    return hip_check(h, e, "copy rotary table");
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_check(h, e, "sync");
+  return VSK_OK;
+}
+
+// ------------------------------------------------------------------ KV
+size_t vsk_kv_pool_bytes(const vsk_model_cfg* cfg, int32_t n_blocks) {
+  std::string why;
+  if (!cfg_ok(cfg, why) || n_blocks <= 0) return 0;
+  return static_cast<size_t>(cfg->n_layers) * 2 * n_blocks * cfg->n_kv_heads * kBlock * cfg->head_dim * 2;
+}
+
+int vsk_kv_init(vsk_handle* h, void* pool_dev, int32_t n_blocks) {
+  if (!h) return VSK_E_ARG;
+  if (n_blocks <= 0) return fail(h, VSK_E_ARG, "n_blocks must be positive");
+  if (static_cast<int64_t>(n_blocks) * kBlock > INT32_MAX) return fail(h, VSK_E_ARG, "pool too large for int32 slots");
+  h->pool = static_cast<uint16_t*>(pool_dev);
+  h->n_blocks = n_blocks;
+  h->alloc = BlockAllocator(n_blocks, kBlock);
+  h->alloc_ready = true;
+  h->batch_built = false;
+  h->batch_uploaded = false;
+  return VSK_OK;
+}
+
+#define NEED_ALLOC(h)                                                   \
+  do {                                                                  \
+    if (!(h)) return VSK_E_ARG;                                         \
+    if (!(h)->alloc_ready) return fail((h), VSK_E_STATE, "kv_init not called"); \
+  } while (0)
+
+int vsk_seq_create(vsk_handle* h, int64_t seq) {
+  NEED_ALLOC(h);
+  return h->alloc.seq_create(seq, h->err);
+}
+
+int vsk_seq_release(vsk_handle* h, int64_t seq) {
+  NEED_ALLOC(h);
+  return h->alloc.seq_release(seq, h->err);
+}
+
+int vsk_seq_set_blocks(vsk_handle* h, int64_t seq, const int32_t* blocks_host, int32_t n, int32_t ctx_len) {
+  NEED_ALLOC(h);
+  return h->alloc.seq_set_blocks(seq, blocks_host, n, ctx_len, h->err);
+}
+
+int vsk_seq_share_prefix(vsk_handle* h, int64_t dst, int64_t src, int32_t n_tokens) {
+  NEED_ALLOC(h);
+  return h->alloc.seq_share_prefix(dst, src, n_tokens, h->err);
+}
+
+int vsk_kv_reserve(vsk_handle* h, int64_t seq, int32_t n_new, int32_t* slots_host) {
+  NEED_ALLOC(h);
+  const SeqState* s = h->alloc.find(seq);
+  if (s && static_cast<int64_t>(s->len) + n_new > h->cfg.max_pos)
+    return fail(h, VSK_E_RANGE, "positions would exceed max_pos");
+  return h->alloc.reserve(seq, n_new, slots_host, h->err);
+}
+
+int vsk_seq_info(const vsk_handle* h, int64_t seq, int32_t* len, int32_t* n_blocks, int32_t* blocks_host,
+                 int32_t cap) {
+  if (!h || !h->alloc_ready) return VSK_E_STATE;
+  const SeqState* s = h->alloc.find(seq);
+  if (!s) return VSK_E_STATE;
+  if (len) *len = s->len;
+  if (n_blocks) *n_blocks = static_cast<int32_t>(s->blocks.size());
+  if (blocks_host)
+    for (int32_t i = 0; i < cap && i < static_cast<int32_t>(s->blocks.size()); ++i) blocks_host[i] = s->blocks[i];
+  return VSK_OK;
+}
+
+int vsk_kv_free_blocks(const vsk_handle* h, int32_t* n_free) {
+  if (!h || !h->alloc_ready || !n_free) return VSK_E_STATE;
+  *n_free = h->alloc.free_count();
+  return VSK_OK;
+}
+
+static int kv_move(vsk_handle* h, bool write, int32_t layer, const int32_t* slots, int32_t n, const void* k,
+                   const void* v, void* stream) {
+  if (!h) return VSK_E_ARG;
+  if (!h->pool) return fail(h, VSK_E_STATE, "no KV pool bound");
+  if (layer < 0 || layer >= h->cfg.n_layers) return fail(h, VSK_E_RANGE, "layer out of range");
+  if (n < 0 || (n > 0 && (!slots || !k || !v))) return fail(h, VSK_E_ARG, "bad KV transfer arguments");
+  hipError_t e = launch_kv_move(write, h->pool, layer, h->n_blocks, h->cfg.n_kv_heads, h->cfg.head_dim, slots, n,
+                                const_cast<uint16_t*>(static_cast<const uint16_t*>(k)),
+                                const_cast<uint16_t*>(static_cast<const uint16_t*>(v)),
+                                static_cast<hipStream_t>(stream));
+  return hip_check(h, e, "kv transfer");
+}
+
+int vsk_kv_write(vsk_handle* h, int32_t layer, const int32_t* slots_dev, int32_t n, const void* k_dev,
+                 const void* v_dev, void* stream) {
+  return kv_move(h, true, layer, slots_dev, n, k_dev, v_dev, stream);
+}
+
+int vsk_kv_read(vsk_handle* h, int32_t layer, const int32_t* slots_dev, int32_t n, void* k_dev, void* v_dev,
+                void* stream) {
+  return kv_move(h, false, layer, slots_dev, n, k_dev, v_dev, stream);
+}
+
+// ------------------------------------------------------------------ batch
+int vsk_batch_build(vsk_handle* h, const int64_t* seqs_host, const int32_t* q_lens_host, int32_t n_seqs) {
+  NEED_ALLOC(h);
+  BatchHost b;
+  int st = build_batch(h->alloc, seqs_host, q_lens_host, n_seqs, b, h->err);
+  if (st != VSK_OK) return st;
+  h->bh = std::move(b);
+  h->batch_built = true;
+  h->batch_uploaded = false;
+  return VSK_OK;
+}
+
+int vsk_batch_shape(const vsk_handle* h, int32_t* n_seqs, int32_t* n_rows, int32_t* max_blocks) {
+  if (!h || !h->batch_built) return VSK_E_STATE;
+  if (n_seqs) *n_seqs = h->bh.n_seqs;
+  if (n_rows) *n_rows = h->bh.n_rows;
+  if (max_blocks) *max_blocks = h->bh.max_blocks;
+  return VSK_OK;
+}
+
+int vsk_batch_host_copy(const vsk_handle* h, int32_t* block_table, int32_t* kv_len, int32_t* cu_q, int32_t* row_seq,
+                        int32_t* pos, int32_t* slot) {
+  if (!h || !h->batch_built) return VSK_E_STATE;
+  const BatchHost& b = h->bh;
+  auto cp = [](int32_t* d, const std::vector<int32_t>& s) {
+    if (d) std::memcpy(d, s.data(), s.size() * 4);
+  };
+  cp(block_table, b.block_table);
+  cp(kv_len, b.kv_len);
+  cp(cu_q, b.cu_q);
+  cp(row_seq, b.row_seq);
+  cp(pos, b.pos);
+  cp(slot, b.slot);
+  return VSK_OK;
+}
+
+static size_t meta_bytes(const BatchHost& b) {
+  return align_up(b.block_table.size() * 4) + align_up(b.kv_len.size() * 4) + align_up(b.cu_q.size() * 4) +
+         3 * align_up(static_cast<size_t>(b.n_rows) * 4);
+}
+
+size_t vsk_batch_device_bytes(const vsk_handle* h) {
+  if (!h || !h->batch_built) return 0;
+  return meta_bytes(h->bh);
+}
+
+int vsk_batch_upload(vsk_handle* h, void* meta_dev, size_t bytes, void* stream) {
+  if (!h) return VSK_E_ARG;
+  if (!h->batch_built) return fail(h, VSK_E_STATE, "no batch built");
+  const BatchHost& b = h->bh;
+  if (!meta_dev || bytes < meta_bytes(b)) return fail(h, VSK_E_ARG, "metadata buffer too small");
+  if (reinterpret_cast<uintptr_t>(meta_dev) % kAlign) return fail(h, VSK_E_ARG, "metadata buffer not aligned");
+  std::vector<uint8_t> staging(meta_bytes(b), 0);
+  size_t o = 0;
+  BatchDev d;
+  uint8_t* base = static_cast<uint8_t*>(meta_dev);
+  auto put = [&](const std::vector<int32_t>& v, const int32_t** dp) {
+    std::memcpy(staging.data() + o, v.data(), v.size() * 4);
+    *dp = reinterpret_cast<const int32_t*>(base + o);
+    o += align_up(std::max<size_t>(v.size(), 1) * 4);
+  };
+  put(b.block_table, &d.block_table);
+  put(b.kv_len, &d.kv_len);
+  put(b.cu_q, &d.cu_q);
+  put(b.row_seq, &d.row_seq);
+  put(b.pos, &d.pos);
+  put(b.slot, &d.slot);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(meta_dev, staging.data(), staging.size(), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);  // staging is a local buffer
+  if (e != hipSuccess) return hip_check(h, e, "metadata upload");
+  d.n_seqs = b.n_seqs;
+  d.n_rows = b.n_rows;
+  d.max_blocks = b.max_blocks;
+  d.max_kv_len = b.max_kv_len;
+  d.max_q_len = b.max_q_len;
+  h->bd = d;
+  h->batch_uploaded = true;
+  return VSK_OK;
+}
+
+// ------------------------------------------------------------------ passes
+size_t vsk_workspace_bytes(const vsk_handle* h, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len) {
+  if (!h || max_rows <= 0 || max_seqs <= 0 || max_kv_len <= 0) return 0;
+  return ws_layout(h->cfg, max_rows, max_seqs, max_kv_len).total;
+}
+
+int vsk_workspace_init(vsk_handle* h, void* ws_dev, size_t bytes, int32_t max_rows, int32_t max_seqs,
+                       int32_t max_kv_len, void* stream) {
+  if (!h || !ws_dev) return VSK_E_ARG;
+  if (max_rows <= 0 || max_seqs <= 0 || max_kv_len <= 0) return fail(h, VSK_E_ARG, "capacity must be positive");
+  if (reinterpret_cast<uintptr_t>(ws_dev) % kAlign) return fail(h, VSK_E_ARG, "workspace not aligned");
+  const WsLayout wl = ws_layout(h->cfg, max_rows, max_seqs, max_kv_len);
+  if (bytes < wl.total) return fail(h, VSK_E_ARG, "workspace smaller than vsk_workspace_bytes()");
+  hipError_t e = launch_fill_zero(ws_dev, wl.total, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_check(h, e, "workspace init");
+  h->ws = static_cast<uint8_t*>(ws_dev);
+  h->ws_bytes = bytes;
+  h->wl = wl;
+  return VSK_OK;
+}
+
+static int pass_common(vsk_handle* h, const int32_t* ids, void* logits, void* ws, size_t ws_bytes) {
+  if (!h) return VSK_E_ARG;
+  if (!h->packed) return fail(h, VSK_E_STATE, "no weights bound");
+  if (!h->pool) return fail(h, VSK_E_STATE, "no KV pool bound");
+  if (!h->batch_uploaded) return fail(h, VSK_E_STATE, "no batch uploaded");
+  if (!ids || !logits || !ws) return fail(h, VSK_E_ARG, "null buffer");
+  if (ws != h->ws || ws_bytes != h->ws_bytes) return fail(h, VSK_E_STATE, "workspace not initialised with this handle");
+  const BatchDev& b = h->bd;
+  if (b.max_kv_len > h->cfg.max_pos) return fail(h, VSK_E_RANGE, "position beyond max_pos");
+  if (b.n_rows > h->wl.max_rows || b.n_seqs > h->wl.max_seqs || b.max_kv_len > h->wl.max_kv_len)
+    return fail(h, VSK_E_ARG, "batch exceeds the workspace capacity");
+  return VSK_OK;
+}
+
+int vsk_decode_step(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int32_t* next_ids_dev, void* ws_dev,
+                    size_t ws_bytes, void* stream) {
+  int st = pass_common(h, ids_dev, logits_dev, ws_dev, ws_bytes);
+  if (st != VSK_OK) return st;
+  if (h->bd.max_q_len != 1) return fail(h, VSK_E_ARG, "decode_step needs one row per sequence");
+  PassArgs a{ids_dev, nullptr, h->bd.n_rows, static_cast<uint16_t*>(logits_dev), next_ids_dev,
+             static_cast<uint8_t*>(ws_dev), h->wl};
+  return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "decode step");
+}
+
+int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logit_rows_dev, int32_t n_logit_rows,
+                      void* logits_dev, int32_t* next_ids_dev, void* ws_dev, size_t ws_bytes, void* stream) {
+  int st = pass_common(h, ids_dev, logits_dev, ws_dev, ws_bytes);
+  if (st != VSK_OK) return st;
+  if (!logit_rows_dev || n_logit_rows < 1 || n_logit_rows > h->bd.n_rows)
+    return fail(h, VSK_E_ARG, "logit rows must be 1..n_rows");
+  PassArgs a{ids_dev, logit_rows_dev, n_logit_rows, static_cast<uint16_t*>(logits_dev), next_ids_dev,
+             static_cast<uint8_t*>(ws_dev), h->wl};
+  return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "prefill chunk");
+}
+
+int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab, int32_t* ids_dev,
+                      void* stream) {
+  if (!logits_dev || !ids_dev || rows < 1 || vocab < 1 || (dtype != 0 && dtype != 1)) return VSK_E_ARG;
+  hipError_t e = launch_argmax_logits(logits_dev, dtype, rows, vocab, ids_dev, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? VSK_OK : VSK_E_HIP;
+}
+
+int vsk_exec_counters(const vsk_handle* h, int64_t* out, int32_t cap) {
+  if (!h || !out) return VSK_E_ARG;
+  for (int i = 0; i < cap && i < 8; ++i) out[i] = h->counters[i];
+  return VSK_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ the pass
+namespace vsk {
+
+hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
+  const vsk_model_cfg& c = h.cfg;
+  const BatchDev& b = h.bd;
+  const WsLayout& wl = pa.wl;
+  const int R = b.n_rows;
+  const int Rg = (R + 15) / 16;
+  const int H = c.hidden, F = c.ffn, d = c.head_dim, Nq = c.n_q_heads * d, Nkv = c.n_kv_heads * d;
+  uint8_t* ws = pa.ws;
+  float* x = reinterpret_cast<float*>(ws + wl.x);
+  uint16_t* act0 = reinterpret_cast<uint16_t*>(ws + wl.act0);
+  uint16_t* act1 = reinterpret_cast<uint16_t*>(ws + wl.act1);
+  uint16_t* q = reinterpret_cast<uint16_t*>(ws + wl.q);
+  const uint8_t* P = h.packed;
+  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+  hipError_t e;
+#define TRY(call)                      \
+  do {                                 \
+    if ((e = (call)) != hipSuccess) return e; \
+  } while (0)
+
+  TRY(launch_embed(reinterpret_cast<const uint16_t*>(P + h.pl.embed), pa.ids, R, H, c.vocab, x, s));
+
+  GemmArgs ga{};
+  ga.part = reinterpret_cast<float*>(ws + wl.gemm_part);
+  ga.cnt = reinterpret_cast<int*>(ws + wl.gemm_cnt);
+  ga.R = R;
+  ga.Rg = Rg;
+  ga.pool = h.pool;
+  ga.n_blocks = h.n_blocks;
+  ga.Hkv = c.n_kv_heads;
+  ga.hd = d;
+  ga.Nq = Nq;
+  ga.Nkv = Nkv;
+  ga.slot = b.slot;
+  ga.pos = b.pos;
+  ga.rope = reinterpret_cast<const float2*>(P + h.pl.rope);
+
+  AttnArgs aa{};
+  aa.q = q;
+  aa.pool = h.pool;
+  aa.n_blocks = h.n_blocks;
+  aa.Hkv = c.n_kv_heads;
+  aa.hd = d;
+  aa.G = c.n_q_heads / c.n_kv_heads;
+  aa.Nq = Nq;
+  aa.block_table = b.block_table;
+  aa.max_blocks = b.max_blocks;
+  aa.row_seq = b.row_seq;
+  aa.pos = b.pos;
+  aa.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d)));
+  aa.max_splits = attn_splits(b.max_kv_len);
+  aa.part_o = reinterpret_cast<float*>(ws + wl.att_o);
+  aa.part_ml = reinterpret_cast<float2*>(ws + wl.att_ml);
+  aa.cnt = reinterpret_cast<int*>(ws + wl.att_cnt);
+  aa.out = act0;
+  aa.out_Rg = Rg;
+
+  const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV);
+  const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID);
+  const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU);
+  const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID);
+
+  for (int l = 0; l < c.n_layers; ++l) {
+    const uint8_t* L = P + h.pl.layer_bytes * l;
+    // attention block
+    TRY(launch_rmsnorm(x, reinterpret_cast<const uint16_t*>(L + h.pl.l.attn_norm), nullptr, R, R, H, c.rms_eps, act0, Rg,
+                       s));
+    ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wqkv);
+    ga.X = reinterpret_cast<const u4*>(act0);
+    ga.Kt = H / 32;
+    ga.N = Nq + 2 * Nkv;
+    ga.out = q;
+    ga.layer = l;
+    TRY(launch_gemm(ga, p_qkv, EPI_QKV, s));
+    aa.layer = l;
+    TRY(launch_attn_decode(aa, R, s));
+    ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);
+    ga.X = reinterpret_cast<const u4*>(act0);
+    ga.Kt = Nq / 32;
+    ga.N = H;
+    ga.x = x;
+    TRY(launch_gemm(ga, p_o, EPI_RESID, s));
+    // MLP block
+    TRY(launch_rmsnorm(x, reinterpret_cast<const uint16_t*>(L + h.pl.l.mlp_norm), nullptr, R, R, H, c.rms_eps, act0, Rg,
+                       s));
+    ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wgu);
+    ga.X = reinterpret_cast<const u4*>(act0);
+    ga.Kt = H / 32;
+    ga.N = 2 * F;
+    ga.out = act1;
+    ga.out_Rg = Rg;
+    TRY(launch_gemm(ga, p_gu, EPI_SWIGLU, s));
+    ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wd);
+    ga.X = reinterpret_cast<const u4*>(act1);
+    ga.Kt = F / 32;
+    ga.N = H;
+    ga.x = x;
+    TRY(launch_gemm(ga, p_d, EPI_RESID, s));
+  }
+  // final norm (gathered logit rows) + lm_head + greedy argmax
+  const int Ro = pa.n_logit_rows;
+  const int Rgo = (Ro + 15) / 16;
+  TRY(launch_rmsnorm(x, reinterpret_cast<const uint16_t*>(P + h.pl.final_norm), pa.logit_rows, Ro, R, H, c.rms_eps, act0,
+                     Rgo, s));
+  const GemmPlan p_lm = plan_gemm(c.vocab, H, Ro, EPI_LOGITS);
+  ga.W = reinterpret_cast<const u4*>(P + h.pl.lm_head);
+  ga.X = reinterpret_cast<const u4*>(act0);
+  ga.Kt = H / 32;
+  ga.N = c.vocab;
+  ga.R = Ro;
+  ga.Rg = Rgo;
+  ga.out = pa.logits;
+  ga.am_val = reinterpret_cast<float*>(ws + wl.am_part);
+  ga.am_idx = reinterpret_cast<int*>(ws + wl.am_part + static_cast<size_t>((c.vocab + 15) / 16) * wl.max_rows * 4);
+  TRY(launch_gemm(ga, p_lm, EPI_LOGITS, s));
+  if (pa.next_ids) TRY(launch_argmax_partials(ga.am_val, ga.am_idx, p_lm.n_groups, Ro, pa.next_ids, s));
+#undef TRY
+  h.counters[0] += 1;
+  h.counters[1] += 4 * c.n_layers + 1;
+  h.counters[2] += c.n_layers;
+  h.counters[3] = aa.max_splits;
+  h.counters[4] = p_d.ks;
+  return hipSuccess;
+}
+
+}  // namespace vsk

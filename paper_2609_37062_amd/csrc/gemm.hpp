@@ -1,0 +1,43 @@
+// Projection kernel interface (see k_gemm.hip).
+#pragma once
+
+#include "internal.hpp"
+
+namespace vsk {
+
+enum { EPI_RESID = 0, EPI_QKV = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+
+struct GemmArgs {
+  const uint32_t __attribute__((ext_vector_type(4)))* W;  // packed tiles
+  const uint32_t __attribute__((ext_vector_type(4)))* X;  // activation frags
+  int Kt;       // K / 32
+  int N;        // output columns
+  int R;        // valid rows
+  int Rg;       // 16-row groups of the X frag buffer
+  int KS;       // K splits across workgroups (set from the plan)
+  float* part;  // split-K partials
+  int* cnt;     // split-K arrival counters [m_tiles * n_groups], zero between launches
+  // epilogue operands
+  float* x;       // RESID: fp32 residual [R][N]
+  uint16_t* out;  // QKV: q [R][Nq]; SWIGLU: frags (out_Rg); LOGITS: logits [R][N]
+  int out_Rg;
+  uint16_t* pool;  // QKV: KV pool
+  int layer, n_blocks, Hkv, hd, Nq, Nkv;
+  const int32_t* slot;
+  const int32_t* pos;
+  const float2* rope;  // [max_pos][hd/2] (cos, sin)
+  float* am_val;       // LOGITS: [n_groups][R]
+  int* am_idx;
+};
+
+struct GemmPlan {
+  int mg = 1;        // 16-row groups per tile
+  int m_tiles = 1;   // tiles along the rows
+  int n_groups = 1;  // workgroups along N
+  int ks = 1;        // K splits across workgroups
+};
+
+GemmPlan plan_gemm(int N, int K, int R, int epi);
+hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s);
+
+}  // namespace vsk

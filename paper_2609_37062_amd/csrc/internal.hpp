@@ -1,0 +1,146 @@
+// Internal declarations shared by the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/vsk.h"
+#include "alloc.hpp"
+
+namespace vsk {
+
+constexpr int kBlock = 16;     // tokens per KV block
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------- packed weights
+// Every matrix W[N][K] is stored as 1 KiB tiles: tile (nt, kt) covers rows
+// 16nt..16nt+15 and columns 32kt..32kt+31 and sits at tile index nt*(K/32)+kt.
+// Inside a tile, lane l (0..63) owns 16 bytes: row l%16, columns
+// 32kt + 8*(l/16) .. +7 -- the A-operand order of the 16x16x32 bf16 MFMA.
+//
+// Row permutations applied while packing:
+//  * QKV (q heads, then k heads, then v heads): inside every q and k head the
+//    packed row 2j holds dim j and 2j+1 holds dim j+d/2, so the rotary pairs
+//    of a head end up in one lane's accumulator registers.
+//  * gate/up: packed row 4u+0,1 = gate rows 2u,2u+1; 4u+2,3 = up rows 2u,2u+1.
+struct LayerOffsets {
+  size_t attn_norm, mlp_norm, wqkv, wo, wgu, wd;
+};
+
+struct PackedLayout {
+  size_t layer_bytes = 0;
+  LayerOffsets l;          // offsets inside one layer record
+  size_t head_base = 0;    // start of the global record
+  size_t final_norm = 0, embed = 0, lm_head = 0, rope = 0;  // absolute offsets
+  size_t total = 0;
+};
+
+PackedLayout packed_layout(const vsk_model_cfg& c);
+
+// ---------------------------------------------------------------- activation frags
+// Activations feeding a projection are bf16 X[R][K] stored in "frag" order:
+// chunk (kt, g) = 1 KiB at ((kt*Rg + g) * 1024) bytes, Rg = ceil(R/16); lane l
+// owns X[16g + l%16][32kt + 8*(l/16) .. +7] -- the B-operand order of the
+// 16x16x32 MFMA.  Padding rows (R..16*Rg) are kept at zero.
+__host__ __device__ inline size_t frag_index(int row, int k, int Rg) {
+  const int kt = k >> 5, kk = k & 31;
+  const int lane = (row & 15) + 16 * (kk >> 3);
+  return ((static_cast<size_t>(kt) * Rg + (row >> 4)) * 64 + lane) * 8 + (kk & 7);
+}
+
+// ---------------------------------------------------------------- KV pool
+// Pool = [L][2][n_blocks][n_kv_heads][block of 16 tokens x head_dim] bf16.
+// K block: chunk c = dim/32 (1 KiB each): lane t + 16*((dim%32)/8), elem dim%8
+//          (A-operand order of the 16x16x32 MFMA for S = K q).
+// V block: chunk c = dim/16 (512 B each): lane dim%16 + 16*(t/4), elem t%4
+//          (A-operand order of the 16x16x16 MFMA for O^T = V^T P^T).
+__host__ __device__ inline int kv_k_index(int t, int e) {
+  const int c = e >> 5, ee = e & 31;
+  return ((c * 64) + t + 16 * (ee >> 3)) * 8 + (ee & 7);
+}
+__host__ __device__ inline int kv_v_index(int t, int e) {
+  const int c = e >> 4;
+  return ((c * 64) + (e & 15) + 16 * (t >> 2)) * 4 + (t & 3);
+}
+
+// ---------------------------------------------------------------- device batch
+struct BatchDev {
+  int32_t n_seqs = 0, n_rows = 0, max_blocks = 0, max_kv_len = 0, max_q_len = 0;
+  const int32_t* block_table = nullptr;  // [n_seqs][max_blocks]
+  const int32_t* kv_len = nullptr;
+  const int32_t* cu_q = nullptr;
+  const int32_t* row_seq = nullptr;
+  const int32_t* pos = nullptr;
+  const int32_t* slot = nullptr;
+};
+
+// ---------------------------------------------------------------- workspace
+struct WsLayout {
+  int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
+  size_t x, act0, act1, q, att_o, att_ml, att_cnt, gemm_part, gemm_cnt, am_part, counters_begin,
+      counters_end, total;
+};
+
+struct Handle {
+  vsk_model_cfg cfg{};
+  std::string err;
+  // weights
+  uint8_t* packed = nullptr;
+  size_t packed_bytes = 0;
+  PackedLayout pl;
+  // kv
+  uint16_t* pool = nullptr;
+  int32_t n_blocks = 0;
+  BlockAllocator alloc;
+  bool alloc_ready = false;
+  // batch
+  BatchHost bh;
+  bool batch_built = false;
+  BatchDev bd;
+  bool batch_uploaded = false;
+  // workspace
+  uint8_t* ws = nullptr;
+  size_t ws_bytes = 0;
+  WsLayout wl;
+  // counters
+  int64_t counters[8] = {0};
+};
+
+WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len);
+
+// attention split: blocks per split-K work item
+constexpr int kAttnBlocksPerSplit = 8;
+inline int attn_splits(int kv_len) {
+  const int nb = (kv_len + kBlock - 1) / kBlock;
+  return (nb + kAttnBlocksPerSplit - 1) / kAttnBlocksPerSplit;
+}
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error.
+hipError_t launch_pack_matrix(const uint16_t* src, uint16_t* dst, int N, int K, int perm_kind, int head_dim,
+                              int n_rope_rows, hipStream_t s);
+hipError_t launch_copy_bf16(const uint16_t* src, uint16_t* dst, size_t n, hipStream_t s);
+hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s);
+hipError_t launch_kv_write(const Handle& h, int layer, const int32_t* slots, int n, const uint16_t* k,
+                           const uint16_t* v, hipStream_t s);
+hipError_t launch_kv_read(const Handle& h, int layer, const int32_t* slots, int n, uint16_t* k, uint16_t* v,
+                          hipStream_t s);
+hipError_t launch_argmax_logits(const void* logits, int dtype, int rows, int vocab, int32_t* ids, hipStream_t s);
+
+struct PassArgs {
+  const int32_t* ids;
+  const int32_t* logit_rows;  // nullable = every row
+  int32_t n_logit_rows;
+  uint16_t* logits;
+  int32_t* next_ids;
+  uint8_t* ws;
+  WsLayout wl;
+};
+hipError_t run_pass(Handle& h, const PassArgs& a, hipStream_t s);
+
+}  // namespace vsk

@@ -1,0 +1,331 @@
+// Weight-streaming projections on the matrix cores, with fused epilogues.
+//
+// Y[R][N] = X[R][K] W[N][K]^T for the rows of a pass.  Below the ridge point
+// the pass is bound by reading W once (paper, appendix "The Switching
+// Thresholds from the Roofline": for M rows the arithmetic intensity of a
+// weight-stationary decode GEMM is M flops per weight byte), so the kernel is
+// organised around streaming W: every wave reads whole 1 KiB tiles with one
+// 16-byte load per lane, several tiles in flight, and feeds them straight
+// to v_mfma_f32_16x16x32_bf16 with W as the A operand (16 output columns)
+// and a 16-row group of X as the B operand.  K is split across the waves of
+// a workgroup (reduced in LDS) and, for narrow N, across workgroups (the last
+// workgroup to finish sums the partials in split order, so results do not
+// depend on scheduling).
+//
+// Epilogues (the tensors stored between kernels are rounded to bf16):
+//   RESID  : x[r][n] += y                      (O and down projections)
+//   QKV    : rotary on q,k; q -> bf16 buffer; k,v -> this layer's KV slot
+//            (Invariant 1: every row writes its own-layer KV)
+//   SWIGLU : a = silu(gate) * up -> bf16 frags for the down projection
+//            (the SwiGLU product of Algorithm 1's RUN cohort step)
+//   LOGITS : bf16 logits + per-workgroup (max, lowest index) for greedy argmax
+#include <climits>
+
+#include "dev.hpp"
+#include "gemm.hpp"
+
+namespace vsk {
+
+__device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v)); }
+
+template <int MG, int NT, int WN, int WK, int PF, int EPI>
+__global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int s_last;
+  __shared__ float s_amv[WN][MG][16];
+  __shared__ int s_ami[WN][MG][16];
+
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int wn = w % WN, wk = w / WN;
+  const int ng = blockIdx.x, ks = blockIdx.y, mt = blockIdx.z;
+  const int n_tiles = a.N >> 4;
+  const int nt0 = (ng * WN + wn) * NT;
+  const int g0 = mt * MG;
+  const int kt_lo = static_cast<int>(static_cast<long>(ks) * a.Kt / a.KS);
+  const int kt_hi = static_cast<int>(static_cast<long>(ks + 1) * a.Kt / a.KS);
+
+  f32x4 acc[NT][MG];
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+#pragma unroll
+    for (int g = 0; g < MG; ++g) acc[j][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  bool tvalid[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) tvalid[j] = (nt0 + j) < n_tiles;
+  bool gvalid[MG];
+#pragma unroll
+  for (int g = 0; g < MG; ++g) gvalid[g] = (g0 + g) < a.Rg;
+
+  const int first = kt_lo + wk;
+  const int n_it = first < kt_hi ? (kt_hi - first + WK - 1) / WK : 0;
+  const u32x4* Wbase = a.W + lane;
+  const u32x4* Xbase = a.X + lane;
+
+  u32x4 fa[PF][NT], fb[PF][MG];
+  auto load = [&](u32x4 (&ra)[NT], u32x4 (&rb)[MG], int kt) {
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+      ra[j] = tvalid[j] ? Wbase[(static_cast<size_t>(nt0 + j) * a.Kt + kt) * 64] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int g = 0; g < MG; ++g)
+      rb[g] = gvalid[g] ? Xbase[(static_cast<size_t>(kt) * a.Rg + g0 + g) * 64] : u32x4{0u, 0u, 0u, 0u};
+  };
+
+#pragma unroll
+  for (int st = 0; st < PF; ++st)
+    if (st < n_it) load(fa[st], fb[st], first + st * WK);
+
+  for (int it = 0; it < n_it; it += PF) {
+#pragma unroll
+    for (int st = 0; st < PF; ++st) {
+      if (it + st < n_it) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
+        const int nx = it + st + PF;
+        if (nx < n_it) load(fa[st], fb[st], first + nx * WK);
+      }
+    }
+  }
+
+  // ---- reduce the K-split waves of this workgroup (fixed order)
+  if constexpr (WK > 1) {
+    f32x4* red = reinterpret_cast<f32x4*>(smem);
+    if (wk > 0) {
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int g = 0; g < MG; ++g) red[((((wk - 1) * WN + wn) * NT + j) * MG + g) * 64 + lane] = acc[j][g];
+    }
+    __syncthreads();
+    if (wk == 0) {
+      for (int w2 = 1; w2 < WK; ++w2)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int g = 0; g < MG; ++g) acc[j][g] += red[((((w2 - 1) * WN + wn) * NT + j) * MG + g) * 64 + lane];
+    }
+  }
+
+  // ---- split-K across workgroups: the last arrival sums the partials in split order
+  if (a.KS > 1) {
+    f32x4* part = reinterpret_cast<f32x4*>(a.part);
+    const size_t tile = static_cast<size_t>(mt) * gridDim.x + ng;
+    if (wk == 0) {
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int g = 0; g < MG; ++g)
+          part[((((tile * a.KS + ks) * WN + wn) * NT + j) * MG + g) * 64 + lane] = acc[j][g];
+    }
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = (atomicAdd(&a.cnt[tile], 1) == a.KS - 1);
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    if (wk == 0) {
+      for (int s = 0; s < a.KS; ++s)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int g = 0; g < MG; ++g) {
+            const f32x4 p = part[((((tile * a.KS + s) * WN + wn) * NT + j) * MG + g) * 64 + lane];
+            acc[j][g] = (s == 0) ? p : acc[j][g] + p;
+          }
+    }
+    if (threadIdx.x == 0) a.cnt[tile] = 0;
+  }
+
+  // ---- epilogues (waves with wk == 0 hold the sums)
+  const int rsub = lane & 15;
+  const int nq = 4 * (lane >> 4);
+  if constexpr (EPI == EPI_RESID) {
+    if (wk == 0) {
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        if (!tvalid[j]) continue;
+        const int n0 = 16 * (nt0 + j) + nq;
+#pragma unroll
+        for (int g = 0; g < MG; ++g) {
+          const int row = 16 * (g0 + g) + rsub;
+          if (row >= a.R) continue;
+          float4* px = reinterpret_cast<float4*>(a.x + static_cast<size_t>(row) * a.N + n0);
+          float4 v = *px;
+          v.x += acc[j][g][0];
+          v.y += acc[j][g][1];
+          v.z += acc[j][g][2];
+          v.w += acc[j][g][3];
+          *px = v;
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    if (wk == 0) {
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        if (!tvalid[j]) continue;
+        const int u = 4 * (nt0 + j) + (lane >> 4);  // output columns 2u, 2u+1
+#pragma unroll
+        for (int g = 0; g < MG; ++g) {
+          const int row = 16 * (g0 + g) + rsub;
+          if (row >= a.R) continue;
+          const float a0 = silu_f(acc[j][g][0]) * acc[j][g][2];
+          const float a1 = silu_f(acc[j][g][1]) * acc[j][g][3];
+          *reinterpret_cast<uint32_t*>(a.out + frag_index(row, 2 * u, a.out_Rg)) = pack_bf2(a0, a1);
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_QKV) {
+    if (wk == 0) {
+      const int hd = a.hd, half = hd >> 1;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        if (!tvalid[j]) continue;
+        const int n0 = 16 * (nt0 + j) + nq;
+#pragma unroll
+        for (int g = 0; g < MG; ++g) {
+          const int row = 16 * (g0 + g) + rsub;
+          if (row >= a.R) continue;
+          const f32x4 v = acc[j][g];
+          const int sl = a.slot[row];
+          const int blk = sl >> 4, t = sl & 15;
+          if (n0 < a.Nq + a.Nkv) {
+            const int ph = n0 % hd;          // packed row inside the head (multiple of 4)
+            const int hb = n0 - ph;          // first packed row of the head
+            const int j0 = ph >> 1;          // dims j0, j0+half, j0+1, j0+1+half
+            const int p = a.pos[row];
+            const float2 cs0 = a.rope[static_cast<size_t>(p) * half + j0];
+            const float2 cs1 = a.rope[static_cast<size_t>(p) * half + j0 + 1];
+            const float y0 = v[0] * cs0.x - v[1] * cs0.y;
+            const float y1 = v[1] * cs0.x + v[0] * cs0.y;
+            const float y2 = v[2] * cs1.x - v[3] * cs1.y;
+            const float y3 = v[3] * cs1.x + v[2] * cs1.y;
+            if (n0 < a.Nq) {
+              uint16_t* q = a.out + static_cast<size_t>(row) * a.Nq + hb;
+              q[j0] = f2bf(y0);
+              q[j0 + half] = f2bf(y1);
+              q[j0 + 1] = f2bf(y2);
+              q[j0 + 1 + half] = f2bf(y3);
+            } else {
+              const int hk = (hb - a.Nq) / hd;
+              uint16_t* kb = a.pool + ((((static_cast<size_t>(a.layer) * 2 + 0) * a.n_blocks + blk) * a.Hkv + hk) *
+                                       kBlock * hd);
+              kb[kv_k_index(t, j0)] = f2bf(y0);
+              kb[kv_k_index(t, j0 + half)] = f2bf(y1);
+              kb[kv_k_index(t, j0 + 1)] = f2bf(y2);
+              kb[kv_k_index(t, j0 + 1 + half)] = f2bf(y3);
+            }
+          } else {
+            const int nv = n0 - a.Nq - a.Nkv;
+            const int hk = nv / hd, e0 = nv % hd;
+            uint16_t* vb = a.pool + ((((static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks + blk) * a.Hkv + hk) *
+                                     kBlock * hd);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) vb[kv_v_index(t, e0 + r)] = f2bf(v[r]);
+          }
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_LOGITS) {
+    if (wk == 0) {
+#pragma unroll
+      for (int g = 0; g < MG; ++g) {
+        const int row = 16 * (g0 + g) + rsub;
+        float bv = -INFINITY;
+        int bi = INT_MAX;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          if (!tvalid[j] || row >= a.R) continue;
+          const int n0 = 16 * (nt0 + j) + nq;
+          const f32x4 v = acc[j][g];
+          uint2 packed;
+          packed.x = pack_bf2(v[0], v[1]);
+          packed.y = pack_bf2(v[2], v[3]);
+          *reinterpret_cast<uint2*>(a.out + static_cast<size_t>(row) * a.N + n0) = packed;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (!(v[r] != v[r])) am_merge(bv, bi, v[r], n0 + r);
+        }
+        // lanes l, l^16, l^32, l^48 hold the same row
+#pragma unroll
+        for (int m = 16; m <= 32; m <<= 1) {
+          const float v2 = shfl_xor(bv, m);
+          const int i2 = shfl_xor(bi, m);
+          am_merge(bv, bi, v2, i2);
+        }
+        if (lane < 16) {
+          s_amv[wn][g][lane] = bv;
+          s_ami[wn][g][lane] = bi;
+        }
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < MG * 16) {
+      const int g = threadIdx.x >> 4, l = threadIdx.x & 15;
+      float bv = s_amv[0][g][l];
+      int bi = s_ami[0][g][l];
+#pragma unroll
+      for (int w2 = 1; w2 < WN; ++w2) am_merge(bv, bi, s_amv[w2][g][l], s_ami[w2][g][l]);
+      const int row = 16 * (g0 + g) + l;
+      if (row < a.R) {
+        a.am_val[static_cast<size_t>(ng) * a.R + row] = bv;
+        a.am_idx[static_cast<size_t>(ng) * a.R + row] = bi;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launcher
+template <int MG, int NT, int WN, int WK, int PF, int EPI>
+static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, hipStream_t s) {
+  const int n_groups = (a.N / 16 + NT * WN - 1) / (NT * WN);
+  dim3 grid(n_groups, a.KS, m_tiles);
+  const size_t smem = (WK > 1 ? (WK - 1) : 0) * WN * NT * MG * 64 * sizeof(f32x4);
+  hipLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI>), grid, dim3(64 * WN * WK), smem, s, a);
+  return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t launch_epi(const GemmArgs& a, int mg, int m_tiles, hipStream_t s) {
+  switch (mg) {
+    case 1: return launch_cfg<1, 1, 1, 8, 4, EPI>(a, m_tiles, s);
+    case 2: return launch_cfg<2, 1, 1, 8, 4, EPI>(a, m_tiles, s);
+    case 4: return launch_cfg<4, 2, 2, 2, 2, EPI>(a, m_tiles, s);
+    default: return launch_cfg<8, 2, 2, 2, 2, EPI>(a, m_tiles, s);
+  }
+}
+
+GemmPlan plan_gemm(int N, int K, int R, int epi) {
+  GemmPlan p;
+  const int Rg = (R + 15) / 16;
+  p.mg = Rg <= 1 ? 1 : Rg <= 2 ? 2 : Rg <= 4 ? 4 : 8;
+  p.m_tiles = (Rg + p.mg - 1) / p.mg;
+  const int rows_per_group = p.mg <= 2 ? 16 : 64;
+  p.n_groups = (N / 16 * 16 + rows_per_group - 1) / rows_per_group;
+  const int Kt = K / 32;
+  const int wk = p.mg <= 2 ? 8 : 2;
+  int ks = 1;
+  if (epi != EPI_LOGITS) {
+    const int target = 512;
+    const int have = p.n_groups * p.m_tiles;
+    while (have * ks < target && Kt / (ks * 2) >= wk * 2) ks *= 2;
+  }
+  p.ks = ks;
+  return p;
+}
+
+hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s) {
+  a.KS = p.ks;
+  switch (epi) {
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, p.mg, p.m_tiles, s);
+    case EPI_QKV: return launch_epi<EPI_QKV>(a, p.mg, p.m_tiles, s);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p.mg, p.m_tiles, s);
+    default: return launch_epi<EPI_LOGITS>(a, p.mg, p.m_tiles, s);
+  }
+}
+
+}  // namespace vsk

@@ -1,0 +1,265 @@
+// Small kernels of the pass: embedding gather, RMSNorm into frags, greedy
+// argmax, weight repacking, KV scatter/gather, workspace clearing.
+#include <climits>
+#include <cmath>
+
+#include "dev.hpp"
+#include "misc.hpp"
+
+namespace vsk {
+
+// ---------------------------------------------------------------- embedding
+// x[r][:] = float(E[ids[r]][:]); one workgroup per row, 8 columns per thread.
+// Token ids outside [0, V) give a zero row.
+__global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, const int32_t* __restrict__ ids,
+                                               int H, int V, float* __restrict__ x) {
+  const int r = blockIdx.x;
+  const int id = ids[r];
+  if (id < 0 || id >= V) {
+    for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4)
+      *reinterpret_cast<float4*>(x + static_cast<size_t>(r) * H + c) = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
+  const size_t base = static_cast<size_t>(id) * H;
+  for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(E + base + c);
+    float4* dst = reinterpret_cast<float4*>(x + static_cast<size_t>(r) * H + c);
+    dst[0] = make_float4(bf2f(v[0] & 0xffffu), bf2f(v[0] >> 16), bf2f(v[1] & 0xffffu), bf2f(v[1] >> 16));
+    dst[1] = make_float4(bf2f(v[2] & 0xffffu), bf2f(v[2] >> 16), bf2f(v[3] & 0xffffu), bf2f(v[3] >> 16));
+  }
+}
+
+hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, float* x, hipStream_t s) {
+  hipLaunchKernelGGL(k_embed, dim3(R), dim3(256), 0, s, E, ids, H, V, x);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- RMSNorm
+// out = bf16(x * 1/sqrt(mean(x^2) + eps) * g) written as frags; output row r
+// reads input row gather[r] (or r).  Rows R..16*Rg of the output are zeroed.
+// A gathered index outside [0, R_in) gives a zero row.
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, const uint16_t* __restrict__ g,
+                                                 const int32_t* __restrict__ gather, int R, int R_in, int H,
+                                                 float eps, uint16_t* __restrict__ out, int Rg) {
+  __shared__ float s_red[8];
+  const int r = blockIdx.x;
+  const int src = r < R ? (gather ? gather[r] : r) : -1;
+  if (src < 0 || src >= R_in) {
+    for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8)
+      *reinterpret_cast<u32x4*>(out + frag_index(r, c, Rg)) = u32x4{0u, 0u, 0u, 0u};
+    return;
+  }
+  const float* xr = x + static_cast<size_t>(src) * H;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(xr + c);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss += shfl_xor(ss, m);
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) tot += s_red[i];
+  const float inv = 1.0f / sqrtf(tot / static_cast<float>(H) + eps);
+  for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8) {
+    const float4 a = *reinterpret_cast<const float4*>(xr + c);
+    const float4 b = *reinterpret_cast<const float4*>(xr + c + 4);
+    const u32x4 gv = *reinterpret_cast<const u32x4*>(g + c);
+    u32x4 o;
+    o[0] = pack_bf2(a.x * inv * bf2f(gv[0] & 0xffffu), a.y * inv * bf2f(gv[0] >> 16));
+    o[1] = pack_bf2(a.z * inv * bf2f(gv[1] & 0xffffu), a.w * inv * bf2f(gv[1] >> 16));
+    o[2] = pack_bf2(b.x * inv * bf2f(gv[2] & 0xffffu), b.y * inv * bf2f(gv[2] >> 16));
+    o[3] = pack_bf2(b.z * inv * bf2f(gv[3] & 0xffffu), b.w * inv * bf2f(gv[3] >> 16));
+    *reinterpret_cast<u32x4*>(out + frag_index(r, c, Rg)) = o;
+  }
+}
+
+hipError_t launch_rmsnorm(const float* x, const uint16_t* g, const int32_t* gather, int R, int R_in, int H,
+                          float eps, uint16_t* out, int Rg, hipStream_t s) {
+  hipLaunchKernelGGL(k_rmsnorm, dim3(16 * Rg), dim3(256), 0, s, x, g, gather, R, R_in, H, eps, out, Rg);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- argmax
+__device__ inline void block_am_reduce(float& bv, int& bi) {
+  __shared__ float s_v[16];
+  __shared__ int s_i[16];
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float v2 = shfl_xor(bv, m);
+    const int i2 = shfl_xor(bi, m);
+    am_merge(bv, bi, v2, i2);
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    s_v[w] = bv;
+    s_i[w] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < (int)(blockDim.x >> 6); ++i) am_merge(bv, bi, s_v[i], s_i[i]);
+  }
+}
+
+// ids[r] from the per-workgroup partials of the lm_head epilogue ([G][R]).
+__global__ __launch_bounds__(256) void k_argmax_partials(const float* __restrict__ pv, const int* __restrict__ pi,
+                                                         int n_groups, int R, int32_t* __restrict__ ids) {
+  const int r = blockIdx.x;
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  for (int g = threadIdx.x; g < n_groups; g += blockDim.x)
+    am_merge(bv, bi, pv[static_cast<size_t>(g) * R + r], pi[static_cast<size_t>(g) * R + r]);
+  block_am_reduce(bv, bi);
+  if (threadIdx.x == 0) ids[r] = (bi == INT_MAX) ? 0 : bi;
+}
+
+hipError_t launch_argmax_partials(const float* pv, const int* pi, int n_groups, int R, int32_t* ids,
+                                  hipStream_t s) {
+  hipLaunchKernelGGL(k_argmax_partials, dim3(R), dim3(256), 0, s, pv, pi, n_groups, R, ids);
+  return hipGetLastError();
+}
+
+template <int DT>
+__global__ __launch_bounds__(1024) void k_argmax_logits(const void* __restrict__ logits, int vocab,
+                                                        int32_t* __restrict__ ids) {
+  const int r = blockIdx.x;
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  for (int j = threadIdx.x; j < vocab; j += blockDim.x) {
+    float v;
+    if constexpr (DT == 0)
+      v = bf2f(reinterpret_cast<const uint16_t*>(logits)[static_cast<size_t>(r) * vocab + j]);
+    else
+      v = reinterpret_cast<const float*>(logits)[static_cast<size_t>(r) * vocab + j];
+    if (!(v != v)) am_merge(bv, bi, v, j);
+  }
+  block_am_reduce(bv, bi);
+  if (threadIdx.x == 0) ids[r] = (bi == INT_MAX) ? 0 : bi;
+}
+
+hipError_t launch_argmax_logits(const void* logits, int dtype, int rows, int vocab, int32_t* ids, hipStream_t s) {
+  if (dtype == 0)
+    hipLaunchKernelGGL(k_argmax_logits<0>, dim3(rows), dim3(1024), 0, s, logits, vocab, ids);
+  else
+    hipLaunchKernelGGL(k_argmax_logits<1>, dim3(rows), dim3(1024), 0, s, logits, vocab, ids);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- weight packing
+// dst tile order (see internal.hpp).  Logical source rows come from up to
+// three matrices stacked vertically (n0, n1, n2 rows); perm_kind selects the
+// packed->logical row map: 0 identity, 1 rotary pairing in the first
+// n_rope_rows rows (per head of head_dim), 2 gate/up interleave (n0 = n1 = F).
+__device__ inline int packed_to_logical(int p, int perm_kind, int head_dim, int n_rope_rows, int F) {
+  if (perm_kind == 1 && p < n_rope_rows) {
+    const int ph = p % head_dim;
+    const int dim = (ph & 1) ? (ph >> 1) + head_dim / 2 : (ph >> 1);
+    return p - ph + dim;
+  }
+  if (perm_kind == 2) {
+    const int u = p >> 2, r = p & 3;
+    return r < 2 ? 2 * u + r : F + 2 * u + (r - 2);
+  }
+  return p;
+}
+
+__global__ __launch_bounds__(256) void k_pack(const uint16_t* __restrict__ s0, const uint16_t* __restrict__ s1,
+                                              const uint16_t* __restrict__ s2, int n0, int n1, int N, int K,
+                                              int perm_kind, int head_dim, int n_rope_rows,
+                                              uint16_t* __restrict__ dst) {
+  const size_t chunk = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;  // 16-byte chunk
+  const int Kt = K / 32;
+  const size_t n_chunks = static_cast<size_t>(N) * K / 8;
+  if (chunk >= n_chunks) return;
+  const size_t tile = chunk / 64;
+  const int lane = static_cast<int>(chunk % 64);
+  const int nt = static_cast<int>(tile / Kt), kt = static_cast<int>(tile % Kt);
+  const int p = 16 * nt + (lane & 15);
+  const int k0 = 32 * kt + 8 * (lane >> 4);
+  int lr = packed_to_logical(p, perm_kind, head_dim, n_rope_rows, n0);
+  const uint16_t* src;
+  if (lr < n0) {
+    src = s0;
+  } else if (lr < n0 + n1) {
+    src = s1;
+    lr -= n0;
+  } else {
+    src = s2;
+    lr -= n0 + n1;
+  }
+  *reinterpret_cast<u32x4*>(dst + chunk * 8) = *reinterpret_cast<const u32x4*>(src + static_cast<size_t>(lr) * K + k0);
+}
+
+hipError_t launch_pack(const uint16_t* s0, const uint16_t* s1, const uint16_t* s2, int n0, int n1, int N, int K,
+                       int perm_kind, int head_dim, int n_rope_rows, uint16_t* dst, hipStream_t s) {
+  const size_t n_chunks = static_cast<size_t>(N) * K / 8;
+  const unsigned blocks = static_cast<unsigned>((n_chunks + 255) / 256);
+  hipLaunchKernelGGL(k_pack, dim3(blocks), dim3(256), 0, s, s0, s1, s2, n0, n1, N, K, perm_kind, head_dim,
+                     n_rope_rows, dst);
+  return hipGetLastError();
+}
+
+__global__ void k_copy16(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst, size_t n) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
+hipError_t launch_copy_bf16(const uint16_t* src, uint16_t* dst, size_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_copy16, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+__global__ void k_zero(uint32_t* __restrict__ dst, size_t n) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = 0u;
+}
+
+hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s) {
+  const size_t n = bytes / 4;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, s,
+                     static_cast<uint32_t*>(dst), n);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- KV scatter / gather
+// One thread per (token, kv head, dim); logical layout [n][Hkv][hd].
+template <bool WRITE>
+__global__ __launch_bounds__(256) void k_kv_move(uint16_t* __restrict__ pool, int layer, int n_blocks, int Hkv,
+                                                 int hd, const int32_t* __restrict__ slots, int n,
+                                                 uint16_t* __restrict__ k, uint16_t* __restrict__ v) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const size_t total = static_cast<size_t>(n) * Hkv * hd;
+  if (i >= total) return;
+  const int e = static_cast<int>(i % hd);
+  const int hk = static_cast<int>((i / hd) % Hkv);
+  const int tok = static_cast<int>(i / (static_cast<size_t>(hd) * Hkv));
+  const int sl = slots[tok];
+  if (sl < 0 || sl >= n_blocks * kBlock) return;  // slots outside the pool are ignored
+  const int blk = sl >> 4, t = sl & 15;
+  const size_t kb = (((static_cast<size_t>(layer) * 2 + 0) * n_blocks + blk) * Hkv + hk) * kBlock * hd;
+  const size_t vb = (((static_cast<size_t>(layer) * 2 + 1) * n_blocks + blk) * Hkv + hk) * kBlock * hd;
+  if (WRITE) {
+    pool[kb + kv_k_index(t, e)] = k[i];
+    pool[vb + kv_v_index(t, e)] = v[i];
+  } else {
+    k[i] = pool[kb + kv_k_index(t, e)];
+    v[i] = pool[vb + kv_v_index(t, e)];
+  }
+}
+
+hipError_t launch_kv_move(bool write, uint16_t* pool, int layer, int n_blocks, int Hkv, int hd,
+                          const int32_t* slots, int n, uint16_t* k, uint16_t* v, hipStream_t s) {
+  const size_t total = static_cast<size_t>(n) * Hkv * hd;
+  if (total == 0) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>((total + 255) / 256);
+  if (write)
+    hipLaunchKernelGGL(k_kv_move<true>, dim3(blocks), dim3(256), 0, s, pool, layer, n_blocks, Hkv, hd, slots, n, k, v);
+  else
+    hipLaunchKernelGGL(k_kv_move<false>, dim3(blocks), dim3(256), 0, s, pool, layer, n_blocks, Hkv, hd, slots, n, k,
+                       v);
+  return hipGetLastError();
+}
+
+}  // namespace vsk

@@ -1,0 +1,18 @@
+// Small-kernel launchers (see k_misc.hip).
+#pragma once
+
+#include "internal.hpp"
+
+namespace vsk {
+
+hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, float* x, hipStream_t s);
+hipError_t launch_rmsnorm(const float* x, const uint16_t* g, const int32_t* gather, int R, int R_in, int H,
+                          float eps, uint16_t* out, int Rg, hipStream_t s);
+hipError_t launch_argmax_partials(const float* pv, const int* pi, int n_groups, int R, int32_t* ids,
+                                  hipStream_t s);
+hipError_t launch_pack(const uint16_t* s0, const uint16_t* s1, const uint16_t* s2, int n0, int n1, int N, int K,
+                       int perm_kind, int head_dim, int n_rope_rows, uint16_t* dst, hipStream_t s);
+hipError_t launch_kv_move(bool write, uint16_t* pool, int layer, int n_blocks, int Hkv, int hd,
+                          const int32_t* slots, int n, uint16_t* k, uint16_t* v, hipStream_t s);
+
+}  // namespace vsk

@@ -1,0 +1,124 @@
+"""Device parity against the oracle at sizes the oracle finishes in seconds.
+
+Every device call goes through the C ABI (paper_2609_37062_amd.vsk); the
+oracle is the float64 CPU statement in oracle/.
+"""
+import copy
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from workloads.configs import ModelCfg, decode_workload, mixed_workload, workload  # noqa: E402
+
+from helpers import compare_logits, oracle_run  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+# two layers, GQA group 4, head_dim 128: several tiles along every matrix,
+# ragged row groups and several attention splits
+MID = ModelCfg("mid-2L", n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=128, ffn=1536,
+               vocab=2048, rope_theta=500000.0)
+
+
+def _run(w, **kw):
+    from paper_2609_37062_amd.runner import DeviceRun
+    print(f"[gpu] {w.name} seqs={w.n_seqs} rows={w.n_rows}", flush=True)
+    kw.setdefault("poison_pool", True)
+    d = DeviceRun(w, **kw)
+    d.step()
+    lg, ids = d.results()
+    return d, lg, ids
+
+
+def _check(w, lg, ids, subset=None, **kw):
+    out, kv, sub, idx, dev_rows = oracle_run(w, subset, **kw)
+    return compare_logits(lg[dev_rows], ids[dev_rows], out["z"]), out, kv, sub, idx
+
+
+def test_config1_tiny_decode():
+    w = workload(1)
+    d, lg, ids = _run(w)
+    st, out, kv, sub, idx = _check(w, lg, ids)
+    # new K,V of every row at every layer (Invariant 1)
+    for l in range(w.model.n_layers):
+        K, V = d.read_kv(l, sub["slot"])
+        Ko, Vo = kv.read(l, sub["slot"])
+        assert np.abs(K - Ko).max() <= 2 ** -7 * np.abs(Ko).max()
+        assert np.abs(V - Vo).max() <= 2 ** -7 * np.abs(Vo).max()
+    print(st)
+
+
+@pytest.mark.parametrize("B", [1, 20, 70, 130])
+def test_mid_decode_batches(B):
+    ctx = np.random.default_rng(B).integers(0, 300, size=B)
+    w = decode_workload(MID, ctx, seed=3, name=f"mid-decode-b{B}")
+    d, lg, ids = _run(w)
+    sub = None if B <= 20 else list(range(0, B, max(1, B // 12)))
+    st, *_ = _check(w, lg, ids, sub)
+    print(st)
+
+
+def test_mid_shared_prefix():
+    ctx = 256 + np.random.default_rng(5).integers(3, 40, size=12)
+    w = decode_workload(MID, ctx, seed=4, shared=256, name="mid-shared")
+    d, lg, ids = _run(w)
+    st, *_ = _check(w, lg, ids)
+    print(st)
+
+
+def test_mid_mixed_prefill_decode():
+    ctx = np.random.default_rng(6).integers(10, 200, size=5)
+    w = mixed_workload(MID, n_pre=2, plen=45, ctx=ctx, seed=7, name="mid-mixed")
+    d, lg, ids = _run(w)
+    st, out, kv, sub, idx = _check(w, lg, ids)
+    # every prefill row wrote its own K,V at every layer
+    for l in range(MID.n_layers):
+        K, V = d.read_kv(l, sub["slot"])
+        Ko, Vo = kv.read(l, sub["slot"])
+        assert np.abs(K - Ko).max() <= 0.05 and np.abs(V - Vo).max() <= 0.05
+    print(st)
+
+
+def test_replay_is_idempotent_and_deterministic():
+    ctx = np.random.default_rng(8).integers(20, 400, size=24)
+    w = decode_workload(MID, ctx, seed=9)
+    d, lg1, ids1 = _run(w)
+    K1, V1 = d.read_kv(1, d.eng.batch_host()["slot"])
+    for _ in range(3):
+        d.step()
+    lg2, ids2 = d.results()
+    K2, V2 = d.read_kv(1, d.eng.batch_host()["slot"])
+    np.testing.assert_array_equal(lg1, lg2)
+    np.testing.assert_array_equal(ids1, ids2)
+    np.testing.assert_array_equal(K1, K2)
+    np.testing.assert_array_equal(V1, V2)
+
+
+def test_block_permutation_is_bitwise_invariant():
+    ctx = np.random.default_rng(10).integers(20, 300, size=9)
+    w = decode_workload(MID, ctx, seed=11)
+    _, lg1, ids1 = _run(w)
+    w2 = copy.deepcopy(w)
+    perm = np.random.default_rng(12).permutation(w.n_pool_blocks)
+    for s in w2.seqs:
+        s.blocks = [int(perm[b]) for b in s.blocks]
+    _, lg2, ids2 = _run(w2)
+    np.testing.assert_array_equal(lg1, lg2)
+    np.testing.assert_array_equal(ids1, ids2)
+
+
+def test_batch_row_order_is_bitwise_invariant():
+    ctx = np.random.default_rng(13).integers(20, 300, size=10)
+    w = decode_workload(MID, ctx, seed=14)
+    _, lg1, ids1 = _run(w)
+    order = np.random.default_rng(15).permutation(10)
+    w2 = copy.deepcopy(w)
+    w2.seqs = [w.seqs[i] for i in order]
+    for j, i in enumerate(order):
+        w2.seqs[j].content = [(p0, n, int(i)) for (p0, n, _c) in w.seqs[i].content]
+    w2.tokens = w.tokens[order]
+    _, lg2, ids2 = _run(w2)
+    np.testing.assert_array_equal(lg1[order], lg2)
+    np.testing.assert_array_equal(ids1[order], ids2)

@@ -212,31 +212,9 @@ def workload(cfg_id: int, seed: int = 0, model: ModelCfg | None = None, batch: i
     if cfg_id == 4:
         m = model or M3B
         n_dec = batch or 32
-        n_pre, plen = 4, 512
         ctx = _rng(seed, 4, 0).integers(256, 2048, endpoint=True, size=n_dec)
-        need_dec = [_nblk(c + 1) for c in ctx]
-        need_pre = n_pre * _nblk(plen)
-        total = sum(need_dec) + need_pre
-        n_pool = int(math.ceil(1.25 * total))
-        perm = _rng(seed, 4, 1).permutation(n_pool).astype(np.int32)
-        seqs = []
-        pos = 0
-        # decoding sequences hold permuted blocks
-        dec = []
-        for i, c in enumerate(ctx):
-            own = [int(b) for b in perm[pos:pos + need_dec[i]]]
-            pos += need_dec[i]
-            dec.append(SeqSpec(int(c), 1, own, [(0, int(c), i)]))
-        # fresh requests get their blocks from the free list (lowest id first)
-        pre = [SeqSpec(0, plen, [], [], logits=True) for _ in range(n_pre)]
-        seqs = pre + dec
-        rng = _rng(seed, 4, 2)
-        tokens = rng.integers(0, m.vocab, size=n_pre * plen + n_dec).astype(np.int32)
-        w = Workload(4, "3B-mixed-prefill4x512-decode32", m, seqs, n_pool, tokens, seed,
-                     "3B-class GQA, chunked prefill 4x512 + 32 decodes ctx U[256,2048]")
-        # blocks that are not handed to decoders are free; prefill takes the lowest ids
-        w.extra["free_blocks"] = sorted(int(b) for b in perm[pos:])
-        return w
+        return mixed_workload(m, 4, 512, ctx, seed, cfg_id=4, name="3B-mixed-prefill4x512-decode32",
+                              desc="3B-class GQA, chunked prefill 4x512 + 32 decodes ctx U[256,2048]")
     if cfg_id == 5:
         m = model or M8B
         B = batch or 128
@@ -247,5 +225,26 @@ def workload(cfg_id: int, seed: int = 0, model: ModelCfg | None = None, batch: i
     raise ValueError(cfg_id)
 
 
-def token_ids_key(seed, cfg_id):
-    return gen.key_of(seed, "tokens", cfg_id)
+def decode_workload(model: ModelCfg, ctx, seed=0, cfg_id=0, shared=None, name="decode", desc=""):
+    """A decode batch (one new row per sequence) with the given cached lengths."""
+    return _decode_workload(cfg_id, name, model, np.asarray(ctx, np.int64), seed, desc, shared=shared)
+
+
+def mixed_workload(model: ModelCfg, n_pre, plen, ctx, seed=0, cfg_id=0, name="mixed", desc=""):
+    """Fresh requests prefilled in one chunk (plen rows each, blocks from the free
+    list, lowest id first) beside decoding sequences holding permuted blocks."""
+    ctx = np.asarray(ctx, np.int64)
+    n_dec = len(ctx)
+    need_dec = [_nblk(c + 1) for c in ctx]
+    total = sum(need_dec) + n_pre * _nblk(plen)
+    n_pool = int(math.ceil(1.25 * total))
+    perm = _rng(seed, cfg_id, 1).permutation(n_pool).astype(np.int32)
+    pos = 0
+    dec = []
+    for i, c in enumerate(ctx):
+        own = [int(b) for b in perm[pos:pos + need_dec[i]]]
+        pos += need_dec[i]
+        dec.append(SeqSpec(int(c), 1, own, [(0, int(c), i)]))
+    pre = [SeqSpec(0, plen, [], [], logits=True) for _ in range(n_pre)]
+    tokens = _rng(seed, cfg_id, 2).integers(0, model.vocab, size=n_pre * plen + n_dec).astype(np.int32)
+    return Workload(cfg_id, name, model, pre + dec, n_pool, tokens, seed, desc)
