@@ -1,0 +1,265 @@
+"""Benchmark of the batched decode step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Workload: the 3B-class GQA decoder (28 layers, hidden 3072, 24/8 heads x 128,
+SwiGLU 8192, vocab 128256), batch 16, cached contexts U[512,1024], KV blocks of
+16 with randomly permuted tables; one decode step + greedy argmax per step.
+Random-init bf16 weights and N(0,1) KV from the seeded generators; inputs are
+resident in HBM before timing starts and the step is replayed idempotently.
+
+Prints ONE JSON line.  ``value`` is decode tokens/s (rows per step / step
+time, the faster of eager launches and a captured HIP graph of the step);
+``roofline`` reports the gate/up projection (the largest kernel of a layer),
+timed live with HIP events around each of its launches during a timed pass
+loop; ``cpu_baseline`` times the float64 CPU oracle on a bounded sample of
+the same workload.  The batch-64 shared-prefix workload is reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+PEAK_HBM = 8.0e12  # MI355X HBM3E, bytes/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, help="decode workload of the value line (2, 3 or 5)")
+    ap.add_argument("--no-batch64", action="store_true", help="skip the batch-64 shared-prefix line")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-layers", type=int, default=2, help="layers in the CPU oracle sample")
+    ap.add_argument("--no-graph", action="store_true")
+    return ap.parse_args()
+
+
+# ------------------------------------------------------------------ HIP events (same runtime as torch)
+class HipEvents:
+    def __init__(self):
+        self.L = C.CDLL("libamdhip64.so.7")
+        self.L.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.L.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.L.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.L.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            e = C.c_void_p()
+            assert self.L.hipEventCreate(C.byref(e)) == 0
+            out.append(e.value)
+        return out
+
+    def elapsed_ms(self, a, b):
+        ms = C.c_float()
+        assert self.L.hipEventSynchronize(C.c_void_p(b)) == 0
+        assert self.L.hipEventElapsedTime(C.byref(ms), C.c_void_p(a), C.c_void_p(b)) == 0
+        return ms.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.L.hipEventDestroy(C.c_void_p(e))
+
+
+# ------------------------------------------------------------------ accounting
+def step_bytes(w):
+    """Algorithmic HBM bytes of one decode step: every matrix once, each unique
+    resident (layer, token) KV entry once, new KV and logits written, embedding rows."""
+    m = w.model
+    B = w.n_rows
+    wbytes = m.weight_bytes_streamed()
+    kv_read = w.unique_resident_tokens() * m.n_layers * m.kv_bytes_per_token_layer
+    kv_write = B * m.n_layers * m.kv_bytes_per_token_layer
+    logits = B * m.vocab * 2
+    emb = B * m.hidden * 2
+    return wbytes + kv_read + kv_write + logits + emb
+
+
+def gateup_bytes(m, R):
+    """Algorithmic bytes of one gate/up launch: its weights, its input rows, its output."""
+    return 2 * m.ffn * m.hidden * 2 + R * m.hidden * 2 + R * m.ffn * 2
+
+
+def time_steps(torch, fn, steps, warmup, stream):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    return e0.elapsed_time(e1) / steps, wall
+
+
+def measure(torch, w, steps, warmup, use_graph, probe=True):
+    from paper_2609_37062_amd.runner import DeviceRun
+    print(f"[bench] setting up {w.name}", file=sys.stderr, flush=True)
+    d = DeviceRun(w)
+    stream = torch.cuda.current_stream()
+    res = {}
+    ms_eager, wall_eager = time_steps(torch, d.step, steps, warmup, stream)
+    res["ms_eager"] = ms_eager
+    res["ms_eager_wall"] = wall_eager
+    print(f"[bench] {w.name}: eager {ms_eager:.3f} ms/step", file=sys.stderr, flush=True)
+    if use_graph:
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            d.step(stream=s.cuda_stream)  # warm the capture stream
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            d.step(stream=torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        ms_graph, wall_graph = time_steps(torch, g.replay, steps, warmup, stream)
+        res["ms_graph"] = ms_graph
+        print(f"[bench] {w.name}: graph {ms_graph:.3f} ms/step", file=sys.stderr, flush=True)
+        # graph replays must reproduce the eager result
+        lg_g, ids_g = d.results()
+        d.step()
+        lg_e, ids_e = d.results()
+        res["graph_matches_eager"] = bool(np.array_equal(lg_g, lg_e) and np.array_equal(ids_g, ids_e))
+        del g
+    if probe:
+        ev = HipEvents()
+        n = steps * w.model.n_layers
+        b, e = ev.create(n), ev.create(n)
+        d.eng.set_probe(0, b, e)
+        for _ in range(steps):
+            d.step()
+        torch.cuda.synchronize()
+        durs = [ev.elapsed_ms(b[i], e[i]) for i in range(n)]
+        d.eng.set_probe(0, [], [])
+        ev.destroy(b + e)
+        res["gateup_ms"] = float(np.mean(durs))
+        res["gateup_ms_median"] = float(np.median(durs))
+    res["counters"] = d.eng.exec_counters().tolist()[:5]
+    d.release()
+    del d
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(w, n_layers_sample):
+    """Time the float64 oracle on a sample: all rows of the workload through
+    1 and 1 + n_layers_sample layers plus the lm_head, extrapolated per layer."""
+    import copy
+    from dataclasses import replace
+
+    from threadpoolctl import threadpool_info
+
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from oracle.model import GeneratedWeights, forward
+    from helpers import oracle_state
+
+    times = {}
+    for nl in (1, 1 + n_layers_sample):
+        ws = copy.copy(w)
+        ws.model = replace(w.model, n_layers=nl)
+        a, batch, sub, rows, kv, idx = oracle_state(ws)
+        W = GeneratedWeights(ws.model, w.seed, cache=True)
+        for l in range(nl):  # weights drawn before timing
+            for n in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "attn_norm", "mlp_norm"):
+                W.get(n, l)
+        W.over[("lm_head", -1)] = GeneratedWeights(ws.model, w.seed).get("lm_head", -1)
+        W.get("final_norm", -1)
+        lr = np.arange(w.n_rows)
+        t0 = time.perf_counter()
+        forward(ws.model, W, kv, sub, w.tokens[rows], lr)
+        times[nl] = time.perf_counter() - t0
+        del W, kv
+    t_layer = (times[1 + n_layers_sample] - times[1]) / n_layers_sample
+    t_step = times[1] + (w.model.n_layers - 1) * t_layer
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": w.n_rows / t_step, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"{w.name}: all {w.n_rows} rows through 1 and {1 + n_layers_sample} of "
+                       f"{w.model.n_layers} layers + lm_head (float64 NumPy, weights and KV drawn "
+                       f"before timing), per-layer time extrapolated to the full step"),
+            "s_per_step": t_step}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1", "n_gpus": a.gpus}))
+        sys.exit(2)
+    import torch
+
+    from workloads.configs import workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = workload(a.workload)
+    r = measure(torch, w, a.steps, a.warmup, not a.no_graph)
+    ms = min(r["ms_eager"], r.get("ms_graph", float("inf")))
+    tokps = w.n_rows / (ms / 1e3)
+    sb = step_bytes(w)
+    gb = gateup_bytes(w.model, w.n_rows)
+    achieved = gb / (r["gateup_ms"] / 1e3)
+    out = {
+        "metric": "decode-step latency (ms) & tokens/s at batch 16/64; achieved HBM TB/s vs peak",
+        "value": round(tokps, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.n_rows, "layers": w.model.n_layers,
+                   "hidden": w.model.hidden, "heads": f"{w.model.n_q_heads}/{w.model.n_kv_heads}x{w.model.head_dim}",
+                   "ffn": w.model.ffn, "vocab": w.model.vocab,
+                   "resident_tokens": w.resident_tokens(), "kv_block": 16},
+        "ms_eager": round(r["ms_eager"], 4),
+        "ms_graph": round(r["ms_graph"], 4) if "ms_graph" in r else None,
+        "graph_matches_eager": r.get("graph_matches_eager"),
+        "step_bytes": sb,
+        "step_hbm_TBps": round(sb / (ms / 1e3) / 1e12, 3),
+        "step_hbm_frac": round(sb / (ms / 1e3) / PEAK_HBM, 4),
+        "roofline": {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm, EPI_SWIGLU)",
+                     "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM, 4), "traffic": None,
+                     "bytes_per_launch": gb, "avg_launch_ms": round(r["gateup_ms"], 5)},
+        "exec_counters": r["counters"],
+    }
+    if not a.no_batch64 and a.workload == 2:
+        w3 = workload(3)
+        r3 = measure(torch, w3, a.steps, a.warmup, not a.no_graph, probe=False)
+        ms3 = min(r3["ms_eager"], r3.get("ms_graph", float("inf")))
+        sb3 = step_bytes(w3)
+        out["batch64_shared_prefix"] = {
+            "workload": w3.name, "ms_per_step": round(ms3, 4), "tokens_per_s": round(w3.n_rows / (ms3 / 1e3), 1),
+            "ms_eager": round(r3["ms_eager"], 4), "ms_graph": round(r3["ms_graph"], 4) if "ms_graph" in r3 else None,
+            "step_bytes": sb3, "step_hbm_TBps": round(sb3 / (ms3 / 1e3) / 1e12, 3),
+            "step_hbm_frac": round(sb3 / (ms3 / 1e3) / PEAK_HBM, 4)}
+    if not a.no_cpu:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cb = cpu_baseline(w, a.cpu_layers)
+        cb.pop("s_per_step")
+        cb["value"] = round(cb["value"], 4)
+        out["cpu_baseline"] = cb
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

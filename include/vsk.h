@@ -197,6 +197,22 @@ int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logi
 int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab,
                       int32_t* ids_dev, void* stream);
 
+/* Timing probes (measurement only).  While set, the first n_pairs launches
+ * of kernel class `which` in the following passes are each bracketed by
+ * hipEventRecord(begin_events[i]) / hipEventRecord(end_events[i]) on the pass
+ * stream, in launch order.  Classes: 0 gate/up projection, 1 down projection,
+ * 2 QKV projection, 3 O projection, 4 attention, 5 lm_head projection.
+ * Events are caller-created hipEvent_t handles; n_pairs = 0 clears the probe.
+ * Do not set probes while a pass is being captured into a graph. */
+int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
+                  void* const* end_events, int32_t n_pairs);
+
+/* Launch-shape tuning (the analogue of a device-tuned tile table).  Results
+ * do not depend on it beyond floating-point summation order.
+ * key 0: attention 16-token blocks per split-K work item (multiple of 8,
+ *        8..4096; default 32). */
+int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
+
 /* Counters of what the last pass executed (kernel variants, split factors),
  * for attestation in tests and benchmarks.  Writes up to cap int64 values:
  * [0] passes run, [1] gemm launches, [2] attention launches, [3] attention

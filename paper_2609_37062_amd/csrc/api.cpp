@@ -43,14 +43,12 @@ PackedLayout packed_layout(const vsk_model_cfg& c) {
 
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// partial-buffer bytes and counter count needed by a projection over up to R rows
-static void gemm_ws_need(int N, int K, int R_max, int epi, size_t& part, size_t& cnt) {
+// partial-buffer bytes of a projection's K splits over up to R_max rows
+static void gemm_ws_need(int N, int K, int R_max, int epi, size_t& part) {
   for (int Rg = 1; Rg <= ceil_div(R_max, 16); ++Rg) {
-    const GemmPlan p = plan_gemm(N, K, 16 * Rg, epi);
-    const size_t tiles = static_cast<size_t>(p.m_tiles) * p.n_groups;
-    const size_t rows_per_group = p.mg <= 2 ? 16 : 64;
-    if (p.ks > 1) part = std::max(part, tiles * p.ks * rows_per_group * 16 * p.mg * 4);
-    cnt = std::max(cnt, tiles);
+    const int R = std::min(16 * Rg, R_max);
+    const GemmPlan p = plan_gemm(N, K, R, epi);
+    if (p.ks > 1) part = std::max(part, static_cast<size_t>(p.ks) * R * N * 4);
   }
 }
 
@@ -60,7 +58,7 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   w.max_seqs = max_seqs;
   w.max_kv_len = max_kv_len;
   w.Rg = ceil_div(max_rows, 16);
-  w.max_splits = attn_splits(max_kv_len);
+  w.max_splits = attn_splits(max_kv_len, kAttnMinBps);
   const size_t H = c.hidden, F = c.ffn, Nq = static_cast<size_t>(c.n_q_heads) * c.head_dim,
                Nkv = static_cast<size_t>(c.n_kv_heads) * c.head_dim;
   const size_t Rp = static_cast<size_t>(w.Rg) * 16;
@@ -73,22 +71,13 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   const size_t rh = static_cast<size_t>(max_rows) * c.n_kv_heads;
   w.att_o = o; o = align_up(o + rh * w.max_splits * G * c.head_dim * 4);
   w.att_ml = o; o = align_up(o + rh * w.max_splits * G * 8);
-  size_t part = 0, cnt = 0;
-  gemm_ws_need(static_cast<int>(Nq + 2 * Nkv), c.hidden, max_rows, EPI_QKV, part, cnt);
-  gemm_ws_need(c.hidden, static_cast<int>(Nq), max_rows, EPI_RESID, part, cnt);
-  gemm_ws_need(2 * c.ffn, c.hidden, max_rows, EPI_SWIGLU, part, cnt);
-  gemm_ws_need(c.hidden, c.ffn, max_rows, EPI_RESID, part, cnt);
+  size_t part = 0;
+  gemm_ws_need(c.hidden, static_cast<int>(Nq), max_rows, EPI_RESID, part);
+  gemm_ws_need(c.hidden, c.ffn, max_rows, EPI_RESID, part);
   w.gemm_part = o; o = align_up(o + part);
   // lm_head partials: n_groups x rows
-  const GemmPlan lp = plan_gemm(c.vocab, c.hidden, max_rows, EPI_LOGITS);
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
-  (void)lp;
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
-  // counters last so one clear covers them
-  w.counters_begin = o;
-  w.att_cnt = o; o = align_up(o + rh * 4);
-  w.gemm_cnt = o; o = align_up(o + cnt * 4);
-  w.counters_end = o;
   w.total = o;
   return w;
 }
@@ -115,6 +104,8 @@ static bool cfg_ok(const vsk_model_cfg* c, std::string& why) {
   if (c->n_q_heads % c->n_kv_heads != 0 || c->n_q_heads / c->n_kv_heads > 16) {
     why = "n_q_heads must be a multiple of n_kv_heads, at most 16 per group"; return false;
   }
+  if (c->hidden > 8192) { why = "hidden must be at most 8192"; return false; }
+  if (c->max_pos > 16384) { why = "max_pos must be at most 16384"; return false; }
   if (c->hidden % 64 || (c->n_q_heads * c->head_dim) % 64 || c->ffn % 64 || c->vocab % 64) {
     why = "hidden, n_q_heads*head_dim, ffn and vocab must be multiples of 64"; return false;
   }
@@ -471,6 +462,31 @@ int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32
   return e == hipSuccess ? VSK_OK : VSK_E_HIP;
 }
 
+int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events, void* const* end_events, int32_t n_pairs) {
+  if (!h) return VSK_E_ARG;
+  if (which < 0 || which >= Handle::kProbeClasses) return fail(h, VSK_E_RANGE, "unknown probe class");
+  if (n_pairs < 0 || (n_pairs > 0 && (!begin_events || !end_events))) return fail(h, VSK_E_ARG, "bad probe events");
+  h->probe_b[which].assign(reinterpret_cast<const hipEvent_t*>(begin_events),
+                           reinterpret_cast<const hipEvent_t*>(begin_events) + n_pairs);
+  h->probe_e[which].assign(reinterpret_cast<const hipEvent_t*>(end_events),
+                           reinterpret_cast<const hipEvent_t*>(end_events) + n_pairs);
+  h->probe_i[which] = 0;
+  return VSK_OK;
+}
+
+int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
+  if (!h) return VSK_E_ARG;
+  switch (key) {
+    case 0:
+      if (value < kAttnMinBps || value % 8 != 0 || value > 4096)
+        return fail(h, VSK_E_ARG, "attention blocks per split must be a multiple of 8 in [8, 4096]");
+      h->attn_bps = value;
+      return VSK_OK;
+    default:
+      return fail(h, VSK_E_ARG, "unknown tuning key");
+  }
+}
+
 int vsk_exec_counters(const vsk_handle* h, int64_t* out, int32_t cap) {
   if (!h || !out) return VSK_E_ARG;
   for (int i = 0; i < cap && i < 8; ++i) out[i] = h->counters[i];
@@ -501,12 +517,23 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   do {                                 \
     if ((e = (call)) != hipSuccess) return e; \
   } while (0)
+  // probe-bracketed launch of kernel class `cls`
+  auto probed = [&](int cls, auto&& launch) -> hipError_t {
+    const bool on = h.probe_i[cls] < h.probe_b[cls].size();
+    hipError_t pe;
+    if (on && (pe = hipEventRecord(h.probe_b[cls][h.probe_i[cls]], s)) != hipSuccess) return pe;
+    if ((pe = launch()) != hipSuccess) return pe;
+    if (on) {
+      if ((pe = hipEventRecord(h.probe_e[cls][h.probe_i[cls]], s)) != hipSuccess) return pe;
+      ++h.probe_i[cls];
+    }
+    return hipSuccess;
+  };
 
   TRY(launch_embed(reinterpret_cast<const uint16_t*>(P + h.pl.embed), pa.ids, R, H, c.vocab, x, s));
 
   GemmArgs ga{};
   ga.part = reinterpret_cast<float*>(ws + wl.gemm_part);
-  ga.cnt = reinterpret_cast<int*>(ws + wl.gemm_cnt);
   ga.R = R;
   ga.Rg = Rg;
   ga.pool = h.pool;
@@ -532,10 +559,10 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   aa.row_seq = b.row_seq;
   aa.pos = b.pos;
   aa.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d)));
-  aa.max_splits = attn_splits(b.max_kv_len);
+  aa.bps = h.attn_bps;
+  aa.max_splits = attn_splits(b.max_kv_len, h.attn_bps);
   aa.part_o = reinterpret_cast<float*>(ws + wl.att_o);
   aa.part_ml = reinterpret_cast<float2*>(ws + wl.att_ml);
-  aa.cnt = reinterpret_cast<int*>(ws + wl.att_cnt);
   aa.out = act0;
   aa.out_Rg = Rg;
 
@@ -544,48 +571,53 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU);
   const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID);
 
+  float* part = reinterpret_cast<float*>(ws + wl.gemm_part);
+  int pending = 0;  // K splits of the last residual projection, folded in by the next norm
   for (int l = 0; l < c.n_layers; ++l) {
     const uint8_t* L = P + h.pl.layer_bytes * l;
     // attention block
-    TRY(launch_rmsnorm(x, reinterpret_cast<const uint16_t*>(L + h.pl.l.attn_norm), nullptr, R, R, H, c.rms_eps, act0, Rg,
-                       s));
+    TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(L + h.pl.l.attn_norm), nullptr, R, R, H,
+                       c.rms_eps, act0, Rg, s));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wqkv);
     ga.X = reinterpret_cast<const u4*>(act0);
     ga.Kt = H / 32;
     ga.N = Nq + 2 * Nkv;
     ga.out = q;
     ga.layer = l;
-    TRY(launch_gemm(ga, p_qkv, EPI_QKV, s));
+    TRY(probed(2, [&] { return launch_gemm(ga, p_qkv, EPI_QKV, s); }));
     aa.layer = l;
-    TRY(launch_attn_decode(aa, R, s));
+    TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);
     ga.X = reinterpret_cast<const u4*>(act0);
     ga.Kt = Nq / 32;
     ga.N = H;
     ga.x = x;
-    TRY(launch_gemm(ga, p_o, EPI_RESID, s));
+    ga.part = part;
+    TRY(probed(3, [&] { return launch_gemm(ga, p_o, EPI_RESID, s); }));
+    pending = p_o.ks > 1 ? p_o.ks : 0;
     // MLP block
-    TRY(launch_rmsnorm(x, reinterpret_cast<const uint16_t*>(L + h.pl.l.mlp_norm), nullptr, R, R, H, c.rms_eps, act0, Rg,
-                       s));
+    TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(L + h.pl.l.mlp_norm), nullptr, R, R, H,
+                       c.rms_eps, act0, Rg, s));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wgu);
     ga.X = reinterpret_cast<const u4*>(act0);
     ga.Kt = H / 32;
     ga.N = 2 * F;
     ga.out = act1;
     ga.out_Rg = Rg;
-    TRY(launch_gemm(ga, p_gu, EPI_SWIGLU, s));
+    TRY(probed(0, [&] { return launch_gemm(ga, p_gu, EPI_SWIGLU, s); }));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wd);
     ga.X = reinterpret_cast<const u4*>(act1);
     ga.Kt = F / 32;
     ga.N = H;
     ga.x = x;
-    TRY(launch_gemm(ga, p_d, EPI_RESID, s));
+    TRY(probed(1, [&] { return launch_gemm(ga, p_d, EPI_RESID, s); }));
+    pending = p_d.ks > 1 ? p_d.ks : 0;
   }
   // final norm (gathered logit rows) + lm_head + greedy argmax
   const int Ro = pa.n_logit_rows;
   const int Rgo = (Ro + 15) / 16;
-  TRY(launch_rmsnorm(x, reinterpret_cast<const uint16_t*>(P + h.pl.final_norm), pa.logit_rows, Ro, R, H, c.rms_eps, act0,
-                     Rgo, s));
+  TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(P + h.pl.final_norm), pa.logit_rows, Ro, R,
+                     H, c.rms_eps, act0, Rgo, s));
   const GemmPlan p_lm = plan_gemm(c.vocab, H, Ro, EPI_LOGITS);
   ga.W = reinterpret_cast<const u4*>(P + h.pl.lm_head);
   ga.X = reinterpret_cast<const u4*>(act0);
@@ -596,7 +628,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ga.out = pa.logits;
   ga.am_val = reinterpret_cast<float*>(ws + wl.am_part);
   ga.am_idx = reinterpret_cast<int*>(ws + wl.am_part + static_cast<size_t>((c.vocab + 15) / 16) * wl.max_rows * 4);
-  TRY(launch_gemm(ga, p_lm, EPI_LOGITS, s));
+  TRY(probed(5, [&] { return launch_gemm(ga, p_lm, EPI_LOGITS, s); }));
   if (pa.next_ids) TRY(launch_argmax_partials(ga.am_val, ga.am_idx, p_lm.n_groups, Ro, pa.next_ids, s));
 #undef TRY
   h.counters[0] += 1;

@@ -14,10 +14,10 @@ struct AttnArgs {
   const int32_t* row_seq;
   const int32_t* pos;
   float scale_log2;  // log2(e) / sqrt(hd)
-  int max_splits;
+  int bps;         // 16-token blocks per split (multiple of 8)
+  int max_splits;  // split stride of the partial buffers
   float* part_o;   // [R][Hkv][max_splits][G][hd]
   float2* part_ml; // [R][Hkv][max_splits][G]
-  int* cnt;        // [R][Hkv], zero between launches
   uint16_t* out;   // o frags (K = Nq)
   int out_Rg;
 };

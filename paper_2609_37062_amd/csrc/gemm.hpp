@@ -15,8 +15,7 @@ struct GemmArgs {
   int R;        // valid rows
   int Rg;       // 16-row groups of the X frag buffer
   int KS;       // K splits across workgroups (set from the plan)
-  float* part;  // split-K partials
-  int* cnt;     // split-K arrival counters [m_tiles * n_groups], zero between launches
+  float* part;  // RESID with KS > 1: partials [KS][R][N]
   // epilogue operands
   float* x;       // RESID: fp32 residual [R][N]
   uint16_t* out;  // QKV: q [R][Nq]; SWIGLU: frags (out_Rg); LOGITS: logits [R][N]
@@ -35,6 +34,7 @@ struct GemmPlan {
   int m_tiles = 1;   // tiles along the rows
   int n_groups = 1;  // workgroups along N
   int ks = 1;        // K splits across workgroups
+  bool wide = false; // four N tiles per wave (mg == 1 only)
 };
 
 GemmPlan plan_gemm(int N, int K, int R, int epi);

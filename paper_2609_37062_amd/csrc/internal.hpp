@@ -6,6 +6,7 @@
 #include <cstddef>
 #include <cstdint>
 #include <string>
+#include <vector>
 
 #include "../../include/vsk.h"
 #include "alloc.hpp"
@@ -82,9 +83,16 @@ struct BatchDev {
 // ---------------------------------------------------------------- workspace
 struct WsLayout {
   int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
-  size_t x, act0, act1, q, att_o, att_ml, att_cnt, gemm_part, gemm_cnt, am_part, counters_begin,
-      counters_end, total;
+  size_t x, act0, act1, q, att_o, att_ml, gemm_part, am_part, total;
 };
+
+// attention split: 16-token blocks per split-K work item (tunable, >= kAttnMinBps)
+constexpr int kAttnMinBps = 8;
+constexpr int kAttnDefaultBps = 32;
+inline int attn_splits(int kv_len, int bps) {
+  const int nb = (kv_len + kBlock - 1) / kBlock;
+  return (nb + bps - 1) / bps;
+}
 
 struct Handle {
   vsk_model_cfg cfg{};
@@ -103,22 +111,22 @@ struct Handle {
   bool batch_built = false;
   BatchDev bd;
   bool batch_uploaded = false;
+  // tuning
+  int attn_bps = kAttnDefaultBps;
   // workspace
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
   WsLayout wl;
+  // timing probes per kernel class
+  static constexpr int kProbeClasses = 6;
+  std::vector<hipEvent_t> probe_b[kProbeClasses], probe_e[kProbeClasses];
+  size_t probe_i[kProbeClasses] = {0};
   // counters
   int64_t counters[8] = {0};
 };
 
 WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len);
 
-// attention split: blocks per split-K work item
-constexpr int kAttnBlocksPerSplit = 8;
-inline int attn_splits(int kv_len) {
-  const int nb = (kv_len + kBlock - 1) / kBlock;
-  return (nb + kAttnBlocksPerSplit - 1) / kAttnBlocksPerSplit;
-}
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipSuccess or the launch error.

@@ -4,13 +4,13 @@
 // query heads of that KV head's group attend to keys 0..p read through the
 // sequence's block table (paper, "Invariants": each layer reads its own
 // cached K,V; Algorithm 1 keeps attention's launch shape).  A workgroup owns
-// one (row, KV head, split) and its four waves take the split's 16-token
+// one (row, KV head, split) and its eight waves take the split's 16-token
 // blocks in turn.  Per block a wave computes S = K q with
 // v_mfma_f32_16x16x32_bf16 (16 tokens x up to 16 heads), an online softmax in
 // the base-2 domain, and O^T += V^T P^T with v_mfma_f32_16x16x16_bf16, so the
 // softmax row lives in the same lanes as the output it rescales.  The waves
-// merge in LDS; splits merge through a small partial buffer, where the last
-// workgroup of a (row, head) to finish combines them in split order.
+// merge in LDS; splits write (m, l, O) partials that a second small kernel
+// merges in split order.
 // Decode attention reads about group-size flops per byte of KV, so it is
 // bound by HBM, not by the matrix cores.
 #include <cmath>
@@ -20,7 +20,7 @@
 
 namespace vsk {
 
-constexpr int kAttnWaves = 4;
+constexpr int kAttnWaves = 8;
 
 template <int D>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
@@ -29,7 +29,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   __shared__ float s_m[kAttnWaves][16];
   __shared__ float s_l[kAttnWaves][16];
   __shared__ f32x4 s_o[kAttnWaves - 1][VC][64];
-  __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -37,12 +36,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   const int G = a.G;
   const int kv_len = a.pos[row] + 1;
   const int nb = (kv_len + kBlock - 1) / kBlock;
-  const int n_splits = (nb + kAttnBlocksPerSplit - 1) / kAttnBlocksPerSplit;
+  const int n_splits = (nb + a.bps - 1) / a.bps;
   if (split >= n_splits) return;
   const int seq = a.row_seq[row];
   const int32_t* table = a.block_table + static_cast<size_t>(seq) * a.max_blocks;
-  const int b_lo = split * kAttnBlocksPerSplit;
-  const int b_hi = min(nb, b_lo + kAttnBlocksPerSplit);
+  const int b_lo = split * a.bps;
+  const int b_hi = min(nb, b_lo + a.bps);
 
   const int h = lane & 15;       // query head within the group (valid if h < G)
   const int quad = lane >> 4;    // token quarter / k sub-range
@@ -66,16 +65,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   const uint16_t* vbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks * kv_stride +
                           static_cast<size_t>(hk) * kBlock * D;
 
-  for (int b = b_lo + w; b < b_hi; b += kAttnWaves) {
-    const size_t blk = static_cast<size_t>(table[b]);
-    const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
-    const u32x2* vp = reinterpret_cast<const u32x2*>(vbase + blk * kv_stride) + lane;
-    u32x4 kf[KC];
-    u32x2 vf[VC];
-#pragma unroll
-    for (int c = 0; c < KC; ++c) kf[c] = kp[c * 64];
-#pragma unroll
-    for (int c = 0; c < VC; ++c) vf[c] = vp[c * 64];
+  // one 16-token block: S = K q, online softmax, O^T += V^T P^T
+  auto process = [&](const u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {
     // slots past kv_len in the last block hold whatever was there: zero their
     // V (a masked probability of 0 times a NaN pattern would still be NaN)
     const int t_lane = b * kBlock + 4 * quad;  // first token of this lane's quarter
@@ -95,8 +86,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
     float mx = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int t = b * kBlock + 4 * quad + r;
-      s[r] = (t < kv_len) ? s[r] * sc : -INFINITY;
+      s[r] = (t_lane + r < kv_len) ? s[r] * sc : -INFINITY;
       mx = fmaxf(mx, s[r]);
     }
     mx = fmaxf(mx, shfl_xor(mx, 16));
@@ -121,6 +111,29 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
       o[c] *= alpha;
       o[c] = mfma_16x16x16(vf[c], pf, o[c]);  // lane holds O[head h][dim 16c + 4*quad + r]
     }
+  };
+  auto load = [&](u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {
+    const size_t blk = static_cast<size_t>(table[b]);
+    const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
+    const u32x2* vp = reinterpret_cast<const u32x2*>(vbase + blk * kv_stride) + lane;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) kf[c] = kp[c * 64];
+#pragma unroll
+    for (int c = 0; c < VC; ++c) vf[c] = vp[c * 64];
+  };
+
+  // this wave's blocks b_lo + w, + kAttnWaves, ...: two blocks in flight
+  u32x4 kA[KC], kB[KC];
+  u32x2 vA[VC], vB[VC];
+  int b = b_lo + w;
+  if (b < b_hi) load(kA, vA, b);
+  for (; b < b_hi; b += 2 * kAttnWaves) {
+    const int bn = b + kAttnWaves;
+    if (bn < b_hi) load(kB, vB, bn);
+    process(kA, vA, b);
+    if (bn >= b_hi) break;
+    if (bn + kAttnWaves < b_hi) load(kA, vA, bn + kAttnWaves);
+    process(kB, vB, bn);
   }
 
   // ---- merge the waves of this workgroup
@@ -169,7 +182,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
     return;
   }
 
-  // ---- several splits: publish this split's (m, l, O), the last one combines
+  // ---- several splits: publish this split's (m, l, O); k_attn_combine merges them
   const size_t rh = static_cast<size_t>(row) * a.Hkv + hk;
   if (w == 0 && h < G) {
     float* po = a.part_o + ((rh * a.max_splits + split) * G + h) * D;
@@ -178,27 +191,53 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
       *reinterpret_cast<float4*>(po + 16 * c + 4 * quad) = make_float4(o[c][0], o[c][1], o[c][2], o[c][3]);
     if (quad == 0) a.part_ml[(rh * a.max_splits + split) * G + h] = make_float2(m, l);
   }
-  __threadfence();
+}
+
+// Merge the split partials of rows with more than one split, in split order:
+// O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.  One workgroup per (KV head, row).
+constexpr int kMaxSplits = 128;  // max_pos <= 16384 with at least 8 blocks per split
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  __shared__ float s_f[kMaxSplits][16];  // per split and head: 2^(m_s - M)
+  __shared__ float s_invL[16];
+  const int hk = blockIdx.x, row = blockIdx.y;
+  const int kv_len = a.pos[row] + 1;
+  const int n_splits = (((kv_len + kBlock - 1) / kBlock) + a.bps - 1) / a.bps;
+  if (n_splits <= 1) return;
+  const int G = a.G, D = a.hd;
+  const size_t rh = static_cast<size_t>(row) * a.Hkv + hk;
+  const float2* ml = a.part_ml + rh * a.max_splits * G;
+  if (threadIdx.x < G) {
+    const int hh = threadIdx.x;
+    float M = -INFINITY;
+    for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml[s * G + hh].x);
+    float L = 0.f;
+    for (int s = 0; s < n_splits; ++s) {
+      const float2 v = ml[s * G + hh];
+      const float f = exp2f(v.x - M);
+      s_f[s][hh] = f;
+      L += v.y * f;
+    }
+    s_invL[hh] = 1.f / L;
+  }
   __syncthreads();
-  if (threadIdx.x == 0) s_last = (atomicAdd(&a.cnt[rh], 1) == n_splits - 1);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  // combine in split order: element (h, e) per thread
+  const float* po = a.part_o + rh * a.max_splits * G * D;
   for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
     const int hh = idx / D, e = idx % D;
-    float M = -INFINITY;
-    for (int s = 0; s < n_splits; ++s) M = fmaxf(M, a.part_ml[(rh * a.max_splits + s) * G + hh].x);
-    float L = 0.f, acc = 0.f;
-    for (int s = 0; s < n_splits; ++s) {
-      const float2 ml = a.part_ml[(rh * a.max_splits + s) * G + hh];
-      const float f = exp2f(ml.x - M);
-      L += ml.y * f;
-      acc += a.part_o[((rh * a.max_splits + s) * G + hh) * D + e] * f;
+    float acc = 0.f;
+    int s = 0;
+    for (; s + 4 <= n_splits; s += 4) {
+      const float v0 = po[(static_cast<size_t>(s + 0) * G + hh) * D + e];
+      const float v1 = po[(static_cast<size_t>(s + 1) * G + hh) * D + e];
+      const float v2 = po[(static_cast<size_t>(s + 2) * G + hh) * D + e];
+      const float v3 = po[(static_cast<size_t>(s + 3) * G + hh) * D + e];
+      acc += v0 * s_f[s][hh];
+      acc += v1 * s_f[s + 1][hh];
+      acc += v2 * s_f[s + 2][hh];
+      acc += v3 * s_f[s + 3][hh];
     }
-    a.out[frag_index(row, (hk * G + hh) * D + e, a.out_Rg)] = static_cast<uint16_t>(f2bf(acc / L));
+    for (; s < n_splits; ++s) acc += po[(static_cast<size_t>(s) * G + hh) * D + e] * s_f[s][hh];
+    a.out[frag_index(row, (hk * G + hh) * D + e, a.out_Rg)] = static_cast<uint16_t>(f2bf(acc * s_invL[hh]));
   }
-  if (threadIdx.x == 0) a.cnt[rh] = 0;
 }
 
 hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s) {
@@ -210,6 +249,9 @@ hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s) {
   } else {
     return hipErrorInvalidValue;
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.max_splits <= 1) return e;
+  hipLaunchKernelGGL(k_attn_combine, dim3(a.Hkv, n_rows), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

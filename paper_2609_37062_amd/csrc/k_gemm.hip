@@ -8,9 +8,8 @@
 // 16-byte load per lane, several tiles in flight, and feeds them straight
 // to v_mfma_f32_16x16x32_bf16 with W as the A operand (16 output columns)
 // and a 16-row group of X as the B operand.  K is split across the waves of
-// a workgroup (reduced in LDS) and, for narrow N, across workgroups (the last
-// workgroup to finish sums the partials in split order, so results do not
-// depend on scheduling).
+// a workgroup (reduced in LDS in a fixed order) and, for the narrow residual
+// projections, across workgroups (partials summed by the next kernel).
 //
 // Epilogues (the tensors stored between kernels are rounded to bf16):
 //   RESID  : x[r][n] += y                      (O and down projections)
@@ -31,7 +30,6 @@ __device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v));
 template <int MG, int NT, int WN, int WK, int PF, int EPI>
 __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ int s_last;
   __shared__ float s_amv[WN][MG][16];
   __shared__ int s_ami[WN][MG][16];
 
@@ -110,40 +108,13 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
     }
   }
 
-  // ---- split-K across workgroups: the last arrival sums the partials in split order
-  if (a.KS > 1) {
-    f32x4* part = reinterpret_cast<f32x4*>(a.part);
-    const size_t tile = static_cast<size_t>(mt) * gridDim.x + ng;
-    if (wk == 0) {
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-#pragma unroll
-        for (int g = 0; g < MG; ++g)
-          part[((((tile * a.KS + ks) * WN + wn) * NT + j) * MG + g) * 64 + lane] = acc[j][g];
-    }
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) s_last = (atomicAdd(&a.cnt[tile], 1) == a.KS - 1);
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    if (wk == 0) {
-      for (int s = 0; s < a.KS; ++s)
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-#pragma unroll
-          for (int g = 0; g < MG; ++g) {
-            const f32x4 p = part[((((tile * a.KS + s) * WN + wn) * NT + j) * MG + g) * 64 + lane];
-            acc[j][g] = (s == 0) ? p : acc[j][g] + p;
-          }
-    }
-    if (threadIdx.x == 0) a.cnt[tile] = 0;
-  }
-
   // ---- epilogues (waves with wk == 0 hold the sums)
   const int rsub = lane & 15;
   const int nq = 4 * (lane >> 4);
   if constexpr (EPI == EPI_RESID) {
+    // KS == 1: x += y.  KS > 1 (K split across workgroups): each split stores
+    // its partial part[ks][row][n]; the next RMSNorm adds them to x in split
+    // order, so no workgroup waits for another and the sum is deterministic.
     if (wk == 0) {
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
@@ -153,13 +124,18 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
         for (int g = 0; g < MG; ++g) {
           const int row = 16 * (g0 + g) + rsub;
           if (row >= a.R) continue;
-          float4* px = reinterpret_cast<float4*>(a.x + static_cast<size_t>(row) * a.N + n0);
-          float4 v = *px;
-          v.x += acc[j][g][0];
-          v.y += acc[j][g][1];
-          v.z += acc[j][g][2];
-          v.w += acc[j][g][3];
-          *px = v;
+          if (a.KS > 1) {
+            *reinterpret_cast<float4*>(a.part + (static_cast<size_t>(ks) * a.R + row) * a.N + n0) =
+                make_float4(acc[j][g][0], acc[j][g][1], acc[j][g][2], acc[j][g][3]);
+          } else {
+            float4* px = reinterpret_cast<float4*>(a.x + static_cast<size_t>(row) * a.N + n0);
+            float4 v = *px;
+            v.x += acc[j][g][0];
+            v.y += acc[j][g][1];
+            v.z += acc[j][g][2];
+            v.w += acc[j][g][3];
+            *px = v;
+          }
         }
       }
     }
@@ -289,13 +265,19 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Launch shapes.  mg = 16-row groups of X per tile.  For mg == 1 two shapes:
+// "narrow" (one 16-row N tile per wave, 8 K-split waves, 8 K tiles in
+// flight) for matrices with few N tiles, and "wide" (four N tiles per wave,
+// 4 K tiles in flight, fewer and longer-running workgroups) for the wide
+// gate/up and lm_head matrices.
 template <int EPI>
-static hipError_t launch_epi(const GemmArgs& a, int mg, int m_tiles, hipStream_t s) {
-  switch (mg) {
-    case 1: return launch_cfg<1, 1, 1, 8, 4, EPI>(a, m_tiles, s);
-    case 2: return launch_cfg<2, 1, 1, 8, 4, EPI>(a, m_tiles, s);
-    case 4: return launch_cfg<4, 2, 2, 2, 2, EPI>(a, m_tiles, s);
-    default: return launch_cfg<8, 2, 2, 2, 2, EPI>(a, m_tiles, s);
+static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+  switch (p.mg) {
+    case 1:
+      return p.wide ? launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, s) : launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
+    case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
+    case 4: return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
+    default: return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
   }
 }
 
@@ -304,15 +286,22 @@ GemmPlan plan_gemm(int N, int K, int R, int epi) {
   const int Rg = (R + 15) / 16;
   p.mg = Rg <= 1 ? 1 : Rg <= 2 ? 2 : Rg <= 4 ? 4 : 8;
   p.m_tiles = (Rg + p.mg - 1) / p.mg;
-  const int rows_per_group = p.mg <= 2 ? 16 : 64;
+  // wide shape when it still leaves at least two workgroups per CU
+  p.wide = p.mg == 1 && (epi == EPI_SWIGLU || epi == EPI_LOGITS) && N / 64 >= 256;
+  const int rows_per_group = p.wide ? 64 : p.mg <= 2 ? 16 : 64;
   p.n_groups = (N / 16 * 16 + rows_per_group - 1) / rows_per_group;
   const int Kt = K / 32;
   const int wk = p.mg <= 2 ? 8 : 2;
+  // Only the residual projections split K across workgroups (their partials
+  // are summed by the next RMSNorm).  Aim for about 1024 workgroups, keep at
+  // least one K tile per wave, and keep the partial traffic (KS x R x N x 8
+  // bytes) under a quarter of the weight bytes.
   int ks = 1;
-  if (epi != EPI_LOGITS) {
-    const int target = 512;
+  if (epi == EPI_RESID) {
     const int have = p.n_groups * p.m_tiles;
-    while (have * ks < target && Kt / (ks * 2) >= wk * 2) ks *= 2;
+    while (have * ks * 2 <= 1024 && Kt / (ks * 2) >= wk &&
+           static_cast<long>(ks * 2) * R * 16 <= static_cast<long>(K))
+      ks *= 2;
   }
   p.ks = ks;
   return p;
@@ -321,10 +310,10 @@ GemmPlan plan_gemm(int N, int K, int R, int epi) {
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s) {
   a.KS = p.ks;
   switch (epi) {
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, p.mg, p.m_tiles, s);
-    case EPI_QKV: return launch_epi<EPI_QKV>(a, p.mg, p.m_tiles, s);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p.mg, p.m_tiles, s);
-    default: return launch_epi<EPI_LOGITS>(a, p.mg, p.m_tiles, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, p, s);
+    case EPI_QKV: return launch_epi<EPI_QKV>(a, p, s);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, s);
+    default: return launch_epi<EPI_LOGITS>(a, p, s);
   }
 }
 

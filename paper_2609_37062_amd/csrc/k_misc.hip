@@ -38,9 +38,14 @@ hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int
 // out = bf16(x * 1/sqrt(mean(x^2) + eps) * g) written as frags; output row r
 // reads input row gather[r] (or r).  Rows R..16*Rg of the output are zeroed.
 // A gathered index outside [0, R_in) gives a zero row.
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, const uint16_t* __restrict__ g,
-                                                 const int32_t* __restrict__ gather, int R, int R_in, int H,
-                                                 float eps, uint16_t* __restrict__ out, int Rg) {
+// With KS > 0, the K-split partials of the preceding residual projection
+// (part[s][row][H], s = 0..KS-1) are first added to x in split order and the
+// updated row is written back: this kernel completes that projection.
+constexpr int kNormChunks = 4;  // 8-column chunks per thread: hidden <= 256*8*4
+__global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ x, const float* __restrict__ part, int KS,
+                                                 const uint16_t* __restrict__ g, const int32_t* __restrict__ gather,
+                                                 int R, int R_in, int H, float eps, uint16_t* __restrict__ out,
+                                                 int Rg) {
   __shared__ float s_red[8];
   const int r = blockIdx.x;
   const int src = r < R ? (gather ? gather[r] : r) : -1;
@@ -49,11 +54,30 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, co
       *reinterpret_cast<u32x4*>(out + frag_index(r, c, Rg)) = u32x4{0u, 0u, 0u, 0u};
     return;
   }
-  const float* xr = x + static_cast<size_t>(src) * H;
+  float* xr = x + static_cast<size_t>(src) * H;
+  float v[kNormChunks][8];
   float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(xr + c);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+  for (int i = 0; i < kNormChunks; ++i) {
+    const int c = (threadIdx.x + i * blockDim.x) * 8;
+    if (c >= H) break;
+    float4 a = *reinterpret_cast<const float4*>(xr + c);
+    float4 b = *reinterpret_cast<const float4*>(xr + c + 4);
+    if (KS > 0) {
+      for (int s = 0; s < KS; ++s) {
+        const float* pr = part + (static_cast<size_t>(s) * R_in + src) * H + c;
+        const float4 pa = *reinterpret_cast<const float4*>(pr);
+        const float4 pb = *reinterpret_cast<const float4*>(pr + 4);
+        a.x += pa.x; a.y += pa.y; a.z += pa.z; a.w += pa.w;
+        b.x += pb.x; b.y += pb.y; b.z += pb.z; b.w += pb.w;
+      }
+      *reinterpret_cast<float4*>(xr + c) = a;
+      *reinterpret_cast<float4*>(xr + c + 4) = b;
+    }
+    v[i][0] = a.x; v[i][1] = a.y; v[i][2] = a.z; v[i][3] = a.w;
+    v[i][4] = b.x; v[i][5] = b.y; v[i][6] = b.z; v[i][7] = b.w;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) ss += v[i][k] * v[i][k];
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) ss += shfl_xor(ss, m);
@@ -62,22 +86,22 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ x, co
   float tot = 0.f;
   for (int i = 0; i < (int)(blockDim.x >> 6); ++i) tot += s_red[i];
   const float inv = 1.0f / sqrtf(tot / static_cast<float>(H) + eps);
-  for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8) {
-    const float4 a = *reinterpret_cast<const float4*>(xr + c);
-    const float4 b = *reinterpret_cast<const float4*>(xr + c + 4);
+#pragma unroll
+  for (int i = 0; i < kNormChunks; ++i) {
+    const int c = (threadIdx.x + i * blockDim.x) * 8;
+    if (c >= H) break;
     const u32x4 gv = *reinterpret_cast<const u32x4*>(g + c);
     u32x4 o;
-    o[0] = pack_bf2(a.x * inv * bf2f(gv[0] & 0xffffu), a.y * inv * bf2f(gv[0] >> 16));
-    o[1] = pack_bf2(a.z * inv * bf2f(gv[1] & 0xffffu), a.w * inv * bf2f(gv[1] >> 16));
-    o[2] = pack_bf2(b.x * inv * bf2f(gv[2] & 0xffffu), b.y * inv * bf2f(gv[2] >> 16));
-    o[3] = pack_bf2(b.z * inv * bf2f(gv[3] & 0xffffu), b.w * inv * bf2f(gv[3] >> 16));
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      o[k] = pack_bf2(v[i][2 * k] * inv * bf2f(gv[k] & 0xffffu), v[i][2 * k + 1] * inv * bf2f(gv[k] >> 16));
     *reinterpret_cast<u32x4*>(out + frag_index(r, c, Rg)) = o;
   }
 }
 
-hipError_t launch_rmsnorm(const float* x, const uint16_t* g, const int32_t* gather, int R, int R_in, int H,
-                          float eps, uint16_t* out, int Rg, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm, dim3(16 * Rg), dim3(256), 0, s, x, g, gather, R, R_in, H, eps, out, Rg);
+hipError_t launch_rmsnorm(float* x, const float* part, int KS, const uint16_t* g, const int32_t* gather, int R,
+                          int R_in, int H, float eps, uint16_t* out, int Rg, hipStream_t s) {
+  hipLaunchKernelGGL(k_rmsnorm, dim3(16 * Rg), dim3(256), 0, s, x, part, KS, g, gather, R, R_in, H, eps, out, Rg);
   return hipGetLastError();
 }
 

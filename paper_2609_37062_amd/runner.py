@@ -122,15 +122,17 @@ class DeviceRun:
         torch.cuda.synchronize(self.device)
 
     # ---------------------------------------------------------- passes
-    def step(self):
-        """Enqueue one pass (decode_step when every q_len is 1, else prefill_chunk)."""
+    def step(self, stream=None):
+        """Enqueue one pass (decode_step when every q_len is 1, else prefill_chunk).
+
+        ``stream``: hipStream_t handle to launch on (default: the setup stream)."""
+        sp = self.sp if stream is None else stream
         if all(q == 1 for q in self.q_lens):
             self.eng.decode_step(self.ids.data_ptr(), self.logits.data_ptr(), self.next_ids.data_ptr(), self.ws,
-                                 self.ws_bytes, self.sp)
+                                 self.ws_bytes, sp)
         else:
             self.eng.prefill_chunk(self.ids.data_ptr(), self.logit_rows.data_ptr(), len(self.logit_rows),
-                                   self.logits.data_ptr(), self.next_ids.data_ptr(), self.ws, self.ws_bytes,
-                                   self.sp)
+                                   self.logits.data_ptr(), self.next_ids.data_ptr(), self.ws, self.ws_bytes, sp)
 
     def results(self):
         torch.cuda.synchronize(self.device)

@@ -73,6 +73,8 @@ SIGNATURES = [
     ("vsk_decode_step", C.c_int, [_VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     ("vsk_prefill_chunk", C.c_int, [_VP, _VP, _VP, _I32, _VP, _VP, _VP, _SZ, _VP]),
     ("vsk_argmax_sample", C.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
+    ("vsk_set_tuning", C.c_int, [_VP, _I32, _I32]),
+    ("vsk_set_probe", C.c_int, [_VP, _I32, C.POINTER(_VP), C.POINTER(_VP), _I32]),
     ("vsk_exec_counters", C.c_int, [_VP, _PI64, _I32]),
 ]
 
@@ -250,6 +252,15 @@ class Engine:
                       stream=None):
         self._ck(lib().vsk_prefill_chunk(self.h, ids_ptr, logit_rows_ptr, n_logit_rows, logits_ptr, next_ids_ptr,
                                          ws_ptr, ws_bytes, stream), "prefill_chunk")
+
+    def set_tuning(self, key, value):
+        self._ck(lib().vsk_set_tuning(self.h, key, value), "set_tuning")
+
+    def set_probe(self, which, begin_events, end_events):
+        n = len(begin_events)
+        B = (C.c_void_p * max(n, 1))(*begin_events)
+        E = (C.c_void_p * max(n, 1))(*end_events)
+        self._ck(lib().vsk_set_probe(self.h, which, B, E, n), "set_probe")
 
     def exec_counters(self):
         out = np.zeros(8, np.int64)
