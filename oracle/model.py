@@ -104,14 +104,17 @@ def _matmul(x, w):
 
 
 def forward(model, W, kv: PagedKV, batch, tokens, logit_rows, *, want_hidden=False,
-            lm_chunk=16384):
+            lm_chunk=16384, x0=None, layers=None):
     """One pass over the rows described by ``batch`` (see kvcache.build_batch).
 
     tokens     : int [R] token id of each row
-    logit_rows : int [n_out] rows whose logits are returned
-    Writes every row's K, V into ``kv`` at every layer.
+    logit_rows : int [n_out] rows whose logits are returned (None: no head)
+    x0         : optional residual stream [R][hidden] to start from instead of
+                 the embedding rows (the pass then covers only ``layers``)
+    layers     : the layer indices to run, in order (default: all)
+    Writes every row's K, V into ``kv`` at every layer it runs.
     Returns dict(z [n_out][V] float64, logits (bf16 values, float64), ids int32,
-    and optionally the final residual stream).
+    and optionally the final residual stream x).
     """
     m = model
     Hq, Hk, d = m.n_q_heads, m.n_kv_heads, m.head_dim
@@ -124,8 +127,8 @@ def forward(model, W, kv: PagedKV, batch, tokens, logit_rows, *, want_hidden=Fal
     kv_len = batch["kv_len"]
     table = batch["block_table"]
     bs = kv.block
-    x = W.rows("embed", tokens)
-    for layer in range(m.n_layers):
+    x = W.rows("embed", tokens) if x0 is None else np.array(x0, dtype=np.float64)
+    for layer in (range(m.n_layers) if layers is None else layers):
         # ---- attention block
         h = nm.bf16_round(nm.rmsnorm(x, W.get("attn_norm", layer), m.rms_eps))
         q = _matmul(h, W.get("wq", layer)).reshape(R, Hq, d)
@@ -155,6 +158,8 @@ def forward(model, W, kv: PagedKV, batch, tokens, logit_rows, *, want_hidden=Fal
         h2 = nm.bf16_round(nm.rmsnorm(x, W.get("mlp_norm", layer), m.rms_eps))
         a = nm.bf16_round(nm.silu(_matmul(h2, W.get("w_gate", layer))) * _matmul(h2, W.get("w_up", layer)))
         x = x + _matmul(a, W.get("w_down", layer))
+    if logit_rows is None:
+        return {"x": x}
     lr = np.asarray(logit_rows, np.int64)
     hf = nm.bf16_round(nm.rmsnorm(x[lr], W.get("final_norm", -1), m.rms_eps))
     z = np.empty((len(lr), m.vocab))

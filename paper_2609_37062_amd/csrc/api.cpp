@@ -482,9 +482,22 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
         return fail(h, VSK_E_ARG, "attention blocks per split must be a multiple of 8 in [8, 4096]");
       h->attn_bps = value;
       return VSK_OK;
+    case 1:
+      if (value < 0 || value > h->cfg.n_layers) return fail(h, VSK_E_ARG, "layer count out of range");
+      h->layers_run = value;
+      return VSK_OK;
     default:
       return fail(h, VSK_E_ARG, "unknown tuning key");
   }
+}
+
+int vsk_residual_copy(vsk_handle* h, void* dst_dev, int32_t n_rows, void* stream) {
+  if (!h || !dst_dev) return VSK_E_ARG;
+  if (!h->ws) return fail(h, VSK_E_STATE, "no workspace bound");
+  if (n_rows < 1 || n_rows > h->wl.max_rows) return fail(h, VSK_E_ARG, "row count out of range");
+  const size_t bytes = static_cast<size_t>(n_rows) * h->cfg.hidden * 4;
+  return hip_check(h, hipMemcpyAsync(dst_dev, h->ws + h->wl.x, bytes, hipMemcpyDeviceToDevice,
+                                     static_cast<hipStream_t>(stream)), "residual copy");
 }
 
 int vsk_exec_counters(const vsk_handle* h, int64_t* out, int32_t cap) {
@@ -573,7 +586,8 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
 
   float* part = reinterpret_cast<float*>(ws + wl.gemm_part);
   int pending = 0;  // K splits of the last residual projection, folded in by the next norm
-  for (int l = 0; l < c.n_layers; ++l) {
+  const int n_run = h.layers_run > 0 ? h.layers_run : c.n_layers;
+  for (int l = 0; l < n_run; ++l) {
     const uint8_t* L = P + h.pl.layer_bytes * l;
     // attention block
     TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(L + h.pl.l.attn_norm), nullptr, R, R, H,
@@ -613,6 +627,14 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     TRY(probed(1, [&] { return launch_gemm(ga, p_d, EPI_RESID, s); }));
     pending = p_d.ks > 1 ? p_d.ks : 0;
   }
+  // inspection runs fold the last split partials into x for every row, so the
+  // residual stream of all rows can be read back (the product path folds only
+  // the logit rows, inside the final norm)
+  if (h.layers_run > 0 && pending > 0) {
+    TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(P + h.pl.final_norm), nullptr, R, R, H,
+                       c.rms_eps, act0, Rg, s));
+    pending = 0;
+  }
   // final norm (gathered logit rows) + lm_head + greedy argmax
   const int Ro = pa.n_logit_rows;
   const int Rgo = (Ro + 15) / 16;
@@ -632,8 +654,8 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   if (pa.next_ids) TRY(launch_argmax_partials(ga.am_val, ga.am_idx, p_lm.n_groups, Ro, pa.next_ids, s));
 #undef TRY
   h.counters[0] += 1;
-  h.counters[1] += 4 * c.n_layers + 1;
-  h.counters[2] += c.n_layers;
+  h.counters[1] += 4 * n_run + 1;
+  h.counters[2] += n_run;
   h.counters[3] = aa.max_splits;
   h.counters[4] = p_d.ks;
   return hipSuccess;

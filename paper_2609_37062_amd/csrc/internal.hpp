@@ -113,6 +113,7 @@ struct Handle {
   bool batch_uploaded = false;
   // tuning
   int attn_bps = kAttnDefaultBps;
+  int layers_run = 0;  // inspection: run only the first layers_run layers (0 = all)
   // workspace
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;

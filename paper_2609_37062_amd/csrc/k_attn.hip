@@ -103,13 +103,18 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
     ps += shfl_xor(ps, 32);
     l = l * alpha + ps;
     m = m_new;
-    u32x2 pf;
+    // P = P_hi + P_lo with both parts bf16 (about 16 significant bits), so the
+    // probabilities are not cut to bf16 precision before P V
+    u32x2 pf, pl;
     pf[0] = pack_bf2(p[0], p[1]);
     pf[1] = pack_bf2(p[2], p[3]);
+    pl[0] = pack_bf2(p[0] - bf2f(pf[0] & 0xffffu), p[1] - bf2f(pf[0] >> 16));
+    pl[1] = pack_bf2(p[2] - bf2f(pf[1] & 0xffffu), p[3] - bf2f(pf[1] >> 16));
 #pragma unroll
     for (int c = 0; c < VC; ++c) {
       o[c] *= alpha;
       o[c] = mfma_16x16x16(vf[c], pf, o[c]);  // lane holds O[head h][dim 16c + 4*quad + r]
+      o[c] = mfma_16x16x16(vf[c], pl, o[c]);
     }
   };
   auto load = [&](u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {

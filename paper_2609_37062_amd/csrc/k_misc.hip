@@ -46,7 +46,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ x, const fl
                                                  const uint16_t* __restrict__ g, const int32_t* __restrict__ gather,
                                                  int R, int R_in, int H, float eps, uint16_t* __restrict__ out,
                                                  int Rg) {
-  __shared__ float s_red[8];
+  __shared__ double s_red[8];
   const int r = blockIdx.x;
   const int src = r < R ? (gather ? gather[r] : r) : -1;
   if (src < 0 || src >= R_in) {
@@ -56,7 +56,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ x, const fl
   }
   float* xr = x + static_cast<size_t>(src) * H;
   float v[kNormChunks][8];
-  float ss = 0.f;
+  double ss = 0.0;  // the row statistics and the scaling are done in double
 #pragma unroll
   for (int i = 0; i < kNormChunks; ++i) {
     const int c = (threadIdx.x + i * blockDim.x) * 8;
@@ -77,15 +77,15 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ x, const fl
     v[i][0] = a.x; v[i][1] = a.y; v[i][2] = a.z; v[i][3] = a.w;
     v[i][4] = b.x; v[i][5] = b.y; v[i][6] = b.z; v[i][7] = b.w;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) ss += v[i][k] * v[i][k];
+    for (int k = 0; k < 8; ++k) ss += static_cast<double>(v[i][k]) * v[i][k];
   }
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) ss += shfl_xor(ss, m);
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
   if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  float tot = 0.f;
+  double tot = 0.0;
   for (int i = 0; i < (int)(blockDim.x >> 6); ++i) tot += s_red[i];
-  const float inv = 1.0f / sqrtf(tot / static_cast<float>(H) + eps);
+  const double inv = 1.0 / sqrt(tot / static_cast<double>(H) + static_cast<double>(eps));
 #pragma unroll
   for (int i = 0; i < kNormChunks; ++i) {
     const int c = (threadIdx.x + i * blockDim.x) * 8;
@@ -94,7 +94,8 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ x, const fl
     u32x4 o;
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      o[k] = pack_bf2(v[i][2 * k] * inv * bf2f(gv[k] & 0xffffu), v[i][2 * k + 1] * inv * bf2f(gv[k] >> 16));
+      o[k] = d2bf(v[i][2 * k] * inv * bf2f(gv[k] & 0xffffu)) |
+             (d2bf(v[i][2 * k + 1] * inv * bf2f(gv[k] >> 16)) << 16);
     *reinterpret_cast<u32x4*>(out + frag_index(r, c, Rg)) = o;
   }
 }

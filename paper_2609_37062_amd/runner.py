@@ -134,6 +134,17 @@ class DeviceRun:
             self.eng.prefill_chunk(self.ids.data_ptr(), self.logit_rows.data_ptr(), len(self.logit_rows),
                                    self.logits.data_ptr(), self.next_ids.data_ptr(), self.ws, self.ws_bytes, sp)
 
+    def set_layers(self, n):
+        """Inspection: run only the first n layers in the following passes (0 = all)."""
+        self.eng.set_tuning(1, n)
+
+    def residual(self):
+        """The fp32 residual stream x [rows][hidden] after the last pass (float64 copy)."""
+        x = torch.empty((self.w.n_rows, self.m.hidden), dtype=torch.float32, device=self.device)
+        self.eng.residual_copy(x.data_ptr(), self.w.n_rows, self.sp)
+        torch.cuda.synchronize(self.device)
+        return x.cpu().numpy().astype(np.float64)
+
     def results(self):
         torch.cuda.synchronize(self.device)
         lg = self.logits.view(torch.bfloat16).float().cpu().numpy().astype(np.float64)

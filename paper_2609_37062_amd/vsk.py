@@ -74,6 +74,7 @@ SIGNATURES = [
     ("vsk_prefill_chunk", C.c_int, [_VP, _VP, _VP, _I32, _VP, _VP, _VP, _SZ, _VP]),
     ("vsk_argmax_sample", C.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
     ("vsk_set_tuning", C.c_int, [_VP, _I32, _I32]),
+    ("vsk_residual_copy", C.c_int, [_VP, _VP, _I32, _VP]),
     ("vsk_set_probe", C.c_int, [_VP, _I32, C.POINTER(_VP), C.POINTER(_VP), _I32]),
     ("vsk_exec_counters", C.c_int, [_VP, _PI64, _I32]),
 ]
@@ -255,6 +256,9 @@ class Engine:
 
     def set_tuning(self, key, value):
         self._ck(lib().vsk_set_tuning(self.h, key, value), "set_tuning")
+
+    def residual_copy(self, dst_ptr, n_rows, stream=None):
+        self._ck(lib().vsk_residual_copy(self.h, dst_ptr, n_rows, stream), "residual_copy")
 
     def set_probe(self, which, begin_events, end_events):
         n = len(begin_events)

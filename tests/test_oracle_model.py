@@ -184,3 +184,24 @@ def test_first_token_attends_to_itself_only():
     v = nm.bf16_round(h @ W.get("wv", 0).T)
     # q heads 0,1 map to kv heads 0,1; o = v, then x = x0 + o (Wo = I)
     np.testing.assert_allclose(out["x"], x0 + v, rtol=0, atol=1e-12)
+
+
+def test_layer_range_composes_to_the_whole_pass():
+    """Running layers [0, k) then [k, L) from the first part's residual is the whole pass."""
+    m = PIN
+    W = GeneratedWeights(m, seed=21, cache=True)
+    tokens = np.random.default_rng(22).integers(0, m.vocab, size=20)
+    perm = list(range(16))
+    a = BlockAllocator(16, 16)
+    a.seq_create(0)
+    a.seq_set_blocks(0, perm[:2], 0)
+    a.reserve(0, 20)
+    b = build_batch(a, [0], [20])
+    kv1 = PagedKV(m.n_layers, 16, m.n_kv_heads, m.head_dim)
+    kv2 = PagedKV(m.n_layers, 16, m.n_kv_heads, m.head_dim)
+    full = forward(m, W, kv1, b, tokens, [19], want_hidden=True)
+    part = forward(m, W, kv2, b, tokens, None, layers=[0])
+    rest = forward(m, W, kv2, b, tokens, [19], x0=part["x"], layers=[1], want_hidden=True)
+    np.testing.assert_array_equal(full["x"], rest["x"])
+    np.testing.assert_array_equal(full["z"], rest["z"])
+    np.testing.assert_array_equal(kv1.K, kv2.K)
