@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 import numpy as np  # noqa: E402
 
 PEAK_HBM = 8.0e12  # MI355X HBM3E, bytes/s
+CALIB_BYTES = 512 << 20  # plain device-to-device copy used to calibrate byte counters
 
 
 def parse():
@@ -42,6 +43,9 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-layers", type=int, default=2, help="layers in the CPU oracle sample")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="for rocprofv3 runs: set up the workload, run one plain copy of "
+                         f"{CALIB_BYTES >> 20} MiB (counter calibration), then --steps passes; no JSON")
     return ap.parse_args()
 
 
@@ -90,6 +94,20 @@ def step_bytes(w):
 def gateup_bytes(m, R):
     """Algorithmic bytes of one gate/up launch: its weights, its input rows, its output."""
     return 2 * m.ffn * m.hidden * 2 + R * m.hidden * 2 + R * m.ffn * 2
+
+
+def gateup_traffic():
+    """Counter-measured HBM bytes per gate/up launch from profiles/, or None when
+    the projection kernel's source has changed since the counters were taken."""
+    import hashlib
+    try:
+        prof = json.load(open(os.path.join(ROOT, "profiles", "gateup_3b_b16_traffic.json")))
+        src = open(os.path.join(ROOT, "paper_2609_37062_amd", "csrc", "k_gemm.hip"), "rb").read()
+    except OSError:
+        return None
+    if hashlib.sha256(src).hexdigest()[:16] != prof.get("k_gemm_source_sha256_16"):
+        return None
+    return prof["traffic_bytes_per_launch"]
 
 
 def time_steps(torch, fn, steps, warmup, stream):
@@ -207,6 +225,21 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     w = workload(a.workload)
+    if a.profile_pass:
+        from paper_2609_37062_amd.runner import DeviceRun
+        d = DeviceRun(w)
+        src = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        for _ in range(a.steps):
+            d.step()
+        torch.cuda.synchronize()
+        print(f"[bench] profile pass: {w.name}, {a.steps} steps, calibration copy {CALIB_BYTES} bytes",
+              file=sys.stderr)
+        return
     r = measure(torch, w, a.steps, a.warmup, not a.no_graph)
     ms = min(r["ms_eager"], r.get("ms_graph", float("inf")))
     tokps = w.n_rows / (ms / 1e3)
@@ -238,7 +271,8 @@ def main():
         "step_hbm_frac": round(sb / (ms / 1e3) / PEAK_HBM, 4),
         "roofline": {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm, EPI_SWIGLU)",
                      "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_HBM, 4),
+                     "traffic": gateup_traffic() if a.workload == 2 else None,
                      "bytes_per_launch": gb, "avg_launch_ms": round(r["gateup_ms"], 5)},
         "exec_counters": r["counters"],
     }
