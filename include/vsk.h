@@ -209,15 +209,15 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
 
 /* Launch-shape tuning (the analogue of a device-tuned tile table).  Results
  * do not depend on it beyond floating-point summation order.
- * key 0: attention 16-token blocks per split-K work item (multiple of 8,
- *        8..4096; default 32).
+ * key 0: attention 16-token blocks per split-K work item (multiple of 8 in
+ *        8..512), or 0 (the default) for automatic: 32 when fewer than 256
+ *        (row, KV head) pairs are in the pass, else 128.
  * key 1: inspection only -- run just the first `value` layers before the
  *        final norm and lm_head (0 = all layers), for layer-local checks. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the
- * bound workspace by the last decode pass (all rows; after a prefill pass
- * only the logit rows are final) to dst_dev. */
+ * bound workspace by the last decode or prefill pass (all rows) to dst_dev. */
 int vsk_residual_copy(vsk_handle* h, void* dst_dev, int32_t n_rows, void* stream);
 
 /* Counters of what the last pass executed (kernel variants, split factors),

@@ -43,15 +43,6 @@ PackedLayout packed_layout(const vsk_model_cfg& c) {
 
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// partial-buffer bytes of a projection's K splits over up to R_max rows
-static void gemm_ws_need(int N, int K, int R_max, int epi, size_t& part) {
-  for (int Rg = 1; Rg <= ceil_div(R_max, 16); ++Rg) {
-    const int R = std::min(16 * Rg, R_max);
-    const GemmPlan p = plan_gemm(N, K, R, epi);
-    if (p.ks > 1) part = std::max(part, static_cast<size_t>(p.ks) * R * N * 4);
-  }
-}
-
 WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len) {
   WsLayout w;
   w.max_rows = max_rows;
@@ -59,23 +50,23 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   w.max_kv_len = max_kv_len;
   w.Rg = ceil_div(max_rows, 16);
   w.max_splits = attn_splits(max_kv_len, kAttnMinBps);
-  const size_t H = c.hidden, F = c.ffn, Nq = static_cast<size_t>(c.n_q_heads) * c.head_dim,
-               Nkv = static_cast<size_t>(c.n_kv_heads) * c.head_dim;
+  const size_t H = c.hidden, F = c.ffn, Nq = static_cast<size_t>(c.n_q_heads) * c.head_dim;
   const size_t Rp = static_cast<size_t>(w.Rg) * 16;
   const int G = c.n_q_heads / c.n_kv_heads;
   size_t o = 0;
   w.x = o; o = align_up(o + static_cast<size_t>(max_rows) * H * 4);
-  w.act0 = o; o = align_up(o + Rp * std::max(H, Nq) * 2);
-  w.act1 = o; o = align_up(o + Rp * F * 2);
+  w.fa = o; o = align_up(o + Rp * std::max(H, Nq) * 2);
+  w.fb = o; o = align_up(o + Rp * H * 2);
+  w.fc = o; o = align_up(o + Rp * F * 2);
   w.q = o; o = align_up(o + static_cast<size_t>(max_rows) * Nq * 2);
   const size_t rh = static_cast<size_t>(max_rows) * c.n_kv_heads;
   w.att_o = o; o = align_up(o + rh * w.max_splits * G * c.head_dim * 4);
   w.att_ml = o; o = align_up(o + rh * w.max_splits * G * 8);
-  size_t part = 0;
-  gemm_ws_need(c.hidden, static_cast<int>(Nq), max_rows, EPI_RESID, part);
-  gemm_ws_need(c.hidden, c.ffn, max_rows, EPI_RESID, part);
-  w.gemm_part = o; o = align_up(o + part);
-  // lm_head partials: n_groups x rows
+  w.att_cnt = o; o = align_up(o + rh * 4);  // zeroed at init, left zero by every pass
+  // x^2 partials: at most one per 16 columns of the hidden size, per row
+  w.ssq = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
+  w.ssq_c = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
+  // lm_head argmax partials: n_groups x rows
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
   w.total = o;
@@ -478,8 +469,8 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
   if (!h) return VSK_E_ARG;
   switch (key) {
     case 0:
-      if (value < kAttnMinBps || value % 8 != 0 || value > 4096)
-        return fail(h, VSK_E_ARG, "attention blocks per split must be a multiple of 8 in [8, 4096]");
+      if (value != 0 && (value < kAttnMinBps || value % 8 != 0 || value > kAttnMaxBps))
+        return fail(h, VSK_E_ARG, "attention blocks per split must be 0 (auto) or a multiple of 8 in [8, 512]");
       h->attn_bps = value;
       return VSK_OK;
     case 1:
@@ -520,11 +511,20 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   const int H = c.hidden, F = c.ffn, d = c.head_dim, Nq = c.n_q_heads * d, Nkv = c.n_kv_heads * d;
   uint8_t* ws = pa.ws;
   float* x = reinterpret_cast<float*>(ws + wl.x);
-  uint16_t* act0 = reinterpret_cast<uint16_t*>(ws + wl.act0);
-  uint16_t* act1 = reinterpret_cast<uint16_t*>(ws + wl.act1);
+  // frag buffers: A = normed input of QKV, then attention output; B = normed
+  // input of gate/up; C = SwiGLU output
+  uint16_t* fa = reinterpret_cast<uint16_t*>(ws + wl.fa);
+  uint16_t* fb = reinterpret_cast<uint16_t*>(ws + wl.fb);
+  uint16_t* fc = reinterpret_cast<uint16_t*>(ws + wl.fc);
   uint16_t* q = reinterpret_cast<uint16_t*>(ws + wl.q);
+  double* ssq = reinterpret_cast<double*>(ws + wl.ssq);
   const uint8_t* P = h.packed;
   typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+  const int n_run = h.layers_run > 0 ? h.layers_run : c.n_layers;
+  auto norm_gain = [&](int layer, bool mlp) {
+    return reinterpret_cast<const uint16_t*>(P + h.pl.layer_bytes * layer + (mlp ? h.pl.l.mlp_norm : h.pl.l.attn_norm));
+  };
+  const uint16_t* final_gain = reinterpret_cast<const uint16_t*>(P + h.pl.final_norm);
   hipError_t e;
 #define TRY(call)                      \
   do {                                 \
@@ -543,12 +543,15 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     return hipSuccess;
   };
 
-  TRY(launch_embed(reinterpret_cast<const uint16_t*>(P + h.pl.embed), pa.ids, R, H, c.vocab, x, s));
+  TRY(launch_embed(reinterpret_cast<const uint16_t*>(P + h.pl.embed), pa.ids, R, H, c.vocab, norm_gain(0, false), x,
+                   fa, Rg, ssq, s));
+  int ssq_parts = 1;
 
   GemmArgs ga{};
-  ga.part = reinterpret_cast<float*>(ws + wl.gemm_part);
   ga.R = R;
   ga.Rg = Rg;
+  ga.norm_dim = H;
+  ga.eps = c.rms_eps;
   ga.pool = h.pool;
   ga.n_blocks = h.n_blocks;
   ga.Hkv = c.n_kv_heads;
@@ -558,6 +561,9 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ga.slot = b.slot;
   ga.pos = b.pos;
   ga.rope = reinterpret_cast<const float2*>(P + h.pl.rope);
+  ga.x = x;
+  ga.hg_Rg = Rg;
+  ga.out_Rg = Rg;
 
   AttnArgs aa{};
   aa.q = q;
@@ -572,11 +578,12 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   aa.row_seq = b.row_seq;
   aa.pos = b.pos;
   aa.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d)));
-  aa.bps = h.attn_bps;
-  aa.max_splits = attn_splits(b.max_kv_len, h.attn_bps);
+  aa.bps = h.attn_bps > 0 ? h.attn_bps : attn_auto_bps(R, c.n_kv_heads);
+  aa.max_splits = attn_splits(b.max_kv_len, aa.bps);
   aa.part_o = reinterpret_cast<float*>(ws + wl.att_o);
   aa.part_ml = reinterpret_cast<float2*>(ws + wl.att_ml);
-  aa.out = act0;
+  aa.counter = reinterpret_cast<int*>(ws + wl.att_cnt);
+  aa.out = fa;
   aa.out_Rg = Rg;
 
   const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV);
@@ -584,69 +591,73 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU);
   const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID);
 
-  float* part = reinterpret_cast<float*>(ws + wl.gemm_part);
-  int pending = 0;  // K splits of the last residual projection, folded in by the next norm
-  const int n_run = h.layers_run > 0 ? h.layers_run : c.n_layers;
   for (int l = 0; l < n_run; ++l) {
     const uint8_t* L = P + h.pl.layer_bytes * l;
-    // attention block
-    TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(L + h.pl.l.attn_norm), nullptr, R, R, H,
-                       c.rms_eps, act0, Rg, s));
+    // attention block: QKV (norm folded: x^2 partials of the previous residual)
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wqkv);
-    ga.X = reinterpret_cast<const u4*>(act0);
+    ga.X = reinterpret_cast<const u4*>(fa);
     ga.Kt = H / 32;
     ga.N = Nq + 2 * Nkv;
+    ga.ssq = ssq;
+    ga.ssq_parts = ssq_parts;
     ga.out = q;
     ga.layer = l;
     TRY(probed(2, [&] { return launch_gemm(ga, p_qkv, EPI_QKV, s); }));
     aa.layer = l;
     TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
+    // O projection: x += o Wo^T; emits the MLP norm's input frags and x^2 partials
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);
-    ga.X = reinterpret_cast<const u4*>(act0);
+    ga.X = reinterpret_cast<const u4*>(fa);
     ga.Kt = Nq / 32;
     ga.N = H;
-    ga.x = x;
-    ga.part = part;
+    ga.ssq = nullptr;
+    ga.hg_out = fb;
+    ga.g_next = norm_gain(l, true);
+    ga.ssq_out = ssq;
     TRY(probed(3, [&] { return launch_gemm(ga, p_o, EPI_RESID, s); }));
-    pending = p_o.ks > 1 ? p_o.ks : 0;
+    ssq_parts = p_o.n_groups;
     // MLP block
-    TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(L + h.pl.l.mlp_norm), nullptr, R, R, H,
-                       c.rms_eps, act0, Rg, s));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wgu);
-    ga.X = reinterpret_cast<const u4*>(act0);
+    ga.X = reinterpret_cast<const u4*>(fb);
     ga.Kt = H / 32;
     ga.N = 2 * F;
-    ga.out = act1;
-    ga.out_Rg = Rg;
+    ga.ssq = ssq;
+    ga.ssq_parts = ssq_parts;
+    ga.out = fc;
     TRY(probed(0, [&] { return launch_gemm(ga, p_gu, EPI_SWIGLU, s); }));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wd);
-    ga.X = reinterpret_cast<const u4*>(act1);
+    ga.X = reinterpret_cast<const u4*>(fc);
     ga.Kt = F / 32;
     ga.N = H;
-    ga.x = x;
+    ga.ssq = nullptr;
+    ga.hg_out = fa;
+    ga.g_next = (l + 1 < n_run) ? norm_gain(l + 1, false) : final_gain;
+    ga.ssq_out = ssq;
     TRY(probed(1, [&] { return launch_gemm(ga, p_d, EPI_RESID, s); }));
-    pending = p_d.ks > 1 ? p_d.ks : 0;
+    ssq_parts = p_d.n_groups;
+    ga.hg_out = nullptr;
+    ga.ssq_out = nullptr;
   }
-  // inspection runs fold the last split partials into x for every row, so the
-  // residual stream of all rows can be read back (the product path folds only
-  // the logit rows, inside the final norm)
-  if (h.layers_run > 0 && pending > 0) {
-    TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(P + h.pl.final_norm), nullptr, R, R, H,
-                       c.rms_eps, act0, Rg, s));
-    pending = 0;
-  }
-  // final norm (gathered logit rows) + lm_head + greedy argmax
+  // lm_head over the logit rows (final norm folded), then greedy argmax
   const int Ro = pa.n_logit_rows;
   const int Rgo = (Ro + 15) / 16;
-  TRY(launch_rmsnorm(x, part, pending, reinterpret_cast<const uint16_t*>(P + h.pl.final_norm), pa.logit_rows, Ro, R,
-                     H, c.rms_eps, act0, Rgo, s));
+  const uint16_t* Xl = fa;
+  const double* ssq_l = ssq;
+  if (pa.logit_rows != nullptr) {
+    double* ssq_c = reinterpret_cast<double*>(ws + wl.ssq_c);
+    TRY(launch_gather_rows(fa, Rg, ssq, ssq_parts, R, pa.logit_rows, Ro, H, fb, Rgo, ssq_c, s));
+    Xl = fb;
+    ssq_l = ssq_c;
+  }
   const GemmPlan p_lm = plan_gemm(c.vocab, H, Ro, EPI_LOGITS);
   ga.W = reinterpret_cast<const u4*>(P + h.pl.lm_head);
-  ga.X = reinterpret_cast<const u4*>(act0);
+  ga.X = reinterpret_cast<const u4*>(Xl);
   ga.Kt = H / 32;
   ga.N = c.vocab;
   ga.R = Ro;
   ga.Rg = Rgo;
+  ga.ssq = ssq_l;
+  ga.ssq_parts = ssq_parts;
   ga.out = pa.logits;
   ga.am_val = reinterpret_cast<float*>(ws + wl.am_part);
   ga.am_idx = reinterpret_cast<int*>(ws + wl.am_part + static_cast<size_t>((c.vocab + 15) / 16) * wl.max_rows * 4);
@@ -657,7 +668,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   h.counters[1] += 4 * n_run + 1;
   h.counters[2] += n_run;
   h.counters[3] = aa.max_splits;
-  h.counters[4] = p_d.ks;
+  h.counters[4] = p_d.n_groups;
   return hipSuccess;
 }
 

@@ -18,6 +18,7 @@ struct AttnArgs {
   int max_splits;  // split stride of the partial buffers
   float* part_o;   // [R][Hkv][max_splits][G][hd]
   float2* part_ml; // [R][Hkv][max_splits][G]
+  int* counter;    // [R][Hkv] arrivals of splits, zero between passes
   uint16_t* out;   // o frags (K = Nq)
   int out_Rg;
 };

@@ -14,10 +14,17 @@ struct GemmArgs {
   int N;        // output columns
   int R;        // valid rows
   int Rg;       // 16-row groups of the X frag buffer
-  int KS;       // K splits across workgroups (set from the plan)
-  float* part;  // RESID with KS > 1: partials [KS][R][N]
+  // folded RMSNorm, consumer side: r = 1/sqrt(sum_p ssq[p][row] / norm_dim + eps)
+  const double* ssq;  // [ssq_parts][R] partial sums of x^2, or null (no scaling)
+  int ssq_parts;
+  int norm_dim;
+  float eps;
   // epilogue operands
-  float* x;       // RESID: fp32 residual [R][N]
+  float* x;              // RESID: fp32 residual [R][N]
+  uint16_t* hg_out;      // RESID: frags of bf16(x * g_next) (hg_Rg groups), or null
+  int hg_Rg;
+  const uint16_t* g_next;  // RESID: gains of the next RMSNorm [N]
+  double* ssq_out;       // RESID: partial sums of x^2 [n_groups][R], or null
   uint16_t* out;  // QKV: q [R][Nq]; SWIGLU: frags (out_Rg); LOGITS: logits [R][N]
   int out_Rg;
   uint16_t* pool;  // QKV: KV pool
@@ -32,9 +39,8 @@ struct GemmArgs {
 struct GemmPlan {
   int mg = 1;        // 16-row groups per tile
   int m_tiles = 1;   // tiles along the rows
-  int n_groups = 1;  // workgroups along N
-  int ks = 1;        // K splits across workgroups
-  bool wide = false; // four N tiles per wave (mg == 1 only)
+  int n_groups = 1;  // workgroups along N (also the number of x^2 partials a RESID emits)
+  int nt = 1;        // N tiles per wave (mg == 1)
 };
 
 GemmPlan plan_gemm(int N, int K, int R, int epi);

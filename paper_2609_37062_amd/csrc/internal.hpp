@@ -83,16 +83,21 @@ struct BatchDev {
 // ---------------------------------------------------------------- workspace
 struct WsLayout {
   int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
-  size_t x, act0, act1, q, att_o, att_ml, gemm_part, am_part, total;
+  size_t x, fa, fb, fc, q, att_o, att_ml, att_cnt, ssq, ssq_c, am_part, total;
 };
 
 // attention split: 16-token blocks per split-K work item (tunable, >= kAttnMinBps)
 constexpr int kAttnMinBps = 8;
-constexpr int kAttnDefaultBps = 32;
+constexpr int kAttnMaxBps = 512;
 inline int attn_splits(int kv_len, int bps) {
   const int nb = (kv_len + kBlock - 1) / kBlock;
   return (nb + bps - 1) / bps;
 }
+// Default split size.  One workgroup streams at most ~60 GB/s, so with few
+// (row, KV head) pairs long contexts are cut into 512-token splits to spread
+// them over the compute units; once the pairs alone fill the 256 CUs, splits
+// of 2048 tokens avoid most of the merge work.
+inline int attn_auto_bps(int n_rows, int n_kv_heads) { return n_rows * n_kv_heads >= 256 ? 128 : 32; }
 
 struct Handle {
   vsk_model_cfg cfg{};
@@ -112,7 +117,7 @@ struct Handle {
   BatchDev bd;
   bool batch_uploaded = false;
   // tuning
-  int attn_bps = kAttnDefaultBps;
+  int attn_bps = 0;  // 0: attn_auto_bps
   int layers_run = 0;  // inspection: run only the first layers_run layers (0 = all)
   // workspace
   uint8_t* ws = nullptr;

@@ -5,12 +5,14 @@
 // sequence's block table (paper, "Invariants": each layer reads its own
 // cached K,V; Algorithm 1 keeps attention's launch shape).  A workgroup owns
 // one (row, KV head, split) and its eight waves take the split's 16-token
-// blocks in turn.  Per block a wave computes S = K q with
+// blocks as contiguous ranges.  The split's block-table entries are staged in
+// LDS first; each wave then keeps NB blocks of K/V loads in flight ahead of
+// the block it processes.  Per block a wave computes S = K q with
 // v_mfma_f32_16x16x32_bf16 (16 tokens x up to 16 heads), an online softmax in
 // the base-2 domain, and O^T += V^T P^T with v_mfma_f32_16x16x16_bf16, so the
 // softmax row lives in the same lanes as the output it rescales.  The waves
-// merge in LDS; splits write (m, l, O) partials that a second small kernel
-// merges in split order.
+// merge in LDS; with several splits the last workgroup to finish a (row, KV
+// head) merges the splits' (m, l, O) partials in split order.
 // Decode attention reads about group-size flops per byte of KV, so it is
 // bound by HBM, not by the matrix cores.
 #include <cmath>
@@ -22,13 +24,22 @@ namespace vsk {
 
 constexpr int kAttnWaves = 8;
 
-template <int D>
+// agent-scope (all XCDs) coherent accesses for the split partials
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int D, int NB>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   constexpr int KC = D / 32;  // K chunks (1 KiB) per block
   constexpr int VC = D / 16;  // V chunks (512 B) per block
   __shared__ float s_m[kAttnWaves][16];
   __shared__ float s_l[kAttnWaves][16];
   __shared__ f32x4 s_o[kAttnWaves - 1][VC][64];
+  __shared__ int32_t s_tbl[kAttnMaxBps];
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -42,7 +53,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   const int32_t* table = a.block_table + static_cast<size_t>(seq) * a.max_blocks;
   const int b_lo = split * a.bps;
   const int b_hi = min(nb, b_lo + a.bps);
-
+  // the split's block-table entries, staged once for all waves
+  for (int i = threadIdx.x; i < b_hi - b_lo; i += blockDim.x) s_tbl[i] = table[b_lo + i];
   const int h = lane & 15;       // query head within the group (valid if h < G)
   const int quad = lane >> 4;    // token quarter / k sub-range
   // q as the B operand of S = K q: lane holds q[h][32c + 8*quad .. +7]
@@ -117,8 +129,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
       o[c] = mfma_16x16x16(vf[c], pl, o[c]);
     }
   };
-  auto load = [&](u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {
-    const size_t blk = static_cast<size_t>(table[b]);
+  auto load = [&](u32x4 (&kf)[KC], u32x2 (&vf)[VC], int32_t tb) {
+    const size_t blk = static_cast<size_t>(tb);
     const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
     const u32x2* vp = reinterpret_cast<const u32x2*>(vbase + blk * kv_stride) + lane;
 #pragma unroll
@@ -127,18 +139,29 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
     for (int c = 0; c < VC; ++c) vf[c] = vp[c * 64];
   };
 
-  // this wave's blocks b_lo + w, + kAttnWaves, ...: two blocks in flight
-  u32x4 kA[KC], kB[KC];
-  u32x2 vA[VC], vB[VC];
-  int b = b_lo + w;
-  if (b < b_hi) load(kA, vA, b);
-  for (; b < b_hi; b += 2 * kAttnWaves) {
-    const int bn = b + kAttnWaves;
-    if (bn < b_hi) load(kB, vB, bn);
-    process(kA, vA, b);
-    if (bn >= b_hi) break;
-    if (bn + kAttnWaves < b_hi) load(kA, vA, bn + kAttnWaves);
-    process(kB, vB, bn);
+  __syncthreads();  // s_tbl
+  // this wave's blocks: a contiguous range of the split, kept NB blocks ahead.
+  // Loads past the range re-read its last block and the final round is
+  // peeled, so the loop's loads are unconditional and stay in flight.
+  const int per = (b_hi - b_lo + kAttnWaves - 1) / kAttnWaves;
+  const int w_lo = min(b_hi - b_lo, w * per);
+  const int cnt = min(b_hi - b_lo, w_lo + per) - w_lo;
+  if (cnt > 0) {
+    u32x4 kf[NB][KC];
+    u32x2 vf[NB][VC];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) load(kf[i], vf[i], s_tbl[w_lo + min(i, cnt - 1)]);
+    int base = 0;
+    for (; base + NB < cnt; base += NB) {
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        process(kf[i], vf[i], b_lo + w_lo + base + i);
+        load(kf[i], vf[i], s_tbl[w_lo + min(base + i + NB, cnt - 1)]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      if (base + i < cnt) process(kf[i], vf[i], b_lo + w_lo + base + i);
   }
 
   // ---- merge the waves of this workgroup
@@ -187,76 +210,85 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
     return;
   }
 
-  // ---- several splits: publish this split's (m, l, O); k_attn_combine merges them
+  // ---- several splits: publish this split's (m, l, O); the workgroup that
+  // completes a (row, KV head) last merges all of them in split order.
+  // Partials are written and read with agent-scope atomic accesses, which
+  // bypass the non-coherent per-XCD L2 copies; a store is complete (visible
+  // at agent scope) once the wave's memory counter has drained, and only
+  // then is the arrival counted.  No workgroup waits for another.
   const size_t rh = static_cast<size_t>(row) * a.Hkv + hk;
   if (w == 0 && h < G) {
     float* po = a.part_o + ((rh * a.max_splits + split) * G + h) * D;
 #pragma unroll
     for (int c = 0; c < VC; ++c)
-      *reinterpret_cast<float4*>(po + 16 * c + 4 * quad) = make_float4(o[c][0], o[c][1], o[c][2], o[c][3]);
-    if (quad == 0) a.part_ml[(rh * a.max_splits + split) * G + h] = make_float2(m, l);
-  }
-}
-
-// Merge the split partials of rows with more than one split, in split order:
-// O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.  One workgroup per (KV head, row).
-constexpr int kMaxSplits = 128;  // max_pos <= 16384 with at least 8 blocks per split
-__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
-  __shared__ float s_f[kMaxSplits][16];  // per split and head: 2^(m_s - M)
-  __shared__ float s_invL[16];
-  const int hk = blockIdx.x, row = blockIdx.y;
-  const int kv_len = a.pos[row] + 1;
-  const int n_splits = (((kv_len + kBlock - 1) / kBlock) + a.bps - 1) / a.bps;
-  if (n_splits <= 1) return;
-  const int G = a.G, D = a.hd;
-  const size_t rh = static_cast<size_t>(row) * a.Hkv + hk;
-  const float2* ml = a.part_ml + rh * a.max_splits * G;
-  if (threadIdx.x < G) {
-    const int hh = threadIdx.x;
-    float M = -INFINITY;
-    for (int s = 0; s < n_splits; ++s) M = fmaxf(M, ml[s * G + hh].x);
-    float L = 0.f;
-    for (int s = 0; s < n_splits; ++s) {
-      const float2 v = ml[s * G + hh];
-      const float f = exp2f(v.x - M);
-      s_f[s][hh] = f;
-      L += v.y * f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) st_agent(po + 16 * c + 4 * quad + r, o[c][r]);
+    if (quad == 0) {
+      float* pm = reinterpret_cast<float*>(a.part_ml + (rh * a.max_splits + split) * G + h);
+      st_agent(pm, m);
+      st_agent(pm + 1, l);
     }
-    s_invL[hh] = 1.f / L;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  __shared__ int s_last;
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(a.counter + rh, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = prev == n_splits - 1;
   }
   __syncthreads();
-  const float* po = a.part_o + rh * a.max_splits * G * D;
+  if (!s_last) return;
+
+  // merge: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, in split order
+  constexpr int kC = 8;  // splits read with one round of independent loads
+  const float* pml = reinterpret_cast<const float*>(a.part_ml + rh * a.max_splits * G);
+  const float* pob = a.part_o + rh * a.max_splits * G * D;
   for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
     const int hh = idx / D, e = idx % D;
-    float acc = 0.f;
-    int s = 0;
-    for (; s + 4 <= n_splits; s += 4) {
-      const float v0 = po[(static_cast<size_t>(s + 0) * G + hh) * D + e];
-      const float v1 = po[(static_cast<size_t>(s + 1) * G + hh) * D + e];
-      const float v2 = po[(static_cast<size_t>(s + 2) * G + hh) * D + e];
-      const float v3 = po[(static_cast<size_t>(s + 3) * G + hh) * D + e];
-      acc += v0 * s_f[s][hh];
-      acc += v1 * s_f[s + 1][hh];
-      acc += v2 * s_f[s + 2][hh];
-      acc += v3 * s_f[s + 3][hh];
+    float acc = 0.f, L = 0.f, M = -INFINITY;
+    for (int s0 = 0; s0 < n_splits; s0 += kC) {
+      float mv[kC];
+#pragma unroll
+      for (int j = 0; j < kC; ++j)
+        mv[j] = s0 + j < n_splits ? ld_agent(pml + 2 * ((s0 + j) * G + hh)) : -INFINITY;
+#pragma unroll
+      for (int j = 0; j < kC; ++j) M = fmaxf(M, mv[j]);
     }
-    for (; s < n_splits; ++s) acc += po[(static_cast<size_t>(s) * G + hh) * D + e] * s_f[s][hh];
-    a.out[frag_index(row, (hk * G + hh) * D + e, a.out_Rg)] = static_cast<uint16_t>(f2bf(acc * s_invL[hh]));
+    for (int s0 = 0; s0 < n_splits; s0 += kC) {
+      float mv[kC], lv[kC], ov[kC];
+#pragma unroll
+      for (int j = 0; j < kC; ++j) {
+        const bool ok = s0 + j < n_splits;
+        const int sj = s0 + j;
+        mv[j] = ok ? ld_agent(pml + 2 * (sj * G + hh)) : -INFINITY;
+        lv[j] = ok ? ld_agent(pml + 2 * (sj * G + hh) + 1) : 0.f;
+        ov[j] = ok ? ld_agent(pob + (static_cast<size_t>(sj) * G + hh) * D + e) : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < kC; ++j) {
+        if (s0 + j < n_splits) {
+          const float f = exp2f(mv[j] - M);
+          L += lv[j] * f;
+          acc += ov[j] * f;
+        }
+      }
+    }
+    a.out[frag_index(row, (hk * G + hh) * D + e, a.out_Rg)] = static_cast<uint16_t>(f2bf(acc * (1.f / L)));
   }
+  // ready for the next pass
+  if (threadIdx.x == 0) __hip_atomic_store(a.counter + rh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s) {
   dim3 grid(a.max_splits, a.Hkv, n_rows);
   if (a.hd == 128) {
-    hipLaunchKernelGGL(k_attn_decode<128>, grid, dim3(64 * kAttnWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_decode<128, 4>), grid, dim3(64 * kAttnWaves), 0, s, a);
   } else if (a.hd == 64) {
-    hipLaunchKernelGGL(k_attn_decode<64>, grid, dim3(64 * kAttnWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_decode<64, 4>), grid, dim3(64 * kAttnWaves), 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.max_splits <= 1) return e;
-  hipLaunchKernelGGL(k_attn_combine, dim3(a.Hkv, n_rows), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -1,4 +1,5 @@
-// Weight-streaming projections on the matrix cores, with fused epilogues.
+// Weight-streaming projections on the matrix cores, with fused epilogues and
+// the RMSNorm folded in.
 //
 // Y[R][N] = X[R][K] W[N][K]^T for the rows of a pass.  Below the ridge point
 // the pass is bound by reading W once (paper, appendix "The Switching
@@ -8,16 +9,22 @@
 // 16-byte load per lane, several tiles in flight, and feeds them straight
 // to v_mfma_f32_16x16x32_bf16 with W as the A operand (16 output columns)
 // and a 16-row group of X as the B operand.  K is split across the waves of
-// a workgroup (reduced in LDS in a fixed order) and, for the narrow residual
-// projections, across workgroups (partials summed by the next kernel).
+// a workgroup and reduced in LDS in a fixed order.
+//
+// RMSNorm folding.  RMSNorm(x)*g W^T = r (x*g) W^T with r = 1/sqrt(mean(x^2)
+// + eps) per row.  The residual projections (O, down) end by writing the
+// updated residual x, the bf16 frags of x*g for the next consumer, and per
+// workgroup partial sums of x^2; the consumer projections (QKV, gate/up,
+// lm_head) sum those partials in a fixed order in their prologue and scale
+// their accumulators by r.  No separate normalisation pass runs.
 //
 // Epilogues (the tensors stored between kernels are rounded to bf16):
-//   RESID  : x[r][n] += y                      (O and down projections)
-//   QKV    : rotary on q,k; q -> bf16 buffer; k,v -> this layer's KV slot
-//            (Invariant 1: every row writes its own-layer KV)
-//   SWIGLU : a = silu(gate) * up -> bf16 frags for the down projection
+//   RESID  : x[r][n] += y; frags of bf16(x * g_next); sum of x^2 partials
+//   QKV    : r scale, rotary on q,k; q -> bf16 buffer; k,v -> this layer's
+//            KV slot (Invariant 1: every row writes its own-layer KV)
+//   SWIGLU : a = silu(r gate) * (r up) -> bf16 frags for the down projection
 //            (the SwiGLU product of Algorithm 1's RUN cohort step)
-//   LOGITS : bf16 logits + per-workgroup (max, lowest index) for greedy argmax
+//   LOGITS : z = r y; bf16 logits + per-workgroup (max, lowest index)
 #include <climits>
 
 #include "dev.hpp"
@@ -32,16 +39,17 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ float s_amv[WN][MG][16];
   __shared__ int s_ami[WN][MG][16];
+  __shared__ double s_r[MG * 16];        // consumer: 1/rms of each row of the tile
+  __shared__ double s_ss[WN][MG][16];    // RESID: per-wave sum of x^2
+  __shared__ double s_ssq_part[64 * WN * WK];  // consumer: partial sums of x^2
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wn = w % WN, wk = w / WN;
-  const int ng = blockIdx.x, ks = blockIdx.y, mt = blockIdx.z;
+  const int ng = blockIdx.x, mt = blockIdx.z;
   const int n_tiles = a.N >> 4;
   const int nt0 = (ng * WN + wn) * NT;
   const int g0 = mt * MG;
-  const int kt_lo = static_cast<int>(static_cast<long>(ks) * a.Kt / a.KS);
-  const int kt_hi = static_cast<int>(static_cast<long>(ks + 1) * a.Kt / a.KS);
 
   f32x4 acc[NT][MG];
 #pragma unroll
@@ -52,40 +60,150 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   bool tvalid[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) tvalid[j] = (nt0 + j) < n_tiles;
-  bool gvalid[MG];
-#pragma unroll
-  for (int g = 0; g < MG; ++g) gvalid[g] = (g0 + g) < a.Rg;
 
-  const int first = kt_lo + wk;
-  const int n_it = first < kt_hi ? (kt_hi - first + WK - 1) / WK : 0;
+  const int first = wk;
+  const int n_it = first < a.Kt ? (a.Kt - first + WK - 1) / WK : 0;
+  // Out-of-range tiles and row groups read a valid one (their sums are never
+  // stored) and the stream past the last K step re-reads the last one, so
+  // every load in the main loop is unconditional: the compiler can then keep
+  // PF steps in flight instead of draining the queue each round.
+  int ntc[NT], gc[MG];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) ntc[j] = min(nt0 + j, n_tiles - 1);
+#pragma unroll
+  for (int g = 0; g < MG; ++g) gc[g] = min(g0 + g, a.Rg - 1);
   const u32x4* Wbase = a.W + lane;
   const u32x4* Xbase = a.X + lane;
 
   u32x4 fa[PF][NT], fb[PF][MG];
-  auto load = [&](u32x4 (&ra)[NT], u32x4 (&rb)[MG], int kt) {
+  auto load = [&](u32x4 (&ra)[NT], u32x4 (&rb)[MG], int i) {
+    const int kt = first + min(i, n_it - 1) * WK;
 #pragma unroll
-    for (int j = 0; j < NT; ++j)
-      ra[j] = tvalid[j] ? Wbase[(static_cast<size_t>(nt0 + j) * a.Kt + kt) * 64] : u32x4{0u, 0u, 0u, 0u};
+    for (int j = 0; j < NT; ++j) ra[j] = Wbase[(static_cast<size_t>(ntc[j]) * a.Kt + kt) * 64];
 #pragma unroll
-    for (int g = 0; g < MG; ++g)
-      rb[g] = gvalid[g] ? Xbase[(static_cast<size_t>(kt) * a.Rg + g0 + g) * 64] : u32x4{0u, 0u, 0u, 0u};
+    for (int g = 0; g < MG; ++g) rb[g] = Xbase[(static_cast<size_t>(kt) * a.Rg + gc[g]) * 64];
   };
 
-#pragma unroll
-  for (int st = 0; st < PF; ++st)
-    if (st < n_it) load(fa[st], fb[st], first + st * WK);
+  const int rsub = lane & 15;
+  const int nq = 4 * (lane >> 4);
 
-  for (int it = 0; it < n_it; it += PF) {
+  // ---- loads the epilogue needs, issued ahead of the weight stream so that
+  // their latency hides under it (decode shapes; larger tiles load them late)
+  constexpr bool kHoist = MG * NT <= 2;
+  // consumer: x^2 partials (r = 1/sqrt(sum x^2 / H + eps)), read after the
+  // weight prefetch is issued; each thread adds a strided subset of one row's
+  // partials, the subsets are then added in a fixed order, so the result does
+  // not depend on timing
+  constexpr int kThreads = 64 * WN * WK;
+  constexpr int kRows = MG * 16;
+  constexpr int kTpr = kThreads / kRows;  // threads per row
+  constexpr int kLd = 16;                 // independent loads per round
+  static_assert(kThreads % kRows == 0, "rows must divide the workgroup");
+  const bool consumer = EPI != EPI_RESID && a.ssq != nullptr;
+  const int ss_rr = threadIdx.x % kRows, ss_sub = threadIdx.x / kRows;
+  const int ss_row = 16 * g0 + ss_rr;
+  // residual: x and the next norm's gains
+  float4 xv[NT][MG];
+  uint2 gv[NT];
+  if constexpr (EPI == EPI_RESID && kHoist) {
+    if (wk == 0) {
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int n0 = 16 * (nt0 + j) + nq;
+        gv[j] = (tvalid[j] && a.hg_out != nullptr) ? *reinterpret_cast<const uint2*>(a.g_next + n0) : uint2{0u, 0u};
+#pragma unroll
+        for (int g = 0; g < MG; ++g) {
+          const int row = 16 * (g0 + g) + rsub;
+          xv[j][g] = (tvalid[j] && row < a.R) ? *reinterpret_cast<const float4*>(a.x + static_cast<size_t>(row) * a.N + n0)
+                                              : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+    }
+  }
+  // QKV: KV slot and position of the rows, then the rotary factors
+  int q_slot[MG], q_pos[MG];
+  float2 q_cs[NT][MG][2];
+  if constexpr (EPI == EPI_QKV && kHoist) {
+    if (wk == 0) {
+#pragma unroll
+      for (int g = 0; g < MG; ++g) {
+        const int row = 16 * (g0 + g) + rsub;
+        q_slot[g] = row < a.R ? a.slot[row] : 0;
+        q_pos[g] = row < a.R ? a.pos[row] : 0;
+      }
+    }
+  }
+
+  if (n_it > 0) {
+#pragma unroll
+    for (int st = 0; st < PF; ++st) load(fa[st], fb[st], st);
+  }
+
+  if constexpr (EPI == EPI_QKV && kHoist) {
+    if (wk == 0) {
+      const int half = a.hd >> 1;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int n0 = 16 * (nt0 + j) + nq;
+        const int j0 = (n0 % a.hd) >> 1;
+        const bool rot = tvalid[j] && n0 < a.Nq + a.Nkv;
+#pragma unroll
+        for (int g = 0; g < MG; ++g) {
+          const int row = 16 * (g0 + g) + rsub;
+          const bool ok = rot && row < a.R;
+          const float2* rp = a.rope + static_cast<size_t>(q_pos[g]) * half + j0;
+          q_cs[j][g][0] = ok ? rp[0] : make_float2(1.f, 0.f);
+          q_cs[j][g][1] = ok ? rp[1] : make_float2(1.f, 0.f);
+        }
+      }
+    }
+  }
+
+  if (consumer) {
+    double* s_part = reinterpret_cast<double*>(s_ssq_part);
+    double s = 0.0;
+    if (ss_row < a.R) {
+      for (int base = ss_sub; base < a.ssq_parts; base += kLd * kTpr) {
+        double v[kLd];
+#pragma unroll
+        for (int j = 0; j < kLd; ++j) {
+          const int p = base + j * kTpr;
+          v[j] = p < a.ssq_parts ? a.ssq[static_cast<size_t>(p) * a.R + ss_row] : 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < kLd; ++j) s += v[j];
+      }
+    }
+    s_part[ss_sub * kRows + ss_rr] = s;
+    __syncthreads();
+    if (threadIdx.x < kRows) {
+      double tot = 0.0;
+      for (int j = 0; j < kTpr; ++j) tot += s_part[j * kRows + threadIdx.x];
+      s_r[threadIdx.x] = 1.0 / sqrt(tot / static_cast<double>(a.norm_dim) + static_cast<double>(a.eps));
+    }
+  }
+
+  int it = 0;
+  for (; it + PF < n_it; it += PF) {
 #pragma unroll
     for (int st = 0; st < PF; ++st) {
-      if (it + st < n_it) {
 #pragma unroll
-        for (int j = 0; j < NT; ++j)
+      for (int j = 0; j < NT; ++j)
 #pragma unroll
-          for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
-        const int nx = it + st + PF;
-        if (nx < n_it) load(fa[st], fb[st], first + nx * WK);
-      }
+        for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
+      load(fa[st], fb[st], it + st + PF);
+      // keep each step's refill next to its use instead of batching a
+      // whole round of loads at the end of the loop body
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int st = 0; st < PF; ++st) {
+    if (it + st < n_it) {
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
     }
   }
 
@@ -106,37 +224,74 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 #pragma unroll
           for (int g = 0; g < MG; ++g) acc[j][g] += red[((((w2 - 1) * WN + wn) * NT + j) * MG + g) * 64 + lane];
     }
+  } else {
+    __syncthreads();  // s_r visible
+  }
+
+  // scale the sums by the per-row 1/rms (double product, rounded once to float)
+  if constexpr (EPI != EPI_RESID) {
+    if (a.ssq != nullptr && wk == 0) {
+#pragma unroll
+      for (int g = 0; g < MG; ++g) {
+        const double r = s_r[16 * g + rsub];
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[j][g][q] = static_cast<float>(static_cast<double>(acc[j][g][q]) * r);
+      }
+    }
   }
 
   // ---- epilogues (waves with wk == 0 hold the sums)
-  const int rsub = lane & 15;
-  const int nq = 4 * (lane >> 4);
   if constexpr (EPI == EPI_RESID) {
-    // KS == 1: x += y.  KS > 1 (K split across workgroups): each split stores
-    // its partial part[ks][row][n]; the next RMSNorm adds them to x in split
-    // order, so no workgroup waits for another and the sum is deterministic.
+    // x += y; frags of bf16(x * g_next); this workgroup's share of sum x^2 per row
     if (wk == 0) {
 #pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        if (!tvalid[j]) continue;
-        const int n0 = 16 * (nt0 + j) + nq;
+      for (int g = 0; g < MG; ++g) {
+        const int row = 16 * (g0 + g) + rsub;
+        double ss = 0.0;
 #pragma unroll
-        for (int g = 0; g < MG; ++g) {
-          const int row = 16 * (g0 + g) + rsub;
-          if (row >= a.R) continue;
-          if (a.KS > 1) {
-            *reinterpret_cast<float4*>(a.part + (static_cast<size_t>(ks) * a.R + row) * a.N + n0) =
-                make_float4(acc[j][g][0], acc[j][g][1], acc[j][g][2], acc[j][g][3]);
-          } else {
-            float4* px = reinterpret_cast<float4*>(a.x + static_cast<size_t>(row) * a.N + n0);
-            float4 v = *px;
-            v.x += acc[j][g][0];
-            v.y += acc[j][g][1];
-            v.z += acc[j][g][2];
-            v.w += acc[j][g][3];
-            *px = v;
+        for (int j = 0; j < NT; ++j) {
+          if (!tvalid[j] || row >= a.R) continue;
+          const int n0 = 16 * (nt0 + j) + nq;
+          float4* px = reinterpret_cast<float4*>(a.x + static_cast<size_t>(row) * a.N + n0);
+          float4 v;
+          if constexpr (kHoist) v = xv[j][g];
+          else v = *px;
+          v.x += acc[j][g][0];
+          v.y += acc[j][g][1];
+          v.z += acc[j][g][2];
+          v.w += acc[j][g][3];
+          *px = v;
+          if (a.hg_out != nullptr) {
+            uint2 gq;
+            if constexpr (kHoist) gq = gv[j];
+            else gq = *reinterpret_cast<const uint2*>(a.g_next + n0);
+            uint2 hv;
+            hv.x = d2bf(static_cast<double>(v.x) * bf2f(gq.x & 0xffffu)) |
+                   (d2bf(static_cast<double>(v.y) * bf2f(gq.x >> 16)) << 16);
+            hv.y = d2bf(static_cast<double>(v.z) * bf2f(gq.y & 0xffffu)) |
+                   (d2bf(static_cast<double>(v.w) * bf2f(gq.y >> 16)) << 16);
+            *reinterpret_cast<uint2*>(a.hg_out + frag_index(row, n0, a.hg_Rg)) = hv;
           }
+          ss += static_cast<double>(v.x) * v.x + static_cast<double>(v.y) * v.y +
+                static_cast<double>(v.z) * v.z + static_cast<double>(v.w) * v.w;
         }
+        // the four lane groups hold the same row
+        ss += __shfl_xor(ss, 16, 64);
+        ss += __shfl_xor(ss, 32, 64);
+        if (lane < 16) s_ss[wn][g][lane] = ss;
+      }
+    }
+    if (a.ssq_out != nullptr) {
+      __syncthreads();
+      if (threadIdx.x < MG * 16) {
+        const int g = threadIdx.x >> 4, l = threadIdx.x & 15;
+        double ss = s_ss[0][g][l];
+#pragma unroll
+        for (int w2 = 1; w2 < WN; ++w2) ss += s_ss[w2][g][l];
+        const int row = 16 * (g0 + g) + l;
+        if (row < a.R) a.ssq_out[static_cast<size_t>(ng) * a.R + row] = ss;
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
@@ -167,15 +322,23 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
           const int row = 16 * (g0 + g) + rsub;
           if (row >= a.R) continue;
           const f32x4 v = acc[j][g];
-          const int sl = a.slot[row];
+          int sl;
+          if constexpr (kHoist) sl = q_slot[g];
+          else sl = a.slot[row];
           const int blk = sl >> 4, t = sl & 15;
           if (n0 < a.Nq + a.Nkv) {
             const int ph = n0 % hd;          // packed row inside the head (multiple of 4)
             const int hb = n0 - ph;          // first packed row of the head
             const int j0 = ph >> 1;          // dims j0, j0+half, j0+1, j0+1+half
-            const int p = a.pos[row];
-            const float2 cs0 = a.rope[static_cast<size_t>(p) * half + j0];
-            const float2 cs1 = a.rope[static_cast<size_t>(p) * half + j0 + 1];
+            float2 cs0, cs1;
+            if constexpr (kHoist) {
+              cs0 = q_cs[j][g][0];
+              cs1 = q_cs[j][g][1];
+            } else {
+              const int p = a.pos[row];
+              cs0 = a.rope[static_cast<size_t>(p) * half + j0];
+              cs1 = a.rope[static_cast<size_t>(p) * half + j0 + 1];
+            }
             const float y0 = v[0] * cs0.x - v[1] * cs0.y;
             const float y1 = v[1] * cs0.x + v[0] * cs0.y;
             const float y2 = v[2] * cs1.x - v[3] * cs1.y;
@@ -259,22 +422,24 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 template <int MG, int NT, int WN, int WK, int PF, int EPI>
 static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, hipStream_t s) {
   const int n_groups = (a.N / 16 + NT * WN - 1) / (NT * WN);
-  dim3 grid(n_groups, a.KS, m_tiles);
+  dim3 grid(n_groups, 1, m_tiles);
   const size_t smem = (WK > 1 ? (WK - 1) : 0) * WN * NT * MG * 64 * sizeof(f32x4);
   hipLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI>), grid, dim3(64 * WN * WK), smem, s, a);
   return hipGetLastError();
 }
 
-// Launch shapes.  mg = 16-row groups of X per tile.  For mg == 1 two shapes:
-// "narrow" (one 16-row N tile per wave, 8 K-split waves, 8 K tiles in
-// flight) for matrices with few N tiles, and "wide" (four N tiles per wave,
-// 4 K tiles in flight, fewer and longer-running workgroups) for the wide
-// gate/up and lm_head matrices.
+// Launch shapes.  mg = 16-row groups of X per tile.  For mg == 1:
+//  narrow  one 16-row N tile per wave, 8 K-split waves, 8 K tiles in flight
+//          (residual projections: N = hidden);
+//  pair    two N tiles per wave, 4 K tiles in flight (QKV, gate/up);
+//  wide    four N tiles per wave (lm_head).
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
   switch (p.mg) {
     case 1:
-      return p.wide ? launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, s) : launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
+      if (p.nt == 4) return launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, s);
+      if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, s);
+      return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
     case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
     case 4: return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
     default: return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
@@ -282,33 +447,19 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
 }
 
 GemmPlan plan_gemm(int N, int K, int R, int epi) {
+  (void)K;
   GemmPlan p;
   const int Rg = (R + 15) / 16;
   p.mg = Rg <= 1 ? 1 : Rg <= 2 ? 2 : Rg <= 4 ? 4 : 8;
   p.m_tiles = (Rg + p.mg - 1) / p.mg;
-  // wide shape when it still leaves at least two workgroups per CU
-  p.wide = p.mg == 1 && (epi == EPI_SWIGLU || epi == EPI_LOGITS) && N / 64 >= 256;
-  const int rows_per_group = p.wide ? 64 : p.mg <= 2 ? 16 : 64;
+  p.nt = 1;
+  if (p.mg == 1 && epi != EPI_RESID) p.nt = (epi == EPI_LOGITS && N / 64 >= 256) ? 4 : 2;
+  const int rows_per_group = p.mg == 1 ? 16 * p.nt : p.mg == 2 ? 16 : 64;
   p.n_groups = (N / 16 * 16 + rows_per_group - 1) / rows_per_group;
-  const int Kt = K / 32;
-  const int wk = p.mg <= 2 ? 8 : 2;
-  // Only the residual projections split K across workgroups (their partials
-  // are summed by the next RMSNorm).  Aim for about 1024 workgroups, keep at
-  // least one K tile per wave, and keep the partial traffic (KS x R x N x 8
-  // bytes) under a quarter of the weight bytes.
-  int ks = 1;
-  if (epi == EPI_RESID) {
-    const int have = p.n_groups * p.m_tiles;
-    while (have * ks * 2 <= 1024 && Kt / (ks * 2) >= wk &&
-           static_cast<long>(ks * 2) * R * 16 <= static_cast<long>(K))
-      ks *= 2;
-  }
-  p.ks = ks;
   return p;
 }
 
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s) {
-  a.KS = p.ks;
   switch (epi) {
     case EPI_RESID: return launch_epi<EPI_RESID>(a, p, s);
     case EPI_QKV: return launch_epi<EPI_QKV>(a, p, s);

@@ -1,4 +1,4 @@
-// Small kernels of the pass: embedding gather, RMSNorm into frags, greedy
+// Small kernels of the pass: embedding gather, logit-row gather, greedy
 // argmax, weight repacking, KV scatter/gather, workspace clearing.
 #include <climits>
 #include <cmath>
@@ -9,100 +9,77 @@
 namespace vsk {
 
 // ---------------------------------------------------------------- embedding
-// x[r][:] = float(E[ids[r]][:]); one workgroup per row, 8 columns per thread.
-// Token ids outside [0, V) give a zero row.
+// x[r][:] = float(E[ids[r]][:]) (fp32 residual), plus what the first QKV
+// projection consumes: frags of bf16(x * g) and per-16-column partial sums
+// of x^2 (ssq[c/16][r]).  Token ids outside [0, V) give a zero row.
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, const int32_t* __restrict__ ids,
-                                               int H, int V, float* __restrict__ x) {
+                                               int H, int V, const uint16_t* __restrict__ g, float* __restrict__ x,
+                                               uint16_t* __restrict__ hg, int hg_Rg, double* __restrict__ ssq) {
+  __shared__ double s_ss[4];
   const int r = blockIdx.x;
   const int id = ids[r];
-  if (id < 0 || id >= V) {
-    for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4)
-      *reinterpret_cast<float4*>(x + static_cast<size_t>(r) * H + c) = make_float4(0.f, 0.f, 0.f, 0.f);
-    return;
-  }
-  const size_t base = static_cast<size_t>(id) * H;
+  const bool valid = id >= 0 && id < V;
+  const size_t base = valid ? static_cast<size_t>(id) * H : 0;
+  double ss = 0.0;
   for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(E + base + c);
-    float4* dst = reinterpret_cast<float4*>(x + static_cast<size_t>(r) * H + c);
-    dst[0] = make_float4(bf2f(v[0] & 0xffffu), bf2f(v[0] >> 16), bf2f(v[1] & 0xffffu), bf2f(v[1] >> 16));
-    dst[1] = make_float4(bf2f(v[2] & 0xffffu), bf2f(v[2] >> 16), bf2f(v[3] & 0xffffu), bf2f(v[3] >> 16));
-  }
-}
-
-hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, float* x, hipStream_t s) {
-  hipLaunchKernelGGL(k_embed, dim3(R), dim3(256), 0, s, E, ids, H, V, x);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------- RMSNorm
-// out = bf16(x * 1/sqrt(mean(x^2) + eps) * g) written as frags; output row r
-// reads input row gather[r] (or r).  Rows R..16*Rg of the output are zeroed.
-// A gathered index outside [0, R_in) gives a zero row.
-// With KS > 0, the K-split partials of the preceding residual projection
-// (part[s][row][H], s = 0..KS-1) are first added to x in split order and the
-// updated row is written back: this kernel completes that projection.
-constexpr int kNormChunks = 4;  // 8-column chunks per thread: hidden <= 256*8*4
-__global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ x, const float* __restrict__ part, int KS,
-                                                 const uint16_t* __restrict__ g, const int32_t* __restrict__ gather,
-                                                 int R, int R_in, int H, float eps, uint16_t* __restrict__ out,
-                                                 int Rg) {
-  __shared__ double s_red[8];
-  const int r = blockIdx.x;
-  const int src = r < R ? (gather ? gather[r] : r) : -1;
-  if (src < 0 || src >= R_in) {
-    for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8)
-      *reinterpret_cast<u32x4*>(out + frag_index(r, c, Rg)) = u32x4{0u, 0u, 0u, 0u};
-    return;
-  }
-  float* xr = x + static_cast<size_t>(src) * H;
-  float v[kNormChunks][8];
-  double ss = 0.0;  // the row statistics and the scaling are done in double
+    u32x4 v = valid ? *reinterpret_cast<const u32x4*>(E + base + c) : u32x4{0u, 0u, 0u, 0u};
+    float e[8];
 #pragma unroll
-  for (int i = 0; i < kNormChunks; ++i) {
-    const int c = (threadIdx.x + i * blockDim.x) * 8;
-    if (c >= H) break;
-    float4 a = *reinterpret_cast<const float4*>(xr + c);
-    float4 b = *reinterpret_cast<const float4*>(xr + c + 4);
-    if (KS > 0) {
-      for (int s = 0; s < KS; ++s) {
-        const float* pr = part + (static_cast<size_t>(s) * R_in + src) * H + c;
-        const float4 pa = *reinterpret_cast<const float4*>(pr);
-        const float4 pb = *reinterpret_cast<const float4*>(pr + 4);
-        a.x += pa.x; a.y += pa.y; a.z += pa.z; a.w += pa.w;
-        b.x += pb.x; b.y += pb.y; b.z += pb.z; b.w += pb.w;
-      }
-      *reinterpret_cast<float4*>(xr + c) = a;
-      *reinterpret_cast<float4*>(xr + c + 4) = b;
+    for (int k = 0; k < 4; ++k) {
+      e[2 * k] = bf2f(v[k] & 0xffffu);
+      e[2 * k + 1] = bf2f(v[k] >> 16);
     }
-    v[i][0] = a.x; v[i][1] = a.y; v[i][2] = a.z; v[i][3] = a.w;
-    v[i][4] = b.x; v[i][5] = b.y; v[i][6] = b.z; v[i][7] = b.w;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) ss += static_cast<double>(v[i][k]) * v[i][k];
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
-  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  double tot = 0.0;
-  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) tot += s_red[i];
-  const double inv = 1.0 / sqrt(tot / static_cast<double>(H) + static_cast<double>(eps));
-#pragma unroll
-  for (int i = 0; i < kNormChunks; ++i) {
-    const int c = (threadIdx.x + i * blockDim.x) * 8;
-    if (c >= H) break;
+    float4* dst = reinterpret_cast<float4*>(x + static_cast<size_t>(r) * H + c);
+    dst[0] = make_float4(e[0], e[1], e[2], e[3]);
+    dst[1] = make_float4(e[4], e[5], e[6], e[7]);
     const u32x4 gv = *reinterpret_cast<const u32x4*>(g + c);
     u32x4 o;
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      o[k] = d2bf(v[i][2 * k] * inv * bf2f(gv[k] & 0xffffu)) |
-             (d2bf(v[i][2 * k + 1] * inv * bf2f(gv[k] >> 16)) << 16);
-    *reinterpret_cast<u32x4*>(out + frag_index(r, c, Rg)) = o;
+    for (int k = 0; k < 4; ++k) {
+      o[k] = d2bf(static_cast<double>(e[2 * k]) * bf2f(gv[k] & 0xffffu)) |
+             (d2bf(static_cast<double>(e[2 * k + 1]) * bf2f(gv[k] >> 16)) << 16);
+      ss += static_cast<double>(e[2 * k]) * e[2 * k] + static_cast<double>(e[2 * k + 1]) * e[2 * k + 1];
+    }
+    *reinterpret_cast<u32x4*>(hg + frag_index(r, c, hg_Rg)) = o;
   }
+  // whole-row sum of x^2 in a fixed order: one partial per row
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+  if ((threadIdx.x & 63) == 0) s_ss[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (threadIdx.x == 0) ssq[r] = (s_ss[0] + s_ss[1]) + (s_ss[2] + s_ss[3]);
 }
 
-hipError_t launch_rmsnorm(float* x, const float* part, int KS, const uint16_t* g, const int32_t* gather, int R,
-                          int R_in, int H, float eps, uint16_t* out, int Rg, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm, dim3(16 * Rg), dim3(256), 0, s, x, part, KS, g, gather, R, R_in, H, eps, out, Rg);
+hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, const uint16_t* g, float* x,
+                        uint16_t* hg, int hg_Rg, double* ssq, hipStream_t s) {
+  hipLaunchKernelGGL(k_embed, dim3(R), dim3(256), 0, s, E, ids, H, V, g, x, hg, hg_Rg, ssq);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- row gather
+// Compact the frags and x^2 partials of the rows that return logits (a
+// prefill pass asks for a few rows out of many).  Indices outside [0, R_in)
+// give a zero row.
+__global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict__ hg_in, int Rg_in,
+                                                     const double* __restrict__ ssq_in, int parts, int R_in,
+                                                     const int32_t* __restrict__ rows, int H,
+                                                     uint16_t* __restrict__ hg_out, int Rg_out,
+                                                     double* __restrict__ ssq_out, int Ro) {
+  const int i = blockIdx.x;
+  const int src = rows[i];
+  const bool valid = src >= 0 && src < R_in;
+  for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8)
+    *reinterpret_cast<u32x4*>(hg_out + frag_index(i, c, Rg_out)) =
+        valid ? *reinterpret_cast<const u32x4*>(hg_in + frag_index(src, c, Rg_in)) : u32x4{0u, 0u, 0u, 0u};
+  for (int p = threadIdx.x; p < parts; p += blockDim.x)
+    ssq_out[static_cast<size_t>(p) * Ro + i] = valid ? ssq_in[static_cast<size_t>(p) * R_in + src] : 0.0;
+}
+
+hipError_t launch_gather_rows(const uint16_t* hg_in, int Rg_in, const double* ssq_in, int parts, int R_in,
+                              const int32_t* rows, int Ro, int H, uint16_t* hg_out, int Rg_out, double* ssq_out,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(k_gather_rows, dim3(Ro), dim3(256), 0, s, hg_in, Rg_in, ssq_in, parts, R_in, rows, H, hg_out,
+                     Rg_out, ssq_out, Ro);
   return hipGetLastError();
 }
 

@@ -16,8 +16,8 @@ from helpers import compare_logits, oracle_run  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-# two layers, GQA group 4, head_dim 128: several tiles along every matrix,
-# ragged row groups and several attention splits
+# two layers, GQA group 4, head_dim 128: several tiles along every matrix
+# and ragged row groups
 MID = ModelCfg("mid-2L", n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=128, ffn=1536,
                vocab=2048, rope_theta=500000.0)
 
@@ -57,6 +57,22 @@ def test_mid_decode_batches(B):
     d, lg, ids = _run(w)
     sub = None if B <= 20 else list(range(0, B, max(1, B // 12)))
     st, *_ = _check(w, lg, ids, sub)
+    print(st)
+
+
+@pytest.mark.parametrize("bps", [8, 24, 64, 512])
+def test_mid_attention_splits(bps):
+    """Split-K attention: one work item per KV head (bps 512) up to many
+    splits merged in split order (bps 8); contexts up to 1500 tokens."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    ctx = np.array([1499, 1, 16, 17, 700, 1023, 1024, 255])
+    w = decode_workload(MID, ctx, seed=11, name=f"mid-splits-{bps}")
+    print(f"[gpu] {w.name} bps={bps}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(0, bps)
+    d.step()
+    lg, ids = d.results()
+    st, *_ = _check(w, lg, ids)
     print(st)
 
 
