@@ -10,25 +10,21 @@ its sequence and writing cache slot ``slot``:
 
   x  = E[token]                                    (float residual stream)
   for each layer l:
-     h  = R(x * g_attn),  r = 1 / sqrt(mean(x^2) + eps)
-     q, k, v = r (h Wq^T), r (h Wk^T), r (h Wv^T)      (RMSNorm, scale applied after)
+     h  = R(rmsnorm(x) * g_attn)
+     q, k, v = h Wq^T, h Wk^T, h Wv^T
      q, k = rope(q, pos), rope(k, pos);  q, k, v = R(q), R(k), R(v)
      cache[l][slot] = (k, v)                       (all rows, before attention)
      o_h = softmax(q_h . K^T / sqrt(d)) V over the sequence's keys 0..pos,
            K, V read through the block table, KV head floor(h*n_kv/n_q)
      x += R(o) Wo^T
-     h2 = R(x * g_mlp),  r2 = 1 / sqrt(mean(x^2) + eps)
-     x += R(silu(r2 h2 Wg^T) * (r2 h2 Wu^T)) Wd^T
-  z  = rf R(x * g_final) Wlm^T  for the rows that return logits
+     h2 = R(rmsnorm(x) * g_mlp)
+     x += R(silu(h2 Wg^T) * (h2 Wu^T)) Wd^T
+  z  = R(rmsnorm(x) * g_final) Wlm^T  for the rows that return logits
   logits = R(z);  token = lowest index of max z
 
 R is round-to-nearest-even to bf16 (the tensors stored between kernels);
-everything else is float64.  RMSNorm(x)*g*W^T = r * ((x*g) W^T) exactly; the
-rounding point is placed on x*g, before the per-row factor r, which scales
-the projection output.  The paper is silent on rounding points; this one
-lets the norm be folded into the neighbouring projections.  Paging and
-split-K only change summation order, so this plain form is the result the
-device path must reach.
+everything else is float64.  Paging and split-K only change summation
+order, so this plain form is the result the device path must reach.
 """
 from __future__ import annotations
 
@@ -134,11 +130,10 @@ def forward(model, W, kv: PagedKV, batch, tokens, logit_rows, *, want_hidden=Fal
     x = W.rows("embed", tokens) if x0 is None else np.array(x0, dtype=np.float64)
     for layer in (range(m.n_layers) if layers is None else layers):
         # ---- attention block
-        h = nm.bf16_round(x * W.get("attn_norm", layer))
-        r = nm.rms_scale(x, m.rms_eps)
-        q = (_matmul(h, W.get("wq", layer)) * r).reshape(R, Hq, d)
-        k = (_matmul(h, W.get("wk", layer)) * r).reshape(R, Hk, d)
-        v = (_matmul(h, W.get("wv", layer)) * r).reshape(R, Hk, d)
+        h = nm.bf16_round(nm.rmsnorm(x, W.get("attn_norm", layer), m.rms_eps))
+        q = _matmul(h, W.get("wq", layer)).reshape(R, Hq, d)
+        k = _matmul(h, W.get("wk", layer)).reshape(R, Hk, d)
+        v = _matmul(h, W.get("wv", layer)).reshape(R, Hk, d)
         q = nm.bf16_round(nm.rope(q, pos, m.rope_theta))
         k = nm.bf16_round(nm.rope(k, pos, m.rope_theta))
         v = nm.bf16_round(v)
@@ -160,18 +155,16 @@ def forward(model, W, kv: PagedKV, batch, tokens, logit_rows, *, want_hidden=Fal
         o = nm.bf16_round(o.reshape(R, Hq * d))
         x = x + _matmul(o, W.get("wo", layer))
         # ---- MLP block
-        h2 = nm.bf16_round(x * W.get("mlp_norm", layer))
-        r2 = nm.rms_scale(x, m.rms_eps)
-        a = nm.bf16_round(nm.silu(_matmul(h2, W.get("w_gate", layer)) * r2) * (_matmul(h2, W.get("w_up", layer)) * r2))
+        h2 = nm.bf16_round(nm.rmsnorm(x, W.get("mlp_norm", layer), m.rms_eps))
+        a = nm.bf16_round(nm.silu(_matmul(h2, W.get("w_gate", layer))) * _matmul(h2, W.get("w_up", layer)))
         x = x + _matmul(a, W.get("w_down", layer))
     if logit_rows is None:
         return {"x": x}
     lr = np.asarray(logit_rows, np.int64)
-    hf = nm.bf16_round(x[lr] * W.get("final_norm", -1))
-    rf = nm.rms_scale(x[lr], m.rms_eps)
+    hf = nm.bf16_round(nm.rmsnorm(x[lr], W.get("final_norm", -1), m.rms_eps))
     z = np.empty((len(lr), m.vocab))
     if ("lm_head", -1) in W.over:
-        z[:] = _matmul(hf, W.get("lm_head", -1)) * rf
+        z[:] = _matmul(hf, W.get("lm_head", -1))
     else:
         from workloads import gen
         key = W.key("lm_head", -1)
@@ -179,7 +172,7 @@ def forward(model, W, kv: PagedKV, batch, tokens, logit_rows, *, want_hidden=Fal
         for v0 in range(0, m.vocab, lm_chunk):
             v1 = min(m.vocab, v0 + lm_chunk)
             wl = nm.from_bf16_bits(gen.bf16_bits_np(key, (v1 - v0) * H, W.dist, start=v0 * H)).reshape(v1 - v0, H)
-            z[:, v0:v1] = _matmul(hf, wl) * rf
+            z[:, v0:v1] = _matmul(hf, wl)
     out = {"z": z, "logits": nm.bf16_round(z), "ids": nm.argmax_lowest(z)}
     if want_hidden:
         out["x"] = x

@@ -5,9 +5,7 @@ Test infrastructure only (see the package docstring).
 The paper serves Llama-3-family decoders (Section "Implementation") and does
 not restate their layer definitions; the readings taken here are the
 standard Llama ones:
-  * RMSNorm: x / sqrt(mean(x^2) + eps) * g, eps = 1e-5.  In the pass the
-    bf16 rounding is applied to x*g and the factor 1/sqrt(mean(x^2) + eps)
-    scales the following projection's output (exactly equal before rounding).
+  * RMSNorm: x / sqrt(mean(x^2) + eps) * g, eps = 1e-5.
   * Rotary positions, rotate-half pairing (i, i + d/2), inverse frequency
     theta^(-2i/d), positions counted from 0, no frequency rescaling.
   * SwiGLU MLP: silu(x Wg^T) * (x Wu^T), silu(z) = z / (1 + exp(-z)); the
@@ -66,12 +64,6 @@ def rmsnorm(x, g, eps: float) -> np.ndarray:
     x = np.asarray(x, dtype=np.float64)
     ms = np.mean(x * x, axis=-1, keepdims=True)
     return x / np.sqrt(ms + eps) * np.asarray(g, dtype=np.float64)
-
-
-def rms_scale(x, eps: float) -> np.ndarray:
-    """Per-row factor 1 / sqrt(mean(x^2) + eps) over the last axis, kept as [..., 1]."""
-    x = np.asarray(x, dtype=np.float64)
-    return 1.0 / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
 
 
 # ------------------------------------------------------------------ rotary

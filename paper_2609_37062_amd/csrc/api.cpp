@@ -55,7 +55,8 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   const int G = c.n_q_heads / c.n_kv_heads;
   size_t o = 0;
   w.x = o; o = align_up(o + static_cast<size_t>(max_rows) * H * 4);
-  w.fa = o; o = align_up(o + Rp * std::max(H, Nq) * 2);
+  w.x_c = o; o = align_up(o + static_cast<size_t>(max_rows) * H * 4);
+  w.fa = o; o = align_up(o + Rp * Nq * 2);
   w.fb = o; o = align_up(o + Rp * H * 2);
   w.fc = o; o = align_up(o + Rp * F * 2);
   w.q = o; o = align_up(o + static_cast<size_t>(max_rows) * Nq * 2);
@@ -511,8 +512,8 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   const int H = c.hidden, F = c.ffn, d = c.head_dim, Nq = c.n_q_heads * d, Nkv = c.n_kv_heads * d;
   uint8_t* ws = pa.ws;
   float* x = reinterpret_cast<float*>(ws + wl.x);
-  // frag buffers: A = normed input of QKV, then attention output; B = normed
-  // input of gate/up; C = SwiGLU output
+  // frag buffers: A = attention output (O input); B = normalised rows (QKV,
+  // gate/up and lm_head input); C = SwiGLU output (down input)
   uint16_t* fa = reinterpret_cast<uint16_t*>(ws + wl.fa);
   uint16_t* fb = reinterpret_cast<uint16_t*>(ws + wl.fb);
   uint16_t* fc = reinterpret_cast<uint16_t*>(ws + wl.fc);
@@ -543,15 +544,12 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     return hipSuccess;
   };
 
-  TRY(launch_embed(reinterpret_cast<const uint16_t*>(P + h.pl.embed), pa.ids, R, H, c.vocab, norm_gain(0, false), x,
-                   fa, Rg, ssq, s));
+  TRY(launch_embed(reinterpret_cast<const uint16_t*>(P + h.pl.embed), pa.ids, R, H, c.vocab, x, ssq, s));
   int ssq_parts = 1;
 
   GemmArgs ga{};
   ga.R = R;
   ga.Rg = Rg;
-  ga.norm_dim = H;
-  ga.eps = c.rms_eps;
   ga.pool = h.pool;
   ga.n_blocks = h.n_blocks;
   ga.Hkv = c.n_kv_heads;
@@ -562,7 +560,6 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ga.pos = b.pos;
   ga.rope = reinterpret_cast<const float2*>(P + h.pl.rope);
   ga.x = x;
-  ga.hg_Rg = Rg;
   ga.out_Rg = Rg;
 
   AttnArgs aa{};
@@ -591,74 +588,71 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU);
   const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID);
 
+  // RMSNorm: one pass over x using the x^2 partials of the step that wrote it
+  auto norm = [&](const uint16_t* gain, const float* xin, int rows, int rg, const double* sq, int parts) {
+    return launch_rmsnorm_frags(xin, gain, sq, parts, rows, H, c.rms_eps, fb, rg, s);
+  };
+  ga.X = reinterpret_cast<const u4*>(fb);
   for (int l = 0; l < n_run; ++l) {
     const uint8_t* L = P + h.pl.layer_bytes * l;
-    // attention block: QKV (norm folded: x^2 partials of the previous residual)
+    // attention block
+    TRY(norm(norm_gain(l, false), x, R, Rg, ssq, ssq_parts));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wqkv);
-    ga.X = reinterpret_cast<const u4*>(fa);
+    ga.X = reinterpret_cast<const u4*>(fb);
     ga.Kt = H / 32;
     ga.N = Nq + 2 * Nkv;
-    ga.ssq = ssq;
-    ga.ssq_parts = ssq_parts;
+    ga.ssq_out = nullptr;
     ga.out = q;
     ga.layer = l;
     TRY(probed(2, [&] { return launch_gemm(ga, p_qkv, EPI_QKV, s); }));
     aa.layer = l;
     TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
-    // O projection: x += o Wo^T; emits the MLP norm's input frags and x^2 partials
+    // O projection: x += o Wo^T, with the x^2 partials of the updated rows
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);
     ga.X = reinterpret_cast<const u4*>(fa);
     ga.Kt = Nq / 32;
     ga.N = H;
-    ga.ssq = nullptr;
-    ga.hg_out = fb;
-    ga.g_next = norm_gain(l, true);
     ga.ssq_out = ssq;
     TRY(probed(3, [&] { return launch_gemm(ga, p_o, EPI_RESID, s); }));
     ssq_parts = p_o.n_groups;
     // MLP block
+    TRY(norm(norm_gain(l, true), x, R, Rg, ssq, ssq_parts));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wgu);
     ga.X = reinterpret_cast<const u4*>(fb);
     ga.Kt = H / 32;
     ga.N = 2 * F;
-    ga.ssq = ssq;
-    ga.ssq_parts = ssq_parts;
+    ga.ssq_out = nullptr;
     ga.out = fc;
     TRY(probed(0, [&] { return launch_gemm(ga, p_gu, EPI_SWIGLU, s); }));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wd);
     ga.X = reinterpret_cast<const u4*>(fc);
     ga.Kt = F / 32;
     ga.N = H;
-    ga.ssq = nullptr;
-    ga.hg_out = fa;
-    ga.g_next = (l + 1 < n_run) ? norm_gain(l + 1, false) : final_gain;
     ga.ssq_out = ssq;
     TRY(probed(1, [&] { return launch_gemm(ga, p_d, EPI_RESID, s); }));
     ssq_parts = p_d.n_groups;
-    ga.hg_out = nullptr;
-    ga.ssq_out = nullptr;
   }
-  // lm_head over the logit rows (final norm folded), then greedy argmax
+  // final norm over the logit rows, lm_head, greedy argmax
   const int Ro = pa.n_logit_rows;
   const int Rgo = (Ro + 15) / 16;
-  const uint16_t* Xl = fa;
-  const double* ssq_l = ssq;
   if (pa.logit_rows != nullptr) {
+    float* x_c = reinterpret_cast<float*>(ws + wl.x_c);
     double* ssq_c = reinterpret_cast<double*>(ws + wl.ssq_c);
-    TRY(launch_gather_rows(fa, Rg, ssq, ssq_parts, R, pa.logit_rows, Ro, H, fb, Rgo, ssq_c, s));
-    Xl = fb;
-    ssq_l = ssq_c;
+    TRY(launch_gather_rows(x, R, pa.logit_rows, Ro, H, x_c, ssq_c, s));
+    TRY(norm(final_gain, x_c, Ro, Rgo, ssq_c, 1));
+  } else {
+    TRY(norm(final_gain, x, Ro, Rgo, ssq, ssq_parts));
   }
   const GemmPlan p_lm = plan_gemm(c.vocab, H, Ro, EPI_LOGITS);
   ga.W = reinterpret_cast<const u4*>(P + h.pl.lm_head);
-  ga.X = reinterpret_cast<const u4*>(Xl);
+  ga.X = reinterpret_cast<const u4*>(fb);
   ga.Kt = H / 32;
   ga.N = c.vocab;
   ga.R = Ro;
   ga.Rg = Rgo;
-  ga.ssq = ssq_l;
-  ga.ssq_parts = ssq_parts;
+  ga.ssq_out = nullptr;
   ga.out = pa.logits;
+  ga.out_Rg = Rgo;
   ga.am_val = reinterpret_cast<float*>(ws + wl.am_part);
   ga.am_idx = reinterpret_cast<int*>(ws + wl.am_part + static_cast<size_t>((c.vocab + 15) / 16) * wl.max_rows * 4);
   TRY(probed(5, [&] { return launch_gemm(ga, p_lm, EPI_LOGITS, s); }));

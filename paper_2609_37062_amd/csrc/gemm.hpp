@@ -14,17 +14,8 @@ struct GemmArgs {
   int N;        // output columns
   int R;        // valid rows
   int Rg;       // 16-row groups of the X frag buffer
-  // folded RMSNorm, consumer side: r = 1/sqrt(sum_p ssq[p][row] / norm_dim + eps)
-  const double* ssq;  // [ssq_parts][R] partial sums of x^2, or null (no scaling)
-  int ssq_parts;
-  int norm_dim;
-  float eps;
-  // epilogue operands
-  float* x;              // RESID: fp32 residual [R][N]
-  uint16_t* hg_out;      // RESID: frags of bf16(x * g_next) (hg_Rg groups), or null
-  int hg_Rg;
-  const uint16_t* g_next;  // RESID: gains of the next RMSNorm [N]
-  double* ssq_out;       // RESID: partial sums of x^2 [n_groups][R], or null
+  float* x;          // RESID: fp32 residual [R][N], x += y
+  double* ssq_out;   // RESID: partial sums of x^2 of the updated rows [n_groups][R]
   uint16_t* out;  // QKV: q [R][Nq]; SWIGLU: frags (out_Rg); LOGITS: logits [R][N]
   int out_Rg;
   uint16_t* pool;  // QKV: KV pool

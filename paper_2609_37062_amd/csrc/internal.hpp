@@ -83,7 +83,7 @@ struct BatchDev {
 // ---------------------------------------------------------------- workspace
 struct WsLayout {
   int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
-  size_t x, fa, fb, fc, q, att_o, att_ml, att_cnt, ssq, ssq_c, am_part, total;
+  size_t x, x_c, fa, fb, fc, q, att_o, att_ml, att_cnt, ssq, ssq_c, am_part, total;
 };
 
 // attention split: 16-token blocks per split-K work item (tunable, >= kAttnMinBps)

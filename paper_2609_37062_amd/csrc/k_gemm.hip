@@ -11,20 +11,18 @@
 // and a 16-row group of X as the B operand.  K is split across the waves of
 // a workgroup and reduced in LDS in a fixed order.
 //
-// RMSNorm folding.  RMSNorm(x)*g W^T = r (x*g) W^T with r = 1/sqrt(mean(x^2)
-// + eps) per row.  The residual projections (O, down) end by writing the
-// updated residual x, the bf16 frags of x*g for the next consumer, and per
-// workgroup partial sums of x^2; the consumer projections (QKV, gate/up,
-// lm_head) sum those partials in a fixed order in their prologue and scale
-// their accumulators by r.  No separate normalisation pass runs.
+// RMSNorm.  The residual projections (O, down) end by updating the fp32
+// residual x and writing per-workgroup partial sums of x^2 of the updated
+// rows, so the normalisation that follows (k_rmsnorm_frags) is one pass over
+// x with no reduction of its own.
 //
 // Epilogues (the tensors stored between kernels are rounded to bf16):
-//   RESID  : x[r][n] += y; frags of bf16(x * g_next); sum of x^2 partials
-//   QKV    : r scale, rotary on q,k; q -> bf16 buffer; k,v -> this layer's
-//            KV slot (Invariant 1: every row writes its own-layer KV)
-//   SWIGLU : a = silu(r gate) * (r up) -> bf16 frags for the down projection
+//   RESID  : x[r][n] += y; sum of x^2 partials
+//   QKV    : rotary on q,k; q -> bf16 buffer; k,v -> this layer's KV slot
+//            (Invariant 1: every row writes its own-layer KV)
+//   SWIGLU : a = silu(gate) * up -> bf16 frags for the down projection
 //            (the SwiGLU product of Algorithm 1's RUN cohort step)
-//   LOGITS : z = r y; bf16 logits + per-workgroup (max, lowest index)
+//   LOGITS : bf16 logits + per-workgroup (max, lowest index)
 #include <climits>
 
 #include "dev.hpp"
@@ -39,9 +37,7 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ float s_amv[WN][MG][16];
   __shared__ int s_ami[WN][MG][16];
-  __shared__ double s_r[MG * 16];        // consumer: 1/rms of each row of the tile
-  __shared__ double s_ss[WN][MG][16];    // RESID: per-wave sum of x^2
-  __shared__ double s_ssq_part[64 * WN * WK];  // consumer: partial sums of x^2
+  __shared__ double s_ss[WN][MG][16];  // RESID: per-wave sum of x^2
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -50,6 +46,8 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   const int n_tiles = a.N >> 4;
   const int nt0 = (ng * WN + wn) * NT;
   const int g0 = mt * MG;
+  const int rsub = lane & 15;
+  const int nq = 4 * (lane >> 4);
 
   f32x4 acc[NT][MG];
 #pragma unroll
@@ -63,7 +61,7 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 
   const int first = wk;
   const int n_it = first < a.Kt ? (a.Kt - first + WK - 1) / WK : 0;
-  // Out-of-range tiles and row groups read a valid one (their sums are never
+  // Out-of-range tiles and rows read a valid one (their sums are never
   // stored) and the stream past the last K step re-reads the last one, so
   // every load in the main loop is unconditional: the compiler can then keep
   // PF steps in flight instead of draining the queue each round.
@@ -84,33 +82,15 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
     for (int g = 0; g < MG; ++g) rb[g] = Xbase[(static_cast<size_t>(kt) * a.Rg + gc[g]) * 64];
   };
 
-  const int rsub = lane & 15;
-  const int nq = 4 * (lane >> 4);
-
   // ---- loads the epilogue needs, issued ahead of the weight stream so that
   // their latency hides under it (decode shapes; larger tiles load them late)
   constexpr bool kHoist = MG * NT <= 2;
-  // consumer: x^2 partials (r = 1/sqrt(sum x^2 / H + eps)), read after the
-  // weight prefetch is issued; each thread adds a strided subset of one row's
-  // partials, the subsets are then added in a fixed order, so the result does
-  // not depend on timing
-  constexpr int kThreads = 64 * WN * WK;
-  constexpr int kRows = MG * 16;
-  constexpr int kTpr = kThreads / kRows;  // threads per row
-  constexpr int kLd = 16;                 // independent loads per round
-  static_assert(kThreads % kRows == 0, "rows must divide the workgroup");
-  const bool consumer = EPI != EPI_RESID && a.ssq != nullptr;
-  const int ss_rr = threadIdx.x % kRows, ss_sub = threadIdx.x / kRows;
-  const int ss_row = 16 * g0 + ss_rr;
-  // residual: x and the next norm's gains
-  float4 xv[NT][MG];
-  uint2 gv[NT];
+  float4 xv[NT][MG];  // RESID: the residual
   if constexpr (EPI == EPI_RESID && kHoist) {
     if (wk == 0) {
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
         const int n0 = 16 * (nt0 + j) + nq;
-        gv[j] = (tvalid[j] && a.hg_out != nullptr) ? *reinterpret_cast<const uint2*>(a.g_next + n0) : uint2{0u, 0u};
 #pragma unroll
         for (int g = 0; g < MG; ++g) {
           const int row = 16 * (g0 + g) + rsub;
@@ -120,9 +100,8 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
       }
     }
   }
-  // QKV: KV slot and position of the rows, then the rotary factors
-  int q_slot[MG], q_pos[MG];
-  float2 q_cs[NT][MG][2];
+  int q_slot[MG], q_pos[MG];  // QKV: KV slot and position of the rows
+  float2 q_cs[NT][MG][2];     // QKV: rotary factors
   if constexpr (EPI == EPI_QKV && kHoist) {
     if (wk == 0) {
 #pragma unroll
@@ -159,38 +138,18 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
     }
   }
 
-  if (consumer) {
-    double* s_part = reinterpret_cast<double*>(s_ssq_part);
-    double s = 0.0;
-    if (ss_row < a.R) {
-      for (int base = ss_sub; base < a.ssq_parts; base += kLd * kTpr) {
-        double v[kLd];
+  auto step = [&](int st) {
 #pragma unroll
-        for (int j = 0; j < kLd; ++j) {
-          const int p = base + j * kTpr;
-          v[j] = p < a.ssq_parts ? a.ssq[static_cast<size_t>(p) * a.R + ss_row] : 0.0;
-        }
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
-        for (int j = 0; j < kLd; ++j) s += v[j];
-      }
-    }
-    s_part[ss_sub * kRows + ss_rr] = s;
-    __syncthreads();
-    if (threadIdx.x < kRows) {
-      double tot = 0.0;
-      for (int j = 0; j < kTpr; ++j) tot += s_part[j * kRows + threadIdx.x];
-      s_r[threadIdx.x] = 1.0 / sqrt(tot / static_cast<double>(a.norm_dim) + static_cast<double>(a.eps));
-    }
-  }
+      for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
+  };
 
   int it = 0;
   for (; it + PF < n_it; it += PF) {
 #pragma unroll
     for (int st = 0; st < PF; ++st) {
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-#pragma unroll
-        for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
+      step(st);
       load(fa[st], fb[st], it + st + PF);
       // keep each step's refill next to its use instead of batching a
       // whole round of loads at the end of the loop body
@@ -198,14 +157,8 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
     }
   }
 #pragma unroll
-  for (int st = 0; st < PF; ++st) {
-    if (it + st < n_it) {
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-#pragma unroll
-        for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
-    }
-  }
+  for (int st = 0; st < PF; ++st)
+    if (it + st < n_it) step(st);
 
   // ---- reduce the K-split waves of this workgroup (fixed order)
   if constexpr (WK > 1) {
@@ -224,27 +177,11 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 #pragma unroll
           for (int g = 0; g < MG; ++g) acc[j][g] += red[((((w2 - 1) * WN + wn) * NT + j) * MG + g) * 64 + lane];
     }
-  } else {
-    __syncthreads();  // s_r visible
-  }
-
-  // scale the sums by the per-row 1/rms (double product, rounded once to float)
-  if constexpr (EPI != EPI_RESID) {
-    if (a.ssq != nullptr && wk == 0) {
-#pragma unroll
-      for (int g = 0; g < MG; ++g) {
-        const double r = s_r[16 * g + rsub];
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) acc[j][g][q] = static_cast<float>(static_cast<double>(acc[j][g][q]) * r);
-      }
-    }
   }
 
   // ---- epilogues (waves with wk == 0 hold the sums)
   if constexpr (EPI == EPI_RESID) {
-    // x += y; frags of bf16(x * g_next); this workgroup's share of sum x^2 per row
+    // x += y; this workgroup's share of sum x^2 per row
     if (wk == 0) {
 #pragma unroll
       for (int g = 0; g < MG; ++g) {
@@ -263,17 +200,6 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
           v.z += acc[j][g][2];
           v.w += acc[j][g][3];
           *px = v;
-          if (a.hg_out != nullptr) {
-            uint2 gq;
-            if constexpr (kHoist) gq = gv[j];
-            else gq = *reinterpret_cast<const uint2*>(a.g_next + n0);
-            uint2 hv;
-            hv.x = d2bf(static_cast<double>(v.x) * bf2f(gq.x & 0xffffu)) |
-                   (d2bf(static_cast<double>(v.y) * bf2f(gq.x >> 16)) << 16);
-            hv.y = d2bf(static_cast<double>(v.z) * bf2f(gq.y & 0xffffu)) |
-                   (d2bf(static_cast<double>(v.w) * bf2f(gq.y >> 16)) << 16);
-            *reinterpret_cast<uint2*>(a.hg_out + frag_index(row, n0, a.hg_Rg)) = hv;
-          }
           ss += static_cast<double>(v.x) * v.x + static_cast<double>(v.y) * v.y +
                 static_cast<double>(v.z) * v.z + static_cast<double>(v.w) * v.w;
         }
@@ -429,9 +355,9 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, hipStream_t s) {
 }
 
 // Launch shapes.  mg = 16-row groups of X per tile.  For mg == 1:
-//  narrow  one 16-row N tile per wave, 8 K-split waves, 8 K tiles in flight
-//          (residual projections: N = hidden);
-//  pair    two N tiles per wave, 4 K tiles in flight (QKV, gate/up);
+//  narrow  one 16-column N tile per wave, 8 K-split waves, 8 K steps in
+//          flight (residual projections: N = hidden);
+//  pair    two N tiles per wave, 4 K steps in flight (QKV, gate/up);
 //  wide    four N tiles per wave (lm_head).
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
@@ -453,7 +379,7 @@ GemmPlan plan_gemm(int N, int K, int R, int epi) {
   p.mg = Rg <= 1 ? 1 : Rg <= 2 ? 2 : Rg <= 4 ? 4 : 8;
   p.m_tiles = (Rg + p.mg - 1) / p.mg;
   p.nt = 1;
-  if (p.mg == 1 && epi != EPI_RESID) p.nt = (epi == EPI_LOGITS && N / 64 >= 256) ? 4 : 2;
+  if (p.mg == 1 && epi != EPI_RESID) p.nt = epi == EPI_LOGITS ? 4 : 2;
   const int rows_per_group = p.mg == 1 ? 16 * p.nt : p.mg == 2 ? 16 : 64;
   p.n_groups = (N / 16 * 16 + rows_per_group - 1) / rows_per_group;
   return p;

@@ -13,8 +13,7 @@ namespace vsk {
 // projection consumes: frags of bf16(x * g) and per-16-column partial sums
 // of x^2 (ssq[c/16][r]).  Token ids outside [0, V) give a zero row.
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, const int32_t* __restrict__ ids,
-                                               int H, int V, const uint16_t* __restrict__ g, float* __restrict__ x,
-                                               uint16_t* __restrict__ hg, int hg_Rg, double* __restrict__ ssq) {
+                                               int H, int V, float* __restrict__ x, double* __restrict__ ssq) {
   __shared__ double s_ss[4];
   const int r = blockIdx.x;
   const int id = ids[r];
@@ -32,15 +31,8 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, c
     float4* dst = reinterpret_cast<float4*>(x + static_cast<size_t>(r) * H + c);
     dst[0] = make_float4(e[0], e[1], e[2], e[3]);
     dst[1] = make_float4(e[4], e[5], e[6], e[7]);
-    const u32x4 gv = *reinterpret_cast<const u32x4*>(g + c);
-    u32x4 o;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      o[k] = d2bf(static_cast<double>(e[2 * k]) * bf2f(gv[k] & 0xffffu)) |
-             (d2bf(static_cast<double>(e[2 * k + 1]) * bf2f(gv[k] >> 16)) << 16);
-      ss += static_cast<double>(e[2 * k]) * e[2 * k] + static_cast<double>(e[2 * k + 1]) * e[2 * k + 1];
-    }
-    *reinterpret_cast<u32x4*>(hg + frag_index(r, c, hg_Rg)) = o;
+    for (int k = 0; k < 8; ++k) ss += static_cast<double>(e[k]) * e[k];
   }
   // whole-row sum of x^2 in a fixed order: one partial per row
 #pragma unroll
@@ -50,36 +42,84 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, c
   if (threadIdx.x == 0) ssq[r] = (s_ss[0] + s_ss[1]) + (s_ss[2] + s_ss[3]);
 }
 
-hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, const uint16_t* g, float* x,
-                        uint16_t* hg, int hg_Rg, double* ssq, hipStream_t s) {
-  hipLaunchKernelGGL(k_embed, dim3(R), dim3(256), 0, s, E, ids, H, V, g, x, hg, hg_Rg, ssq);
+hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, float* x, double* ssq,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(k_embed, dim3(R), dim3(256), 0, s, E, ids, H, V, x, ssq);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- row gather
-// Compact the frags and x^2 partials of the rows that return logits (a
-// prefill pass asks for a few rows out of many).  Indices outside [0, R_in)
-// give a zero row.
-__global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict__ hg_in, int Rg_in,
-                                                     const double* __restrict__ ssq_in, int parts, int R_in,
+// Compact the residual rows that return logits (a prefill pass asks for a
+// few rows out of many) with each row's sum of x^2 (one partial per row, in
+// a fixed order).  Indices outside [0, R_in) give a zero row.
+__global__ __launch_bounds__(256) void k_gather_rows(const float* __restrict__ x_in, int R_in,
                                                      const int32_t* __restrict__ rows, int H,
-                                                     uint16_t* __restrict__ hg_out, int Rg_out,
-                                                     double* __restrict__ ssq_out, int Ro) {
+                                                     float* __restrict__ x_out, double* __restrict__ ssq_out) {
+  __shared__ double s_ss[4];
   const int i = blockIdx.x;
   const int src = rows[i];
   const bool valid = src >= 0 && src < R_in;
-  for (int c = threadIdx.x * 8; c < H; c += blockDim.x * 8)
-    *reinterpret_cast<u32x4*>(hg_out + frag_index(i, c, Rg_out)) =
-        valid ? *reinterpret_cast<const u32x4*>(hg_in + frag_index(src, c, Rg_in)) : u32x4{0u, 0u, 0u, 0u};
-  for (int p = threadIdx.x; p < parts; p += blockDim.x)
-    ssq_out[static_cast<size_t>(p) * Ro + i] = valid ? ssq_in[static_cast<size_t>(p) * R_in + src] : 0.0;
+  double ss = 0.0;
+  for (int c = threadIdx.x * 4; c < H; c += blockDim.x * 4) {
+    const float4 v = valid ? *reinterpret_cast<const float4*>(x_in + static_cast<size_t>(src) * H + c)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<float4*>(x_out + static_cast<size_t>(i) * H + c) = v;
+    ss += static_cast<double>(v.x) * v.x + static_cast<double>(v.y) * v.y + static_cast<double>(v.z) * v.z +
+          static_cast<double>(v.w) * v.w;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+  if ((threadIdx.x & 63) == 0) s_ss[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (threadIdx.x == 0) ssq_out[i] = (s_ss[0] + s_ss[1]) + (s_ss[2] + s_ss[3]);
 }
 
-hipError_t launch_gather_rows(const uint16_t* hg_in, int Rg_in, const double* ssq_in, int parts, int R_in,
-                              const int32_t* rows, int Ro, int H, uint16_t* hg_out, int Rg_out, double* ssq_out,
-                              hipStream_t s) {
-  hipLaunchKernelGGL(k_gather_rows, dim3(Ro), dim3(256), 0, s, hg_in, Rg_in, ssq_in, parts, R_in, rows, H, hg_out,
-                     Rg_out, ssq_out, Ro);
+hipError_t launch_gather_rows(const float* x_in, int R_in, const int32_t* rows, int Ro, int H, float* x_out,
+                              double* ssq_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_gather_rows, dim3(Ro), dim3(256), 0, s, x_in, R_in, rows, H, x_out, ssq_out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- RMSNorm
+// h = bf16(x * g / sqrt(mean(x^2) + eps)), written as frags for the
+// projection that follows (the rounding point of the norm's output).  The
+// residual projection that produced x also wrote per-workgroup partial sums
+// of x^2; every workgroup of a row adds them in the same fixed order, so all
+// of them hold the same r, and the row is normalised in one pass over x.
+// One wave per 512 elements of a row: each lane writes 8 (one 16-byte frag
+// piece); the product is taken in double and rounded once.
+__global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ x, const uint16_t* __restrict__ g,
+                                                      const double* __restrict__ ssq, int parts, int R, int H,
+                                                      float eps, uint16_t* __restrict__ hg, int Rg) {
+  const int r = blockIdx.y;
+  const int c = blockIdx.x * 512 + threadIdx.x * 8;
+  const bool on = c < H;
+  const float* xr = x + static_cast<size_t>(r) * H;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+  u32x4 gv = u32x4{0u, 0u, 0u, 0u};
+  if (on) {
+    a = *reinterpret_cast<const float4*>(xr + c);
+    b = *reinterpret_cast<const float4*>(xr + c + 4);
+    gv = *reinterpret_cast<const u32x4*>(g + c);
+  }
+  double s = 0.0;
+  for (int p = threadIdx.x; p < parts; p += 64) s += ssq[static_cast<size_t>(p) * R + r];
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
+  const double rr = 1.0 / sqrt(s / static_cast<double>(H) + static_cast<double>(eps));
+  if (!on) return;
+  const float e[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  u32x4 o;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    o[k] = d2bf(static_cast<double>(e[2 * k]) * bf2f(gv[k] & 0xffffu) * rr) |
+           (d2bf(static_cast<double>(e[2 * k + 1]) * bf2f(gv[k] >> 16) * rr) << 16);
+  *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
+}
+
+hipError_t launch_rmsnorm_frags(const float* x, const uint16_t* g, const double* ssq, int parts, int R, int H,
+                                float eps, uint16_t* hg, int Rg, hipStream_t s) {
+  hipLaunchKernelGGL(k_rmsnorm_frags, dim3((H + 511) / 512, R), dim3(64), 0, s, x, g, ssq, parts, R, H, eps, hg, Rg);
   return hipGetLastError();
 }
 

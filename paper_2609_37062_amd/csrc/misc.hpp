@@ -5,11 +5,12 @@
 
 namespace vsk {
 
-hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, const uint16_t* g, float* x,
-                        uint16_t* hg, int hg_Rg, double* ssq, hipStream_t s);
-hipError_t launch_gather_rows(const uint16_t* hg_in, int Rg_in, const double* ssq_in, int parts, int R_in,
-                              const int32_t* rows, int Ro, int H, uint16_t* hg_out, int Rg_out, double* ssq_out,
-                              hipStream_t s);
+hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int V, float* x, double* ssq,
+                        hipStream_t s);
+hipError_t launch_gather_rows(const float* x_in, int R_in, const int32_t* rows, int Ro, int H, float* x_out,
+                              double* ssq_out, hipStream_t s);
+hipError_t launch_rmsnorm_frags(const float* x, const uint16_t* g, const double* ssq, int parts, int R, int H,
+                                float eps, uint16_t* hg, int Rg, hipStream_t s);
 hipError_t launch_argmax_partials(const float* pv, const int* pi, int n_groups, int R, int32_t* ids,
                                   hipStream_t s);
 hipError_t launch_pack(const uint16_t* s0, const uint16_t* s1, const uint16_t* s2, int n0, int n1, int N, int K,
