@@ -43,6 +43,10 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-layers", type=int, default=2, help="layers in the CPU oracle sample")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--mode", type=int, default=0,
+                    help="execution path: 0 automatic, 1 one kernel per operation, 2 persistent step kernel")
+    ap.add_argument("--trace", action="store_true",
+                    help="print the persistent kernel's per-phase timeline (stderr) after the timed steps")
     ap.add_argument("--profile-pass", action="store_true",
                     help="for rocprofv3 runs: set up the workload, run one plain copy of "
                          f"{CALIB_BYTES >> 20} MiB (counter calibration), then --steps passes; no JSON")
@@ -126,10 +130,54 @@ def time_steps(torch, fn, steps, warmup, stream):
     return e0.elapsed_time(e1) / steps, wall
 
 
-def measure(torch, w, steps, warmup, use_graph, probe=True):
+PHASES = ("qkv", "attention", "o_proj", "gate_up", "down")
+
+
+def step_timeline(torch, d, reps=3):
+    """Per-phase times of the persistent kernel from its timestamp trace:
+    for each phase kind, the mean over layers of the span from the first
+    workgroup's release at the previous point to the last workgroup's arrival
+    (span), the median workgroup's busy time (busy) and the release latency
+    after the last arrival (sync).  Microseconds, median of `reps` passes."""
+    n_wgs, n_pts = d.eng.set_step_trace(0, 0)
+    if n_wgs == 0:
+        return None
+    buf = torch.zeros(n_pts * n_wgs * 2, dtype=torch.int64, device=d.device)
+    d.eng.set_step_trace(buf.data_ptr(), buf.numel() * 8)
+    runs = []
+    for _ in range(reps):
+        d.step()
+        torch.cuda.synchronize()
+        t = buf.cpu().numpy().reshape(n_pts, n_wgs, 2).astype(np.float64) * 0.01  # 100 MHz -> us
+        runs.append(t)
+    d.eng.set_step_trace(0, 0)
+    L = (n_pts - 2) // 5
+    out = {}
+    for name, pts in [("embed", [0])] + [(PHASES[k], [1 + 5 * l + k for l in range(L)]) for k in range(5)] + \
+            [("lm_head", [5 * L + 1])]:
+        span, busy, sync = [], [], []
+        for t in runs:
+            for p in pts:
+                if p == 0:
+                    continue
+                arr, rel = t[p, :, 0], t[p, :, 1]
+                prev = t[p - 1, :, 1]
+                span.append(arr.max() - prev.min())
+                busy.append(np.median(arr - prev))
+                sync.append(rel.min() - arr.max())
+        if span:
+            out[name] = {"span_us": round(float(np.median(span)), 2), "busy_us": round(float(np.median(busy)), 2),
+                         "sync_us": round(float(np.median(sync)), 2), "count": len(pts)}
+    tot = [t[-1, :, 1].max() - t[0, :, 0].min() for t in runs]
+    out["total_us_from_first_point"] = round(float(np.median(tot)), 1)
+    return out
+
+
+def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False):
     from paper_2609_37062_amd.runner import DeviceRun
     print(f"[bench] setting up {w.name}", file=sys.stderr, flush=True)
     d = DeviceRun(w)
+    d.eng.set_tuning(2, mode)
     stream = torch.cuda.current_stream()
     res = {}
     ms_eager, wall_eager = time_steps(torch, d.step, steps, warmup, stream)
@@ -156,7 +204,22 @@ def measure(torch, w, steps, warmup, use_graph, probe=True):
         lg_e, ids_e = d.results()
         res["graph_matches_eager"] = bool(np.array_equal(lg_g, lg_e) and np.array_equal(ids_g, ids_e))
         del g
-    if probe:
+    res["persistent"] = bool(d.eng.exec_counters()[5])
+    if probe and res["persistent"]:
+        # the whole step is one kernel: HIP events around each launch on its stream
+        ev = HipEvents()
+        b, e = ev.create(steps), ev.create(steps)
+        sp = stream.cuda_stream
+        for i in range(steps):
+            ev.L.hipEventRecord(C.c_void_p(b[i]), C.c_void_p(sp))
+            d.step(stream=sp)
+            ev.L.hipEventRecord(C.c_void_p(e[i]), C.c_void_p(sp))
+        torch.cuda.synchronize()
+        durs = [ev.elapsed_ms(b[i], e[i]) for i in range(steps)]
+        ev.destroy(b + e)
+        res["kernel_ms"] = float(np.mean(durs))
+        res["kernel_ms_median"] = float(np.median(durs))
+    elif probe:
         ev = HipEvents()
         n = steps * w.model.n_layers
         b, e = ev.create(n), ev.create(n)
@@ -167,9 +230,13 @@ def measure(torch, w, steps, warmup, use_graph, probe=True):
         durs = [ev.elapsed_ms(b[i], e[i]) for i in range(n)]
         d.eng.set_probe(0, [], [])
         ev.destroy(b + e)
-        res["gateup_ms"] = float(np.mean(durs))
-        res["gateup_ms_median"] = float(np.median(durs))
-    res["counters"] = d.eng.exec_counters().tolist()[:5]
+        res["kernel_ms"] = float(np.mean(durs))
+        res["kernel_ms_median"] = float(np.median(durs))
+    if trace and res["persistent"]:
+        res["timeline"] = step_timeline(torch, d)
+        print(f"[bench] {w.name} timeline: {json.dumps(res['timeline'])}", file=sys.stderr, flush=True)
+    d.eng.device_status(stream.cuda_stream)
+    res["counters"] = d.eng.exec_counters().tolist()[:6]
     d.release()
     del d
     torch.cuda.empty_cache()
@@ -228,6 +295,7 @@ def main():
     if a.profile_pass:
         from paper_2609_37062_amd.runner import DeviceRun
         d = DeviceRun(w)
+        d.eng.set_tuning(2, a.mode)
         src = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         src.fill_(1)
@@ -240,12 +308,17 @@ def main():
         print(f"[bench] profile pass: {w.name}, {a.steps} steps, calibration copy {CALIB_BYTES} bytes",
               file=sys.stderr)
         return
-    r = measure(torch, w, a.steps, a.warmup, not a.no_graph)
+    r = measure(torch, w, a.steps, a.warmup, not a.no_graph, mode=a.mode, trace=a.trace)
     ms = min(r["ms_eager"], r.get("ms_graph", float("inf")))
     tokps = w.n_rows / (ms / 1e3)
     sb = step_bytes(w)
-    gb = gateup_bytes(w.model, w.n_rows)
-    achieved = gb / (r["gateup_ms"] / 1e3)
+    if r["persistent"]:
+        kname = "persistent decode step (k_step: every layer's projections, attention, lm_head, argmax)"
+        kb = sb
+    else:
+        kname = "gate/up projection + SwiGLU (k_gemm, EPI_SWIGLU)"
+        kb = gateup_bytes(w.model, w.n_rows)
+    achieved = kb / (r["kernel_ms"] / 1e3)
     out = {
         "metric": "decode-step latency (ms) & tokens/s at batch 16/64; achieved HBM TB/s vs peak",
         "value": round(tokps, 1),
@@ -269,16 +342,18 @@ def main():
         "step_bytes": sb,
         "step_hbm_TBps": round(sb / (ms / 1e3) / 1e12, 3),
         "step_hbm_frac": round(sb / (ms / 1e3) / PEAK_HBM, 4),
-        "roofline": {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm, EPI_SWIGLU)",
+        "roofline": {"bound": "hbm", "kernel": kname,
                      "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM, 4),
-                     "traffic": gateup_traffic() if a.workload == 2 else None,
-                     "bytes_per_launch": gb, "avg_launch_ms": round(r["gateup_ms"], 5)},
+                     "traffic": (None if r["persistent"] else gateup_traffic()) if a.workload == 2 else None,
+                     "bytes_per_launch": kb, "avg_launch_ms": round(r["kernel_ms"], 5)},
         "exec_counters": r["counters"],
     }
+    if "timeline" in r:
+        out["timeline"] = r["timeline"]
     if not a.no_batch64 and a.workload == 2:
         w3 = workload(3)
-        r3 = measure(torch, w3, a.steps, a.warmup, not a.no_graph, probe=False)
+        r3 = measure(torch, w3, a.steps, a.warmup, not a.no_graph, probe=False, mode=a.mode if a.mode != 2 else 0)
         ms3 = min(r3["ms_eager"], r3.get("ms_graph", float("inf")))
         sb3 = step_bytes(w3)
         out["batch64_shared_prefix"] = {

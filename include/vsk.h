@@ -213,7 +213,15 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        8..512), or 0 (the default) for automatic: 32 when fewer than 256
  *        (row, KV head) pairs are in the pass, else 128.
  * key 1: inspection only -- run just the first `value` layers before the
- *        final norm and lm_head (0 = all layers), for layer-local checks. */
+ *        final norm and lm_head (0 = all layers), for layer-local checks.
+ * key 2: execution path.  0 (default) and 1: one kernel per operation.
+ *        2: the whole pass as one persistent kernel (one workgroup per
+ *        compute unit, grid synchronisation between the phases of a layer,
+ *        the next projection's weight stream started before each wait); it
+ *        covers decode passes of at most 16 rows (workspace sized for at most
+ *        16 rows) whose every projection K is a multiple of 256 and at least
+ *        2048, with hidden at most 4096, and returns VSK_E_UNSUPPORTED for
+ *        other passes.  Both paths compute the same values. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the
@@ -222,9 +230,26 @@ int vsk_residual_copy(vsk_handle* h, void* dst_dev, int32_t n_rows, void* stream
 
 /* Counters of what the last pass executed (kernel variants, split factors),
  * for attestation in tests and benchmarks.  Writes up to cap int64 values:
- * [0] passes run, [1] gemm launches, [2] attention launches, [3] attention
- * splits (max per row), [4] gemm K-splits of the last down projection. */
+ * [0] passes run, [1] projection phases, [2] attention phases, [3] attention
+ * splits (max per row), [4] workgroups per 16-column tile of the last down
+ * projection, [5] 1 if the last pass ran as the persistent kernel, else 0. */
 int vsk_exec_counters(const vsk_handle* h, int64_t* out, int32_t cap);
+
+/* Measurement: while buf_dev is set (NULL clears it), each persistent pass
+ * writes, per synchronisation point and workgroup, two uint64 timestamps of
+ * the device's constant 100 MHz clock: when the workgroup arrived at the
+ * point and when it was released from it ([points][workgroups][2]; a
+ * buffer too small for the pass is ignored).  *n_wgs and *n_points
+ * (nullable) receive the workgroup count of a persistent launch on the
+ * current device (0: the kernel cannot run there) and the points of a pass. */
+int vsk_set_step_trace(vsk_handle* h, void* buf_dev, size_t bytes, int32_t* n_wgs, int32_t* n_points);
+
+/* Synchronise `stream`, then report whether a persistent pass on the bound
+ * workspace failed: VSK_OK, or VSK_E_HIP when one of its grid
+ * synchronisation waits exceeded its spin limit (the kernel then ended
+ * without finishing the pass; the error stays recorded until
+ * vsk_workspace_init) or the stream reported a HIP error. */
+int vsk_device_status(vsk_handle* h, void* stream);
 
 #ifdef __cplusplus
 }

@@ -12,10 +12,15 @@
 #include "gemm.hpp"
 #include "internal.hpp"
 #include "misc.hpp"
+#include "step.hpp"
 
 using namespace vsk;
 
 struct vsk_handle : public Handle {};
+
+namespace vsk {
+static int step_workgroups(Handle& h);
+}
 
 namespace vsk {
 
@@ -70,6 +75,20 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   // lm_head argmax partials: n_groups x rows
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
+  // persistent decode step: every per-layer buffer is written once per launch
+  w.step = max_rows <= kStepMaxRows && step_shape_ok(c);
+  if (w.step) {
+    const size_t L = c.n_layers, nx = 2 * L + 1, R = max_rows;
+    w.s_x = o; o = align_up(o + nx * R * H * 4);
+    w.s_ssq = o; o = align_up(o + nx * (H / 16) * R * 8);
+    w.s_q = o; o = align_up(o + L * R * Nq * 2);
+    w.s_o = o; o = align_up(o + L * kStepMaxRows * Nq * 2);
+    w.s_a = o; o = align_up(o + L * kStepMaxRows * F * 2);
+    w.s_am = o; o = align_up(o + static_cast<size_t>(c.vocab / 16) * R * 8);
+    w.s_flags = o; o = align_up(o + static_cast<size_t>(step_syncs(c.n_layers)) * kSyncCounters * kFlagWords * 4);
+    w.s_err = o; o = align_up(o + 4);
+    w.s_epoch = o; o = align_up(o + 4);
+  }
   w.total = o;
   return w;
 }
@@ -433,6 +452,8 @@ int vsk_decode_step(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int
   if (h->bd.max_q_len != 1) return fail(h, VSK_E_ARG, "decode_step needs one row per sequence");
   PassArgs a{ids_dev, nullptr, h->bd.n_rows, static_cast<uint16_t*>(logits_dev), next_ids_dev,
              static_cast<uint8_t*>(ws_dev), h->wl};
+  if (h->exec_mode == 2 && !step_eligible(*h, a))
+    return fail(h, VSK_E_UNSUPPORTED, "the persistent step kernel does not cover this pass (rows, shape or device)");
   return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "decode step");
 }
 
@@ -444,6 +465,7 @@ int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logi
     return fail(h, VSK_E_ARG, "logit rows must be 1..n_rows");
   PassArgs a{ids_dev, logit_rows_dev, n_logit_rows, static_cast<uint16_t*>(logits_dev), next_ids_dev,
              static_cast<uint8_t*>(ws_dev), h->wl};
+  if (h->exec_mode == 2) return fail(h, VSK_E_UNSUPPORTED, "the persistent step kernel serves decode passes only");
   return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "prefill chunk");
 }
 
@@ -478,6 +500,10 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       if (value < 0 || value > h->cfg.n_layers) return fail(h, VSK_E_ARG, "layer count out of range");
       h->layers_run = value;
       return VSK_OK;
+    case 2:
+      if (value < 0 || value > 2) return fail(h, VSK_E_ARG, "execution mode must be 0, 1 or 2");
+      h->exec_mode = value;
+      return VSK_OK;
     default:
       return fail(h, VSK_E_ARG, "unknown tuning key");
   }
@@ -498,16 +524,130 @@ int vsk_exec_counters(const vsk_handle* h, int64_t* out, int32_t cap) {
   return VSK_OK;
 }
 
+int vsk_set_step_trace(vsk_handle* h, void* buf_dev, size_t bytes, int32_t* n_wgs, int32_t* n_points) {
+  if (!h) return VSK_E_ARG;
+  if (buf_dev && reinterpret_cast<uintptr_t>(buf_dev) % 8) return fail(h, VSK_E_ARG, "trace buffer not 8-byte aligned");
+  h->step_trace = static_cast<uint64_t*>(buf_dev);
+  h->step_trace_cap = buf_dev ? bytes / 8 : 0;
+  const int wgs = step_workgroups(*h);
+  if (n_wgs) *n_wgs = wgs;
+  if (n_points) *n_points = step_syncs(h->layers_run > 0 ? h->layers_run : h->cfg.n_layers);
+  return VSK_OK;
+}
+
+int vsk_device_status(vsk_handle* h, void* stream) {
+  if (!h) return VSK_E_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_check(h, e, "stream");
+  if (!h->ws || !h->wl.step) return VSK_OK;
+  uint32_t err = 0;
+  e = hipMemcpyAsync(&err, h->ws + h->wl.s_err, 4, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_check(h, e, "status read");
+  if (err != 0)
+    return fail(h, VSK_E_HIP, "a persistent pass (epoch " + std::to_string(err) +
+                                  ") timed out at a grid synchronisation point; re-initialise the workspace");
+  return VSK_OK;
+}
+
 }  // extern "C"
 
 // ------------------------------------------------------------------ the pass
 namespace vsk {
+
+// Workgroups of a persistent launch on the current device: one per compute
+// unit when the kernel fits there with its LDS (0 when it does not).
+static int step_workgroups(Handle& h) {
+  if (h.step_wgs < 0) {
+    int dev = 0, cus = 0;
+    h.step_wgs = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        step_occupancy(h.cfg) >= 1)
+      h.step_wgs = std::min(cus, kStepMaxWgs);
+  }
+  return h.step_wgs;
+}
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+static hipError_t run_step(Handle& h, const PassArgs& pa, int n_wgs, hipStream_t s) {
+  const vsk_model_cfg& c = h.cfg;
+  const BatchDev& b = h.bd;
+  const WsLayout& wl = pa.wl;
+  uint8_t* ws = pa.ws;
+  const int d = c.head_dim;
+  StepArgs a{};
+  a.n_run = h.layers_run > 0 ? h.layers_run : c.n_layers;
+  a.H = c.hidden;
+  a.Nq = c.n_q_heads * d;
+  a.Nkv = c.n_kv_heads * d;
+  a.F = c.ffn;
+  a.V = c.vocab;
+  a.hd = d;
+  a.G = c.n_q_heads / c.n_kv_heads;
+  a.Hkv = c.n_kv_heads;
+  a.eps = c.rms_eps;
+  a.P = h.packed;
+  a.layer_bytes = h.pl.layer_bytes;
+  a.lo = h.pl.l;
+  a.embed = reinterpret_cast<const uint16_t*>(h.packed + h.pl.embed);
+  a.lm_head = reinterpret_cast<const u32x4_t*>(h.packed + h.pl.lm_head);
+  a.final_gain = reinterpret_cast<const uint16_t*>(h.packed + h.pl.final_norm);
+  a.rope = reinterpret_cast<const float2*>(h.packed + h.pl.rope);
+  a.pool = h.pool;
+  a.n_blocks = h.n_blocks;
+  a.R = b.n_rows;
+  a.ids = pa.ids;
+  a.pos = b.pos;
+  a.slot = b.slot;
+  a.row_seq = b.row_seq;
+  a.block_table = b.block_table;
+  a.max_blocks = b.max_blocks;
+  a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d)));
+  a.bps = h.attn_bps > 0 ? h.attn_bps : attn_auto_bps(b.n_rows, c.n_kv_heads);
+  a.max_splits = attn_splits(b.max_kv_len, a.bps);
+  a.part_o = reinterpret_cast<float*>(ws + wl.att_o);
+  a.part_ml = reinterpret_cast<float2*>(ws + wl.att_ml);
+  a.att_cnt = reinterpret_cast<int*>(ws + wl.att_cnt);
+  a.xs = reinterpret_cast<float*>(ws + wl.s_x);
+  a.ssq = reinterpret_cast<double*>(ws + wl.s_ssq);
+  a.qs = reinterpret_cast<uint16_t*>(ws + wl.s_q);
+  a.os = reinterpret_cast<uint16_t*>(ws + wl.s_o);
+  a.as = reinterpret_cast<uint16_t*>(ws + wl.s_a);
+  a.am_val = reinterpret_cast<float*>(ws + wl.s_am);
+  a.am_idx = reinterpret_cast<int*>(ws + wl.s_am + static_cast<size_t>(c.vocab / 16) * wl.max_rows * 4);
+  a.flags = reinterpret_cast<unsigned*>(ws + wl.s_flags);
+  a.err = reinterpret_cast<unsigned*>(ws + wl.s_err);
+  a.epoch_ctr = reinterpret_cast<unsigned*>(ws + wl.s_epoch);
+  a.x_out = reinterpret_cast<float*>(ws + wl.x);
+  a.logits = pa.logits;
+  a.next_ids = pa.next_ids;
+  a.trace = h.step_trace_cap >= static_cast<size_t>(step_syncs(c.n_layers)) * n_wgs * 2 ? h.step_trace : nullptr;
+  hipError_t e = launch_step(a, n_wgs, step_lds_bytes(c), s);
+  if (e != hipSuccess) return e;
+  h.counters[0] += 1;
+  h.counters[1] += 4 * a.n_run + 1;
+  h.counters[2] += a.n_run;
+  h.counters[3] = a.max_splits;
+  h.counters[4] = 1;
+  h.counters[5] = 1;
+  return hipSuccess;
+}
+
+bool step_eligible(Handle& h, const PassArgs& pa) {
+  return h.exec_mode == 2 && pa.logit_rows == nullptr && h.bd.max_q_len == 1 && pa.wl.step &&
+         h.bd.n_rows <= kStepMaxRows && step_workgroups(h) > 0;
+}
 
 hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   const vsk_model_cfg& c = h.cfg;
   const BatchDev& b = h.bd;
   const WsLayout& wl = pa.wl;
   const int R = b.n_rows;
+  // the persistent step kernel serves decode passes of up to 16 rows
+  if (step_eligible(h, pa)) return run_step(h, pa, step_workgroups(h), s);
   const int Rg = (R + 15) / 16;
   const int H = c.hidden, F = c.ffn, d = c.head_dim, Nq = c.n_q_heads * d, Nkv = c.n_kv_heads * d;
   uint8_t* ws = pa.ws;
@@ -663,6 +803,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   h.counters[2] += n_run;
   h.counters[3] = aa.max_splits;
   h.counters[4] = p_d.n_groups;
+  h.counters[5] = 0;
   return hipSuccess;
 }
 

@@ -51,6 +51,34 @@ __device__ __forceinline__ f32x4 mfma_16x16x16(u32x2 a, u32x2 b, f32x4 c) {
                                                    __builtin_bit_cast(bf16x4_t, b), c, 0, 0, 0);
 }
 
+// Write-through stores (sc1): the data goes to memory instead of staying in
+// this XCD's L2, so a workgroup on another XCD of the same launch reads it
+// once this wave's memory counter has drained.  Plain stores are only made
+// visible to other XCDs at the end of the kernel.
+__device__ __forceinline__ void store_wt(void* p, u32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void store_wt(void* p, u32x2 v) {
+  asm volatile("global_store_dwordx2 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void store_wt(void* p, uint32_t v) {
+  asm volatile("global_store_dword %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void store_wt(void* p, double v) { store_wt(p, __builtin_bit_cast(u32x2, v)); }
+__device__ __forceinline__ void store_wt16(void* p, uint32_t v) {
+  asm volatile("global_store_short %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+}
+
+// threadIdx.x through an opaque move: values derived from it inside a
+// phase of a persistent kernel are then computed in that phase instead of
+// being hoisted out of the surrounding loop and held in registers across
+// every other phase.
+__device__ __forceinline__ int opaque_tid() {
+  int t;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"(static_cast<int>(threadIdx.x)));
+  return t;
+}
+
 __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
 __device__ __forceinline__ int shfl_xor(int v, int m) { return __shfl_xor(v, m, 64); }
 

@@ -84,6 +84,10 @@ struct BatchDev {
 struct WsLayout {
   int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
   size_t x, x_c, fa, fb, fc, q, att_o, att_ml, att_cnt, ssq, ssq_c, am_part, total;
+  // persistent decode step (present when max_rows <= kStepMaxRows and the
+  // model shape is covered): per-layer activations, sync flags, error word, epoch
+  bool step = false;
+  size_t s_x, s_ssq, s_q, s_o, s_a, s_am, s_flags, s_err, s_epoch;
 };
 
 // attention split: 16-token blocks per split-K work item (tunable, >= kAttnMinBps)
@@ -119,6 +123,10 @@ struct Handle {
   // tuning
   int attn_bps = 0;  // 0: attn_auto_bps
   int layers_run = 0;  // inspection: run only the first layers_run layers (0 = all)
+  int exec_mode = 0;   // 0 automatic, 1 one kernel per operation, 2 persistent step kernel
+  int step_wgs = -1;   // workgroups of a persistent launch on this device (0: not runnable; -1: not queried)
+  uint64_t* step_trace = nullptr;  // measurement: timestamp buffer of the persistent kernel
+  size_t step_trace_cap = 0;       // its capacity in uint64
   // workspace
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
@@ -156,5 +164,7 @@ struct PassArgs {
   WsLayout wl;
 };
 hipError_t run_pass(Handle& h, const PassArgs& a, hipStream_t s);
+// True when run_pass would take the persistent step kernel for this pass.
+bool step_eligible(Handle& h, const PassArgs& a);
 
 }  // namespace vsk

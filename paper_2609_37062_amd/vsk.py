@@ -77,6 +77,8 @@ SIGNATURES = [
     ("vsk_residual_copy", C.c_int, [_VP, _VP, _I32, _VP]),
     ("vsk_set_probe", C.c_int, [_VP, _I32, C.POINTER(_VP), C.POINTER(_VP), _I32]),
     ("vsk_exec_counters", C.c_int, [_VP, _PI64, _I32]),
+    ("vsk_set_step_trace", C.c_int, [_VP, _VP, _SZ, _PI32, _PI32]),
+    ("vsk_device_status", C.c_int, [_VP, _VP]),
 ]
 
 _lib = None
@@ -265,6 +267,17 @@ class Engine:
         B = (C.c_void_p * max(n, 1))(*begin_events)
         E = (C.c_void_p * max(n, 1))(*end_events)
         self._ck(lib().vsk_set_probe(self.h, which, B, E, n), "set_probe")
+
+    def set_step_trace(self, ptr, nbytes):
+        """Point the persistent kernel's timestamp trace at a device buffer (0 clears it).
+        Returns (workgroups per launch, synchronisation points per pass)."""
+        n, p = C.c_int32(), C.c_int32()
+        self._ck(lib().vsk_set_step_trace(self.h, ptr or None, nbytes, C.byref(n), C.byref(p)), "set_step_trace")
+        return n.value, p.value
+
+    def device_status(self, stream=None):
+        """Synchronise the stream and raise if a persistent pass timed out at a grid sync."""
+        self._ck(lib().vsk_device_status(self.h, stream), "device_status")
 
     def exec_counters(self):
         out = np.zeros(8, np.int64)
