@@ -221,7 +221,12 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        covers decode passes of at most 16 rows (workspace sized for at most
  *        16 rows) whose every projection K is a multiple of 256 and at least
  *        2048, with hidden at most 4096, and returns VSK_E_UNSUPPORTED for
- *        other passes.  Both paths compute the same values. */
+ *        other passes.  Both paths compute the same values.
+ * key 3: launch shape of the per-operation projections for 33..128 rows
+ *        (and longer row-tiled passes): 0 (default) one column of eight
+ *        K-split waves per workgroup over one 16-column tile (residual and
+ *        QKV projections) or two (gate/up, lm_head); 1 one tile everywhere;
+ *        2 two tiles everywhere; 3 a 2 x 2 grid of waves over four tiles. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

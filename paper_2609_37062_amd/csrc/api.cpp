@@ -504,6 +504,10 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       if (value < 0 || value > 2) return fail(h, VSK_E_ARG, "execution mode must be 0, 1 or 2");
       h->exec_mode = value;
       return VSK_OK;
+    case 3:
+      if (value < 0 || value > 3) return fail(h, VSK_E_ARG, "projection shape must be 0..3");
+      h->gemm_shape = value;
+      return VSK_OK;
     default:
       return fail(h, VSK_E_ARG, "unknown tuning key");
   }
@@ -723,10 +727,10 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   aa.out = fa;
   aa.out_Rg = Rg;
 
-  const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV);
-  const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID);
-  const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU);
-  const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID);
+  const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape);
+  const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape);
+  const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape);
+  const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape);
 
   // RMSNorm: one pass over x using the x^2 partials of the step that wrote it
   auto norm = [&](const uint16_t* gain, const float* xin, int rows, int rg, const double* sq, int parts) {
@@ -783,7 +787,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   } else {
     TRY(norm(final_gain, x, Ro, Rgo, ssq, ssq_parts));
   }
-  const GemmPlan p_lm = plan_gemm(c.vocab, H, Ro, EPI_LOGITS);
+  const GemmPlan p_lm = plan_gemm(c.vocab, H, Ro, EPI_LOGITS, h.gemm_shape);
   ga.W = reinterpret_cast<const u4*>(P + h.pl.lm_head);
   ga.X = reinterpret_cast<const u4*>(fb);
   ga.Kt = H / 32;

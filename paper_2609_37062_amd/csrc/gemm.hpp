@@ -31,10 +31,12 @@ struct GemmPlan {
   int mg = 1;        // 16-row groups per tile
   int m_tiles = 1;   // tiles along the rows
   int n_groups = 1;  // workgroups along N (also the number of x^2 partials a RESID emits)
-  int nt = 1;        // N tiles per wave (mg == 1)
+  int nt = 1;        // N tiles per wave
+  int wn = 1;        // waves side by side along N
 };
 
-GemmPlan plan_gemm(int N, int K, int R, int epi);
+// shape: launch shape for 4 or 8 row groups (0 default; see k_gemm.hip)
+GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0);
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s);
 
 }  // namespace vsk

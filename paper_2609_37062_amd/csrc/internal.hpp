@@ -124,6 +124,7 @@ struct Handle {
   int attn_bps = 0;  // 0: attn_auto_bps
   int layers_run = 0;  // inspection: run only the first layers_run layers (0 = all)
   int exec_mode = 0;   // 0 automatic, 1 one kernel per operation, 2 persistent step kernel
+  int gemm_shape = 0;  // projection launch shape for 4 or 8 row groups (0 default)
   int step_wgs = -1;   // workgroups of a persistent launch on this device (0: not runnable; -1: not queried)
   uint64_t* step_trace = nullptr;  // measurement: timestamp buffer of the persistent kernel
   size_t step_trace_cap = 0;       // its capacity in uint64

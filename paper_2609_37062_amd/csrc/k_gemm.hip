@@ -82,12 +82,19 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
     for (int g = 0; g < MG; ++g) rb[g] = Xbase[(static_cast<size_t>(kt) * a.Rg + gc[g]) * 64];
   };
 
-  // ---- loads the epilogue needs, issued ahead of the weight stream so that
-  // their latency hides under it (decode shapes; larger tiles load them late)
+  // ---- loads the epilogue needs.  They are all issued before the first
+  // store of the epilogue: behind a store to a buffer the compiler cannot
+  // prove disjoint, each would otherwise wait for a full memory round trip
+  // of its own.  Small tiles issue them ahead of the weight stream, so that
+  // their latency hides under it; larger ones (more registers) right after
+  // the stream, before the cross-wave reduction.
   constexpr bool kHoist = MG * NT <= 2;
-  float4 xv[NT][MG];  // RESID: the residual
-  if constexpr (EPI == EPI_RESID && kHoist) {
-    if (wk == 0) {
+  float4 xv[NT][MG];          // RESID: the residual
+  int q_slot[MG], q_pos[MG];  // QKV: KV slot and position of the rows
+  float2 q_cs[NT][MG][2];     // QKV: rotary factors
+  auto epi_loads_a = [&]() {
+    if (wk != 0) return;
+    if constexpr (EPI == EPI_RESID) {
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
         const int n0 = 16 * (nt0 + j) + nq;
@@ -98,12 +105,7 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
                                               : make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
-    }
-  }
-  int q_slot[MG], q_pos[MG];  // QKV: KV slot and position of the rows
-  float2 q_cs[NT][MG][2];     // QKV: rotary factors
-  if constexpr (EPI == EPI_QKV && kHoist) {
-    if (wk == 0) {
+    } else if constexpr (EPI == EPI_QKV) {
 #pragma unroll
       for (int g = 0; g < MG; ++g) {
         const int row = 16 * (g0 + g) + rsub;
@@ -111,15 +113,10 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
         q_pos[g] = row < a.R ? a.pos[row] : 0;
       }
     }
-  }
-
-  if (n_it > 0) {
-#pragma unroll
-    for (int st = 0; st < PF; ++st) load(fa[st], fb[st], st);
-  }
-
-  if constexpr (EPI == EPI_QKV && kHoist) {
-    if (wk == 0) {
+  };
+  auto epi_loads_b = [&]() {  // rotary factors, after the positions
+    if (wk != 0) return;
+    if constexpr (EPI == EPI_QKV) {
       const int half = a.hd >> 1;
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
@@ -136,7 +133,15 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
         }
       }
     }
+  };
+  if constexpr (kHoist) epi_loads_a();
+
+  if (n_it > 0) {
+#pragma unroll
+    for (int st = 0; st < PF; ++st) load(fa[st], fb[st], st);
   }
+
+  if constexpr (kHoist) epi_loads_b();
 
   auto step = [&](int st) {
 #pragma unroll
@@ -160,6 +165,11 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   for (int st = 0; st < PF; ++st)
     if (it + st < n_it) step(st);
 
+  if constexpr (!kHoist) {
+    epi_loads_a();
+    epi_loads_b();
+  }
+
   // ---- reduce the K-split waves of this workgroup (fixed order)
   if constexpr (WK > 1) {
     f32x4* red = reinterpret_cast<f32x4*>(smem);
@@ -171,6 +181,9 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
     }
     __syncthreads();
     if (wk == 0) {
+      // one partner wave at a time: unrolled, the LDS reads of all seven
+      // would be hoisted and hold 28 registers per output tile
+#pragma unroll 1
       for (int w2 = 1; w2 < WK; ++w2)
 #pragma unroll
         for (int j = 0; j < NT; ++j)
@@ -192,9 +205,7 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
           if (!tvalid[j] || row >= a.R) continue;
           const int n0 = 16 * (nt0 + j) + nq;
           float4* px = reinterpret_cast<float4*>(a.x + static_cast<size_t>(row) * a.N + n0);
-          float4 v;
-          if constexpr (kHoist) v = xv[j][g];
-          else v = *px;
+          float4 v = xv[j][g];
           v.x += acc[j][g][0];
           v.y += acc[j][g][1];
           v.z += acc[j][g][2];
@@ -248,23 +259,14 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
           const int row = 16 * (g0 + g) + rsub;
           if (row >= a.R) continue;
           const f32x4 v = acc[j][g];
-          int sl;
-          if constexpr (kHoist) sl = q_slot[g];
-          else sl = a.slot[row];
+          const int sl = q_slot[g];
           const int blk = sl >> 4, t = sl & 15;
           if (n0 < a.Nq + a.Nkv) {
             const int ph = n0 % hd;          // packed row inside the head (multiple of 4)
             const int hb = n0 - ph;          // first packed row of the head
             const int j0 = ph >> 1;          // dims j0, j0+half, j0+1, j0+1+half
-            float2 cs0, cs1;
-            if constexpr (kHoist) {
-              cs0 = q_cs[j][g][0];
-              cs1 = q_cs[j][g][1];
-            } else {
-              const int p = a.pos[row];
-              cs0 = a.rope[static_cast<size_t>(p) * half + j0];
-              cs1 = a.rope[static_cast<size_t>(p) * half + j0 + 1];
-            }
+            const float2 cs0 = q_cs[j][g][0];
+            const float2 cs1 = q_cs[j][g][1];
             const float y0 = v[0] * cs0.x - v[1] * cs0.y;
             const float y1 = v[1] * cs0.x + v[0] * cs0.y;
             const float y2 = v[2] * cs1.x - v[3] * cs1.y;
@@ -359,6 +361,13 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, hipStream_t s) {
 //          flight (residual projections: N = hidden);
 //  pair    two N tiles per wave, 4 K steps in flight (QKV, gate/up);
 //  wide    four N tiles per wave (lm_head).
+// For 4..8 row groups (shape 0, the default) each workgroup is one column of
+// K-split waves (8; 4 for two tiles of 8 row groups, whose cross-wave sums
+// would not fit 64 KiB of LDS) over one N tile (residual, QKV) or two
+// (gate/up, lm_head):
+// N = hidden then still gives 192-256 workgroups.  Shape 1 takes one N tile
+// everywhere, shape 2 two, shape 3 is a 2 x 2 wave grid over four N tiles
+// (fewer workgroups, each X chunk feeding four tiles).
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
   switch (p.mg) {
@@ -367,21 +376,38 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, s);
       return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
     case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
-    case 4: return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
-    default: return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
+    case 4:
+      if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
+      if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, s);
+      return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, s);
+    default:
+      if (p.wn == 2) return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
+      if (p.nt == 2) return launch_cfg<8, 2, 1, 4, 2, EPI>(a, p.m_tiles, s);
+      return launch_cfg<8, 1, 1, 8, 4, EPI>(a, p.m_tiles, s);
   }
 }
 
-GemmPlan plan_gemm(int N, int K, int R, int epi) {
+GemmPlan plan_gemm(int N, int K, int R, int epi, int shape) {
   (void)K;
   GemmPlan p;
   const int Rg = (R + 15) / 16;
   p.mg = Rg <= 1 ? 1 : Rg <= 2 ? 2 : Rg <= 4 ? 4 : 8;
   p.m_tiles = (Rg + p.mg - 1) / p.mg;
   p.nt = 1;
-  if (p.mg == 1 && epi != EPI_RESID) p.nt = epi == EPI_LOGITS ? 4 : 2;
-  const int rows_per_group = p.mg == 1 ? 16 * p.nt : p.mg == 2 ? 16 : 64;
-  p.n_groups = (N / 16 * 16 + rows_per_group - 1) / rows_per_group;
+  p.wn = 1;
+  if (p.mg == 1) {
+    if (epi != EPI_RESID) p.nt = epi == EPI_LOGITS ? 4 : 2;
+  } else if (p.mg >= 4) {
+    const bool wide_n = epi == EPI_SWIGLU || epi == EPI_LOGITS;
+    if (shape == 3) {
+      p.nt = 2;
+      p.wn = 2;
+    } else {
+      p.nt = shape == 1 ? 1 : shape == 2 ? 2 : (wide_n ? 2 : 1);
+    }
+  }
+  const int cols_per_group = 16 * p.nt * p.wn;
+  p.n_groups = (N / 16 * 16 + cols_per_group - 1) / cols_per_group;
   return p;
 }
 

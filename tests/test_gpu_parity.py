@@ -76,6 +76,25 @@ def test_mid_attention_splits(bps):
     print(st)
 
 
+@pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3), (100, 0), (100, 1), (100, 2), (100, 3)])
+def test_mid_projection_shapes(B, shape):
+    """Every launch shape of the projections for 3 and 7 row groups (one or
+    two 16-column tiles per wave column, or a 2 x 2 wave grid)."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    ctx = np.random.default_rng(100 + B).integers(0, 400, size=B)
+    w = decode_workload(MID, ctx, seed=13, name=f"mid-shape-b{B}-s{shape}")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(3, shape)
+    d.step()
+    lg, ids = d.results()
+    d.step()
+    lg2, ids2 = d.results()
+    assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
+    st, *_ = _check(w, lg, ids, list(range(0, B, max(1, B // 12))))
+    print(st)
+
+
 def test_mid_shared_prefix():
     ctx = 256 + np.random.default_rng(5).integers(3, 40, size=12)
     w = decode_workload(MID, ctx, seed=4, shared=256, name="mid-shared")
