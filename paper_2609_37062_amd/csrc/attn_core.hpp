@@ -56,7 +56,7 @@ __device__ __forceinline__ int attn_row_splits(int kv_len, int bps) {
 // WT: the attention output is stored write-through (sc1), so that other
 // workgroups of the same launch read it from memory, not from a stale L2.
 template <int D, int NB, bool WT>
-__device__ void attn_unit(const AttnArgs& a, int row, int hk, int split, AttnLds<D>& sm) {
+__device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, int split, AttnLds<D>& sm) {
   constexpr int KC = D / 32;  // K chunks (1 KiB) per block
   constexpr int VC = D / 16;  // V chunks (512 B) per block
 

@@ -102,8 +102,17 @@ __global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ 
     b = *reinterpret_cast<const float4*>(xr + c + 4);
     gv = *reinterpret_cast<const u32x4*>(g + c);
   }
+  // partials p = lane, lane + 64, ... added in that order; four are loaded
+  // before the first is added, so their latencies overlap
   double s = 0.0;
-  for (int p = threadIdx.x; p < parts; p += 64) s += ssq[static_cast<size_t>(p) * R + r];
+  for (int p0 = threadIdx.x; p0 < parts; p0 += 256) {
+    double v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = p0 + 64 * q < parts ? ssq[static_cast<size_t>(p0 + 64 * q) * R + r] : 0.0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (p0 + 64 * q < parts) s += v[q];
+  }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
   const double rr = 1.0 / sqrt(s / static_cast<double>(H) + static_cast<double>(eps));
@@ -150,8 +159,21 @@ __global__ __launch_bounds__(256) void k_argmax_partials(const float* __restrict
   const int r = blockIdx.x;
   float bv = -INFINITY;
   int bi = INT_MAX;
-  for (int g = threadIdx.x; g < n_groups; g += blockDim.x)
-    am_merge(bv, bi, pv[static_cast<size_t>(g) * R + r], pi[static_cast<size_t>(g) * R + r]);
+  // eight partials per lane are loaded before any is merged (the merge is a
+  // total order on (value, -index), so its order does not matter)
+  constexpr int kU = 8;
+  for (int g0 = threadIdx.x; g0 < n_groups; g0 += kU * blockDim.x) {
+    float v[kU];
+    int i[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int g = g0 + u * blockDim.x;
+      v[u] = g < n_groups ? pv[static_cast<size_t>(g) * R + r] : -INFINITY;
+      i[u] = g < n_groups ? pi[static_cast<size_t>(g) * R + r] : INT_MAX;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) am_merge(bv, bi, v[u], i[u]);
+  }
   block_am_reduce(bv, bi);
   if (threadIdx.x == 0) ids[r] = (bi == INT_MAX) ? 0 : bi;
 }

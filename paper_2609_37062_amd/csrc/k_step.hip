@@ -55,6 +55,7 @@ constexpr int kPF = 8;                    // weight tiles in flight per wave
 constexpr unsigned kSpinLimit = 1u << 21; // a few seconds of polling before a wait is declared failed
 constexpr size_t kLdsRed = 2 * (kWaves - 1) * 1024;  // double-buffered cross-wave reduction
 constexpr int kAttnBlocksInFlight = 2;    // K/V blocks in flight per wave in the attention phase
+constexpr int kMaxParts = 256;            // sum-of-squares partials per row (hidden / 16, hidden <= 4096)
 
 __device__ __forceinline__ unsigned ld_agent_u32(const unsigned* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -70,7 +71,7 @@ struct Sync {
   uint64_t* trace;  // nullable: [points][gridDim.x][2] arrival and release times (100 MHz clock)
 };
 
-__device__ void arrive(const Sync& s, int point) {
+__device__ __forceinline__ void arrive(const Sync& s, int point) {
   __builtin_amdgcn_s_waitcnt(0);  // this wave's write-through stores have reached memory
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -88,7 +89,7 @@ __device__ void arrive(const Sync& s, int point) {
 // (one counter each) with a pause between polls: polls go to memory, and
 // hundreds of idle workgroups polling without pause would take a large share
 // of the bandwidth the streaming workgroups need.
-__device__ bool await(const Sync& s, int point) {
+__device__ __forceinline__ bool await(const Sync& s, int point) {
   int bad = 0;
   if (threadIdx.x < kSyncCounters) {
     const unsigned n = (gridDim.x - threadIdx.x + kSyncCounters - 1) / kSyncCounters;
@@ -150,42 +151,69 @@ struct NormIn {
 // steps w, w+8, ... of the 16 rows as B-operand frags, h = bf16(x g r) with
 // r = 1/sqrt(sum x^2 / H + eps) summed from `parts` per-tile partials in a
 // fixed order (the same order and arithmetic as the per-op norm kernel).
-__device__ void stage_norm(const float* __restrict__ x, const uint16_t* __restrict__ gain,
+__device__ __forceinline__ void stage_norm(const float* __restrict__ x, const uint16_t* __restrict__ gain,
                            const double* __restrict__ ssq, int parts, int R, int H, float eps, unsigned char* lds) {
   const int tid = opaque_tid();
   const int lane = tid & 63, w = tid >> 6;
   double* s_r = reinterpret_cast<double*>(lds + static_cast<size_t>(H / 256) * kWaves * 1024 + kLdsRed);
+  // this wave's two rows: every partial this lane adds is loaded before the
+  // first sum (at most kParts / 64 per row), then added in partial order
+  constexpr int kPl = kMaxParts / 64;
+  double pv[2][kPl];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int row = 2 * w + k;
+#pragma unroll
+    for (int q = 0; q < kPl; ++q) {
+      const int p = lane + 64 * q;
+      pv[k][q] = (row < R && p < parts) ? as_global(ssq)[static_cast<size_t>(p) * R + row] : 0.0;
+    }
+  }
+#pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int row = 2 * w + k;
     double s = 0.0;
-    if (row < R)
-      for (int p = lane; p < parts; p += 64) s += as_global(ssq)[static_cast<size_t>(p) * R + row];
+#pragma unroll
+    for (int q = 0; q < kPl; ++q)
+      if (lane + 64 * q < parts) s += pv[k][q];
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
-    if (lane == 0) s_r[row] = 1.0 / sqrt(s / static_cast<double>(H) + static_cast<double>(eps));
+    if (lane == 0 && row < R) s_r[row] = 1.0 / sqrt(s / static_cast<double>(H) + static_cast<double>(eps));
   }
   __syncthreads();
   const int row = lane & 15, c8 = 8 * (lane >> 4);
   const int S = H / 256;
   const double rr = row < R ? s_r[row] : 0.0;
   u32x4* dst = reinterpret_cast<u32x4*>(lds) + static_cast<size_t>(w) * S * 64 + lane;
-  // one K step at a time: the products are taken in double, and unrolling
-  // would hold more doubles than the registers the other phases leave free
-#pragma unroll 1
-  for (int i = 0; i < S; ++i) {
-    const int c = 32 * (w + kWaves * i) + c8;
-    u32x4 o = u32x4{0u, 0u, 0u, 0u};
-    if (row < R) {
-      const float4 a = __builtin_bit_cast(float4, ldg4(x + static_cast<size_t>(row) * H + c));
-      const float4 b = __builtin_bit_cast(float4, ldg4(x + static_cast<size_t>(row) * H + c + 4));
-      const u32x4 gv = ldg4(gain + c);
-      const float e[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  // four K steps per round: their loads are all issued before the first
+  // product (one memory round trip per round instead of one per K step),
+  // and the products are taken in double
+  constexpr int kR = 4;
+  for (int i0 = 0; i0 < S; i0 += kR) {
+    float4 va[kR], vb[kR];
+    u32x4 gv[kR];
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        o[k] = d2bf(static_cast<double>(e[2 * k]) * bf2f(gv[k] & 0xffffu) * rr) |
-               (d2bf(static_cast<double>(e[2 * k + 1]) * bf2f(gv[k] >> 16) * rr) << 16);
+    for (int k = 0; k < kR; ++k) {
+      const int c = 32 * (w + kWaves * (i0 + k)) + c8;
+      const bool ok = row < R && i0 + k < S;
+      const float* xp = x + static_cast<size_t>(ok ? row : 0) * H + (ok ? c : 0);
+      va[k] = __builtin_bit_cast(float4, ldg4(xp));
+      vb[k] = __builtin_bit_cast(float4, ldg4(xp + 4));
+      gv[k] = ldg4(gain + (ok ? c : 0));
     }
-    dst[static_cast<size_t>(i) * 64] = o;
+#pragma unroll
+    for (int k = 0; k < kR; ++k) {
+      if (i0 + k >= S) break;
+      u32x4 o = u32x4{0u, 0u, 0u, 0u};
+      if (row < R) {
+        const float e[8] = {va[k].x, va[k].y, va[k].z, va[k].w, vb[k].x, vb[k].y, vb[k].z, vb[k].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          o[q] = d2bf(static_cast<double>(e[2 * q]) * bf2f(gv[k][q] & 0xffffu) * rr) |
+                 (d2bf(static_cast<double>(e[2 * q + 1]) * bf2f(gv[k][q] >> 16) * rr) << 16);
+      }
+      dst[static_cast<size_t>(i0 + k) * 64] = o;
+    }
   }
 }
 
@@ -239,7 +267,7 @@ __device__ __forceinline__ void epi_pre(const Epi& e, int unit, EpiPre& p) {
 }
 
 template <int EPI>
-__device__ void epilogue(const Epi& e, int unit, const f32x4 v, const EpiPre& p) {
+__device__ __forceinline__ void epilogue(const Epi& e, int unit, const f32x4 v, const EpiPre& p) {
   const int lane = threadIdx.x & 63;
   const int row = lane & 15;
   const int n0 = 16 * unit + 4 * (lane >> 4);
@@ -333,7 +361,7 @@ __device__ void epilogue(const Epi& e, int unit, const f32x4 v, const EpiPre& p)
 // g.Xf beside the weights), then run the units.  Returns false when a wait
 // of this pass failed.
 template <int EPI, bool XN>
-__device__ bool gemm_phase(const GemmPh& g, const Epi& e, const NormIn& ni, float eps, unsigned char* lds,
+__device__ __forceinline__ bool gemm_phase(const GemmPh& g, const Epi& e, const NormIn& ni, float eps, unsigned char* lds,
                            const Sync& sy, int point) {
   const int tid = opaque_tid();
   const int lane = tid & 63, w = tid >> 6;
@@ -449,7 +477,7 @@ __device__ bool gemm_phase(const GemmPh& g, const Epi& e, const NormIn& ni, floa
 // ---------------------------------------------------------------- small phases
 // x[0] = float(E[id]) and one partial of sum x^2 per row (the per-op
 // embedding kernel's arithmetic and order, on its first 256 threads).
-__device__ void embed_phase(const StepArgs& a, unsigned char* lds) {
+__device__ __forceinline__ void embed_phase(const StepArgs& a, unsigned char* lds) {
   double* s_ss = reinterpret_cast<double*>(lds);
   for (int r = blockIdx.x; r < a.R; r += gridDim.x) {
     double ss = 0.0;
@@ -483,15 +511,27 @@ __device__ void embed_phase(const StepArgs& a, unsigned char* lds) {
 
 // Greedy ids from the lm_head partials ([tiles][R]), lowest index of the
 // maximum; and the final residual copied out for inspection.
-__device__ void argmax_phase(const StepArgs& a, const float* x_fin, unsigned char* lds) {
+__device__ __forceinline__ void argmax_phase(const StepArgs& a, const float* x_fin, unsigned char* lds) {
   float* s_v = reinterpret_cast<float*>(lds);
   int* s_i = reinterpret_cast<int*>(lds + 64);
   const int tiles = a.V / 16;
   for (int r = blockIdx.x; r < a.R; r += gridDim.x) {
     float bv = -INFINITY;
     int bi = INT_MAX;
-    for (int t = threadIdx.x; t < tiles; t += blockDim.x)
-      am_merge(bv, bi, a.am_val[static_cast<size_t>(t) * a.R + r], a.am_idx[static_cast<size_t>(t) * a.R + r]);
+    // eight partials per lane loaded before any is merged (the merge is a
+    // total order on (value, -index), so its order does not matter)
+    for (int t0 = threadIdx.x; t0 < tiles; t0 += 8 * blockDim.x) {
+      float v[8];
+      int ix[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int t = t0 + u * blockDim.x;
+        v[u] = t < tiles ? a.am_val[static_cast<size_t>(t) * a.R + r] : -INFINITY;
+        ix[u] = t < tiles ? a.am_idx[static_cast<size_t>(t) * a.R + r] : INT_MAX;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) am_merge(bv, bi, v[u], ix[u]);
+    }
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) {
       const float v2 = shfl_xor(bv, m);
