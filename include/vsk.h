@@ -153,6 +153,15 @@ int vsk_batch_build(vsk_handle* h, const int64_t* seqs_host, const int32_t* q_le
 int vsk_batch_shape(const vsk_handle* h, int32_t* n_seqs, int32_t* n_rows, int32_t* max_blocks);
 int vsk_batch_host_copy(const vsk_handle* h, int32_t* block_table, int32_t* kv_len, int32_t* cu_q,
                         int32_t* row_seq, int32_t* pos, int32_t* slot);
+/* Shared prefixes of the built batch (decode passes only; paper, "Invariants
+ * for Correct Mixed-Depth Execution": the page mappings are rebuilt per pass).
+ * Sequences whose block tables start with the same blocks form a group when
+ * at least two share at least 4 full blocks before their current tokens; the
+ * group's prefix is the longest such run.  The pass then reads each prefix
+ * block once per group instead of once per sequence (unless tuning key 4
+ * turns it off).  pfx_blocks_host (nullable) int32[n_rows]: prefix blocks of
+ * each row's group, 0 for a row in no group; n_groups (nullable). */
+int vsk_batch_prefix_info(const vsk_handle* h, int32_t* pfx_blocks_host, int32_t* n_groups);
 /* Device bytes needed by vsk_batch_upload for the current batch. */
 size_t vsk_batch_device_bytes(const vsk_handle* h);
 /* Copy the metadata into caller device memory (H2D on stream) and make it
@@ -226,7 +235,10 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        (and longer row-tiled passes): 0 (default) one column of eight
  *        K-split waves per workgroup over one 16-column tile (residual and
  *        QKV projections) or two (gate/up, lm_head); 1 one tile everywhere;
- *        2 two tiles everywhere; 3 a 2 x 2 grid of waves over four tiles. */
+ *        2 two tiles everywhere; 3 a 2 x 2 grid of waves over four tiles.
+ * key 4: shared prefixes of a decode pass (vsk_batch_prefix_info): 1 (the
+ *        default) reads each group's prefix blocks once for the group, 0 reads
+ *        them once per sequence. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

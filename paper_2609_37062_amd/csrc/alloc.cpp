@@ -1,6 +1,9 @@
 // Host-side KV block allocator and batch metadata builder (see alloc.hpp).
 #include "alloc.hpp"
 
+#include <climits>
+#include <map>
+
 #include <algorithm>
 #include <unordered_set>
 
@@ -194,8 +197,75 @@ int build_batch(const BlockAllocator& a, const int64_t* seqs, const int32_t* q_l
       b.slot[r] = s->blocks[p / bs] * bs + p % bs;
     }
   }
+  b.pfx_blocks.assign(b.n_rows, 0);
+  if (b.max_q_len == 1) find_shared_prefixes(b, bs);
   out = std::move(b);
   return kOk;
+}
+
+void plan_prefix_items(BatchHost& b, int32_t group_size, int32_t n_kv_heads, int32_t target_wgs) {
+  b.pfx_splits.assign(b.n_rows, 0);
+  b.pfx_items.clear();
+  b.max_pfx_splits = 0;
+  const int32_t ng = b.n_groups();
+  if (ng == 0) return;
+  auto cdiv = [](int32_t x, int32_t y) { return (x + y - 1) / y; };
+  int32_t chunks = 0;
+  for (int32_t g = 0; g < ng; ++g) chunks += cdiv(b.grp_info[4 * g + 1] * group_size, kPfxCols);
+  const int32_t want = std::max(1, cdiv(target_wgs, chunks * n_kv_heads));
+  for (int32_t g = 0; g < ng; ++g) {
+    const int32_t off = b.grp_info[4 * g], rows = b.grp_info[4 * g + 1], P = b.grp_info[4 * g + 2];
+    const int32_t lo = cdiv(P, kMaxPfxBps), hi = std::min(kMaxPfxSplits, std::max(1, P / 2));
+    int32_t splits = std::max(lo, std::min(want, hi));
+    const int32_t bps = cdiv(P, splits);
+    splits = cdiv(P, bps);
+    b.max_pfx_splits = std::max(b.max_pfx_splits, splits);
+    for (int32_t k = 0; k < rows; ++k) b.pfx_splits[b.grp_rows[off + k]] = splits;
+    for (int32_t c0 = 0; c0 < rows * group_size; c0 += kPfxCols)
+      for (int32_t sp = 0; sp < splits; ++sp) {
+        const int32_t it[5] = {g, c0, sp * bps, std::min(P, (sp + 1) * bps), sp};
+        b.pfx_items.insert(b.pfx_items.end(), it, it + 5);
+      }
+  }
+}
+
+void find_shared_prefixes(BatchHost& b, int32_t block, int32_t min_blocks) {
+  b.pfx_blocks.assign(b.n_rows, 0);
+  b.grp_rows.clear();
+  b.grp_info.clear();
+  b.pfx_tbl.clear();
+  if (b.max_q_len != 1) return;
+  // sequences by first block, in sequence order
+  std::map<int32_t, std::vector<int32_t>> by_first;
+  for (int32_t i = 0; i < b.n_seqs; ++i) {
+    const int32_t full = (b.kv_len[i] - 1) / block;  // blocks before the current token's block
+    if (full >= min_blocks) by_first[b.block_table[static_cast<size_t>(i) * b.max_blocks]].push_back(i);
+  }
+  for (const auto& kv : by_first) {
+    const std::vector<int32_t>& m = kv.second;
+    if (m.size() < 2) continue;
+    int32_t lim = INT32_MAX;
+    for (int32_t i : m) lim = std::min(lim, (b.kv_len[i] - 1) / block);
+    const int32_t* t0 = b.block_table.data() + static_cast<size_t>(m[0]) * b.max_blocks;
+    int32_t p = 0;
+    for (; p < lim; ++p) {
+      bool same = true;
+      for (size_t k = 1; k < m.size() && same; ++k)
+        same = b.block_table[static_cast<size_t>(m[k]) * b.max_blocks + p] == t0[p];
+      if (!same) break;
+    }
+    if (p < min_blocks) continue;
+    b.grp_info.push_back(static_cast<int32_t>(b.grp_rows.size()));
+    b.grp_info.push_back(static_cast<int32_t>(m.size()));
+    b.grp_info.push_back(p);
+    b.grp_info.push_back(static_cast<int32_t>(b.pfx_tbl.size()));
+    b.pfx_tbl.insert(b.pfx_tbl.end(), t0, t0 + p);
+    for (int32_t i : m) {
+      const int32_t r = b.cu_q[i];  // the sequence's one row
+      b.grp_rows.push_back(r);
+      b.pfx_blocks[r] = p;
+    }
+  }
 }
 
 }  // namespace vsk

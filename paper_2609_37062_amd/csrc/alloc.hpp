@@ -67,7 +67,37 @@ struct BatchHost {
   std::vector<int32_t> row_seq;      // [n_rows]
   std::vector<int32_t> pos;          // [n_rows]
   std::vector<int32_t> slot;         // [n_rows]
+  // Shared prefixes of a decode pass: groups of sequences whose tables start
+  // with the same full blocks before each member's current token.
+  std::vector<int32_t> pfx_blocks;   // [n_rows] blocks of the row's group prefix (0: none)
+  std::vector<int32_t> grp_rows;     // rows of every group, group by group
+  std::vector<int32_t> grp_info;     // [n_groups][4]: first entry in grp_rows, rows, prefix blocks, first entry in pfx_tbl
+  std::vector<int32_t> pfx_tbl;      // every group's prefix block ids, group by group
+  int32_t n_groups() const { return static_cast<int32_t>(grp_info.size() / 4); }
+  // Work items of the shared-prefix attention (plan_prefix_items)
+  std::vector<int32_t> pfx_splits;   // [n_rows] prefix splits of the row's group (0: none)
+  std::vector<int32_t> pfx_items;    // [n_items][5]: group, first column, first block, end block, split
+  int32_t max_pfx_splits = 0;
+  int32_t n_pfx_items() const { return static_cast<int32_t>(pfx_items.size() / 5); }
 };
+
+// Columns (row, query head) of one shared-prefix work item: 8 waves x 16.
+constexpr int32_t kPfxCols = 128;
+// Most prefix splits of one group, and the largest split (blocks).
+constexpr int32_t kMaxPfxSplits = 16;
+constexpr int32_t kMaxPfxBps = 512;
+// Split every group's prefix so that the work items of all groups and KV
+// heads come to about target_wgs workgroups (at least 2 blocks per split).
+void plan_prefix_items(BatchHost& b, int32_t group_size, int32_t n_kv_heads, int32_t target_wgs = 128);
+
+// Smallest common prefix (in blocks) worth reading once for a group.
+constexpr int32_t kMinSharedPrefixBlocks = 4;
+// Fill the shared-prefix fields of a decode pass (one row per sequence):
+// sequences are grouped by their first block; a group's prefix is the
+// longest run of leading blocks that every member holds and that lies
+// wholly before every member's current token.  Groups of one sequence and
+// prefixes shorter than min_blocks are dropped.
+void find_shared_prefixes(BatchHost& b, int32_t block, int32_t min_blocks = kMinSharedPrefixBlocks);
 
 int build_batch(const BlockAllocator& a, const int64_t* seqs, const int32_t* q_lens, int32_t n,
                 BatchHost& out, std::string& err);

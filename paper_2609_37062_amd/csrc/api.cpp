@@ -54,7 +54,8 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   w.max_seqs = max_seqs;
   w.max_kv_len = max_kv_len;
   w.Rg = ceil_div(max_rows, 16);
-  w.max_splits = attn_splits(max_kv_len, kAttnMinBps);
+  // a row's own splits, and the prefix splits of its group ahead of them
+  w.max_splits = attn_splits(max_kv_len, kAttnMinBps) + kMaxPfxSplits;
   const size_t H = c.hidden, F = c.ffn, Nq = static_cast<size_t>(c.n_q_heads) * c.head_dim;
   const size_t Rp = static_cast<size_t>(w.Rg) * 16;
   const int G = c.n_q_heads / c.n_kv_heads;
@@ -335,6 +336,7 @@ int vsk_batch_build(vsk_handle* h, const int64_t* seqs_host, const int32_t* q_le
   BatchHost b;
   int st = build_batch(h->alloc, seqs_host, q_lens_host, n_seqs, b, h->err);
   if (st != VSK_OK) return st;
+  plan_prefix_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads, h->cfg.n_kv_heads);
   h->bh = std::move(b);
   h->batch_built = true;
   h->batch_uploaded = false;
@@ -365,9 +367,17 @@ int vsk_batch_host_copy(const vsk_handle* h, int32_t* block_table, int32_t* kv_l
   return VSK_OK;
 }
 
+int vsk_batch_prefix_info(const vsk_handle* h, int32_t* pfx_blocks_host, int32_t* n_groups) {
+  if (!h || !h->batch_built) return VSK_E_STATE;
+  if (pfx_blocks_host) std::memcpy(pfx_blocks_host, h->bh.pfx_blocks.data(), h->bh.pfx_blocks.size() * 4);
+  if (n_groups) *n_groups = h->bh.n_groups();
+  return VSK_OK;
+}
+
 static size_t meta_bytes(const BatchHost& b) {
-  return align_up(b.block_table.size() * 4) + align_up(b.kv_len.size() * 4) + align_up(b.cu_q.size() * 4) +
-         3 * align_up(static_cast<size_t>(b.n_rows) * 4);
+  auto sz = [](const std::vector<int32_t>& v) { return align_up(std::max<size_t>(v.size(), 1) * 4); };
+  return sz(b.block_table) + sz(b.kv_len) + sz(b.cu_q) + sz(b.row_seq) + sz(b.pos) + sz(b.slot) +
+         sz(b.pfx_blocks) + sz(b.pfx_splits) + sz(b.pfx_items) + sz(b.grp_rows) + sz(b.grp_info) + sz(b.pfx_tbl);
 }
 
 size_t vsk_batch_device_bytes(const vsk_handle* h) {
@@ -396,6 +406,14 @@ int vsk_batch_upload(vsk_handle* h, void* meta_dev, size_t bytes, void* stream) 
   put(b.row_seq, &d.row_seq);
   put(b.pos, &d.pos);
   put(b.slot, &d.slot);
+  put(b.pfx_blocks, &d.pfx_blocks);
+  put(b.pfx_splits, &d.pfx_splits);
+  put(b.pfx_items, &d.pfx_items);
+  put(b.grp_rows, &d.grp_rows);
+  put(b.grp_info, &d.grp_info);
+  put(b.pfx_tbl, &d.pfx_tbl);
+  d.n_pfx_items = b.n_pfx_items();
+  d.max_pfx_splits = b.max_pfx_splits;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(meta_dev, staging.data(), staging.size(), hipMemcpyHostToDevice, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);  // staging is a local buffer
@@ -507,6 +525,10 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
     case 3:
       if (value < 0 || value > 3) return fail(h, VSK_E_ARG, "projection shape must be 0..3");
       h->gemm_shape = value;
+      return VSK_OK;
+    case 4:
+      if (value < 0 || value > 1) return fail(h, VSK_E_ARG, "shared-prefix switch must be 0 or 1");
+      h->shared_prefix = value;
       return VSK_OK;
     default:
       return fail(h, VSK_E_ARG, "unknown tuning key");
@@ -726,6 +748,29 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   aa.counter = reinterpret_cast<int*>(ws + wl.att_cnt);
   aa.out = fa;
   aa.out_Rg = Rg;
+  // shared prefixes of a decode pass: read once per group by k_attn_prefix
+  const bool cascade = h.shared_prefix != 0 && b.n_pfx_items > 0 && pa.logit_rows == nullptr;
+  aa.split_stride = aa.max_splits + (cascade ? b.max_pfx_splits : 0);
+  aa.pfx_blocks = cascade ? b.pfx_blocks : nullptr;
+  aa.pfx_splits = cascade ? b.pfx_splits : nullptr;
+  AttnPrefixArgs ap{};
+  ap.q = q;
+  ap.pool = h.pool;
+  ap.n_blocks = h.n_blocks;
+  ap.Hkv = c.n_kv_heads;
+  ap.G = aa.G;
+  ap.Nq = Nq;
+  ap.block_table = b.block_table;
+  ap.max_blocks = b.max_blocks;
+  ap.row_seq = b.row_seq;
+  ap.items = b.pfx_items;
+  ap.grp_rows = b.grp_rows;
+  ap.grp_info = b.grp_info;
+  ap.pfx_tbl = b.pfx_tbl;
+  ap.scale_log2 = aa.scale_log2;
+  ap.split_stride = aa.split_stride;
+  ap.part_o = aa.part_o;
+  ap.part_ml = aa.part_ml;
 
   const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape);
   const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape);
@@ -750,6 +795,10 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     ga.layer = l;
     TRY(probed(2, [&] { return launch_gemm(ga, p_qkv, EPI_QKV, s); }));
     aa.layer = l;
+    if (cascade) {
+      ap.layer = l;
+      TRY(launch_attn_prefix(ap, b.n_pfx_items, d, s));
+    }
     TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
     // O projection: x += o Wo^T, with the x^2 partials of the updated rows
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);

@@ -1,12 +1,12 @@
 // One work item of paged-attention decode: (row, KV head, split of the
-// context), processed by a workgroup of kAttnWaves waves.  Shared by the
+// context), processed by a workgroup of NW waves.  Shared by the
 // per-op attention kernel (k_attn.hip) and the persistent step kernel
 // (k_step.hip).
 //
 // For every row (one token at position p of its sequence) and KV head, the
 // query heads of that KV head's group attend to keys 0..p read through the
 // sequence's block table (paper, "Invariants": each layer reads its own
-// cached K,V; Algorithm 1 keeps attention's launch shape).  The eight waves
+// cached K,V; Algorithm 1 keeps attention's launch shape).  The NW waves
 // take the split's 16-token blocks as contiguous ranges.  The split's
 // block-table entries are staged in LDS first; each wave then keeps NB
 // blocks of K/V loads in flight ahead of the block it processes.  Per block
@@ -26,15 +26,15 @@
 
 namespace vsk {
 
-constexpr int kAttnWaves = 8;
+constexpr int kAttnWaves = 4;  // waves of a per-op decode work item (the persistent kernel uses 8)
 
 // LDS of one work item (the persistent kernel overlays it on the space its
 // projections use)
-template <int D>
+template <int D, int NW>
 struct AttnLds {
-  float m[kAttnWaves][16];
-  float l[kAttnWaves][16];
-  f32x4 o[kAttnWaves - 1][D / 16][64];
+  float m[NW][16];
+  float l[NW][16];
+  f32x4 o[NW - 1][D / 16][64];
   int32_t tbl[kAttnMaxBps];
   int last;
 };
@@ -55,8 +55,8 @@ __device__ __forceinline__ int attn_row_splits(int kv_len, int bps) {
 
 // WT: the attention output is stored write-through (sc1), so that other
 // workgroups of the same launch read it from memory, not from a stale L2.
-template <int D, int NB, bool WT>
-__device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, int split, AttnLds<D>& sm) {
+template <int D, int NB, bool WT, int NW>
+__device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, int split, AttnLds<D, NW>& sm) {
   constexpr int KC = D / 32;  // K chunks (1 KiB) per block
   constexpr int VC = D / 16;  // V chunks (512 B) per block
 
@@ -66,11 +66,15 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   const int G = a.G;
   const int kv_len = a.pos[row] + 1;
   const int nb = (kv_len + kBlock - 1) / kBlock;
-  const int n_splits = (nb + a.bps - 1) / a.bps;
+  // a shared prefix of P blocks is read by the prefix work items; this row's
+  // splits cover blocks P.. and follow the prefix partials
+  const int P = a.pfx_blocks != nullptr ? a.pfx_blocks[row] : 0;
+  const int n_ps = P > 0 ? a.pfx_splits[row] : 0;
+  const int n_splits = (nb - P + a.bps - 1) / a.bps;
   if (split >= n_splits) return;
   const int seq = a.row_seq[row];
   const int32_t* table = a.block_table + static_cast<size_t>(seq) * a.max_blocks;
-  const int b_lo = split * a.bps;
+  const int b_lo = P + split * a.bps;
   const int b_hi = min(nb, b_lo + a.bps);
   // the split's block-table entries, staged once for all waves
   for (int i = tid; i < b_hi - b_lo; i += blockDim.x) sm.tbl[i] = table[b_lo + i];
@@ -162,14 +166,36 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   // this wave's blocks: a contiguous range of the split, kept NB blocks ahead.
   // Loads past the range re-read its last block and the final round is
   // peeled, so the loop's loads are unconditional and stay in flight.
-  const int per = (b_hi - b_lo + kAttnWaves - 1) / kAttnWaves;
+  const int per = (b_hi - b_lo + NW - 1) / NW;
   const int w_lo = min(b_hi - b_lo, w * per);
   const int cnt = min(b_hi - b_lo, w_lo + per) - w_lo;
+  u32x4 kf[NB][KC];
+  u32x2 vf[NB][VC];
   if (cnt > 0) {
-    u32x4 kf[NB][KC];
-    u32x2 vf[NB][VC];
 #pragma unroll
     for (int i = 0; i < NB; ++i) load(kf[i], vf[i], sm.tbl[w_lo + min(i, cnt - 1)]);
+  }
+  // the first split starts from the group's shared-prefix partials: wave w
+  // folds in partials w, w + NW, ... (their loads wait behind the K/V loads
+  // just issued, whose latency they share)
+  if (split == 0 && n_ps > 0 && h < G) {
+    const size_t rh0 = static_cast<size_t>(row) * a.Hkv + hk;
+    for (int sp = w; sp < n_ps; sp += NW) {
+      const float* po = a.part_o + ((rh0 * a.split_stride + sp) * G + h) * D;
+      const float2 ml = a.part_ml[(rh0 * a.split_stride + sp) * G + h];
+      f32x4 op[VC];
+#pragma unroll
+      for (int c = 0; c < VC; ++c) op[c] = *reinterpret_cast<const f32x4*>(po + 16 * c + 4 * quad);
+      const float M = fmaxf(m, ml.x);
+      const float f0 = m == -INFINITY ? 0.f : exp2f(m - M);
+      const float f1 = exp2f(ml.x - M);
+      l = l * f0 + ml.y * f1;
+#pragma unroll
+      for (int c = 0; c < VC; ++c) o[c] = o[c] * f0 + op[c] * f1;
+      m = M;
+    }
+  }
+  if (cnt > 0) {
     int base = 0;
     for (; base + NB < cnt; base += NB) {
 #pragma unroll
@@ -196,12 +222,12 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   if (w == 0) {
     float M = sm.m[0][h];
 #pragma unroll
-    for (int w2 = 1; w2 < kAttnWaves; ++w2) M = fmaxf(M, sm.m[w2][h]);
+    for (int w2 = 1; w2 < NW; ++w2) M = fmaxf(M, sm.m[w2][h]);
     const float f0 = exp2f(sm.m[0][h] - M);
     float L = sm.l[0][h] * f0;
 #pragma unroll
     for (int c = 0; c < VC; ++c) o[c] *= f0;
-    for (int w2 = 1; w2 < kAttnWaves; ++w2) {
+    for (int w2 = 1; w2 < NW; ++w2) {
       const float mw = sm.m[w2][h];
       const float f = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
       L += sm.l[w2][h] * f;
@@ -238,13 +264,13 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   // then is the arrival counted.  No workgroup waits for another.
   const size_t rh = static_cast<size_t>(row) * a.Hkv + hk;
   if (w == 0 && h < G) {
-    float* po = a.part_o + ((rh * a.max_splits + split) * G + h) * D;
+    float* po = a.part_o + ((rh * a.split_stride + n_ps + split) * G + h) * D;
 #pragma unroll
     for (int c = 0; c < VC; ++c)
 #pragma unroll
       for (int r = 0; r < 4; ++r) st_agent(po + 16 * c + 4 * quad + r, o[c][r]);
     if (quad == 0) {
-      float* pm = reinterpret_cast<float*>(a.part_ml + (rh * a.max_splits + split) * G + h);
+      float* pm = reinterpret_cast<float*>(a.part_ml + (rh * a.split_stride + n_ps + split) * G + h);
       st_agent(pm, m);
       st_agent(pm + 1, l);
     }
@@ -260,25 +286,27 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   if (!sm.last) return;
 
   // merge: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, in split order
+  // (this row's own splits, which follow its group's prefix partials)
   constexpr int kC = 8;  // splits read with one round of independent loads
-  const float* pml = reinterpret_cast<const float*>(a.part_ml + rh * a.max_splits * G);
-  const float* pob = a.part_o + rh * a.max_splits * G * D;
+  const int n_all = n_splits;
+  const float* pml = reinterpret_cast<const float*>(a.part_ml + (rh * a.split_stride + n_ps) * G);
+  const float* pob = a.part_o + (rh * a.split_stride + n_ps) * G * D;
   for (int idx = tid; idx < G * D; idx += blockDim.x) {
     const int hh = idx / D, e = idx % D;
     float acc = 0.f, L = 0.f, M = -INFINITY;
-    for (int s0 = 0; s0 < n_splits; s0 += kC) {
+    for (int s0 = 0; s0 < n_all; s0 += kC) {
       float mv[kC];
 #pragma unroll
       for (int j = 0; j < kC; ++j)
-        mv[j] = s0 + j < n_splits ? ld_agent(pml + 2 * ((s0 + j) * G + hh)) : -INFINITY;
+        mv[j] = s0 + j < n_all ? ld_agent(pml + 2 * ((s0 + j) * G + hh)) : -INFINITY;
 #pragma unroll
       for (int j = 0; j < kC; ++j) M = fmaxf(M, mv[j]);
     }
-    for (int s0 = 0; s0 < n_splits; s0 += kC) {
+    for (int s0 = 0; s0 < n_all; s0 += kC) {
       float mv[kC], lv[kC], ov[kC];
 #pragma unroll
       for (int j = 0; j < kC; ++j) {
-        const bool ok = s0 + j < n_splits;
+        const bool ok = s0 + j < n_all;
         const int sj = s0 + j;
         mv[j] = ok ? ld_agent(pml + 2 * (sj * G + hh)) : -INFINITY;
         lv[j] = ok ? ld_agent(pml + 2 * (sj * G + hh) + 1) : 0.f;
@@ -286,7 +314,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
       }
 #pragma unroll
       for (int j = 0; j < kC; ++j) {
-        if (s0 + j < n_splits) {
+        if (s0 + j < n_all) {
           const float f = exp2f(mv[j] - M);
           L += lv[j] * f;
           acc += ov[j] * f;

@@ -78,6 +78,14 @@ struct BatchDev {
   const int32_t* row_seq = nullptr;
   const int32_t* pos = nullptr;
   const int32_t* slot = nullptr;
+  // shared prefixes (decode passes): see BatchHost
+  const int32_t* pfx_blocks = nullptr;
+  const int32_t* pfx_splits = nullptr;
+  const int32_t* pfx_items = nullptr;
+  const int32_t* grp_rows = nullptr;
+  const int32_t* grp_info = nullptr;
+  const int32_t* pfx_tbl = nullptr;
+  int32_t n_pfx_items = 0, max_pfx_splits = 0;
 };
 
 // ---------------------------------------------------------------- workspace
@@ -125,6 +133,7 @@ struct Handle {
   int layers_run = 0;  // inspection: run only the first layers_run layers (0 = all)
   int exec_mode = 0;   // 0 automatic, 1 one kernel per operation, 2 persistent step kernel
   int gemm_shape = 0;  // projection launch shape for 4 or 8 row groups (0 default)
+  int shared_prefix = 1;  // read shared prefixes once per group (decode passes)
   int step_wgs = -1;   // workgroups of a persistent launch on this device (0: not runnable; -1: not queried)
   uint64_t* step_trace = nullptr;  // measurement: timestamp buffer of the persistent kernel
   size_t step_trace_cap = 0;       // its capacity in uint64

@@ -1,22 +1,171 @@
 // Paged-attention decode over the block-table KV cache, split-K over context:
 // one workgroup per (split, KV head, row); the work item itself is
 // attn_unit (attn_core.hpp).
+//
+// Shared prefixes.  When several sequences of a decode pass hold the same
+// leading blocks (a common prompt prefix stored once in the paged cache),
+// k_attn_prefix reads each such block once per work item for up to 128
+// (row, query head) pairs of the group instead of once per sequence: the
+// 16 columns of each wave's MFMA tiles are 16 such pairs, and the eight waves
+// of a workgroup walk the same blocks.  Each work item leaves, per pair, the
+// (max, sum, unnormalised output) of its run of prefix blocks as one split
+// partial; the decode kernel then reads only the blocks after the prefix, its
+// waves starting their online softmax from the prefix partials.  Softmax over the
+// union of key sets is exactly the merge of the per-set partials, so this
+// only changes the summation order.
 #include "attn_core.hpp"
 
 namespace vsk {
 
+constexpr int kAttnNB = 2;                // K/V blocks in flight per wave (decode work items)
+constexpr int kPfxWaves = kPfxCols / 16;  // waves of a shared-prefix work item (16 columns each)
+
 template <int D, int NB>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
-  __shared__ AttnLds<D> sm;
-  attn_unit<D, NB, false>(a, blockIdx.z, blockIdx.y, blockIdx.x, sm);
+  __shared__ AttnLds<D, kAttnWaves> sm;
+  attn_unit<D, NB, false, kAttnWaves>(a, blockIdx.z, blockIdx.y, blockIdx.x, sm);
 }
 
 hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s) {
   dim3 grid(a.max_splits, a.Hkv, n_rows);
   if (a.hd == 128) {
-    hipLaunchKernelGGL((k_attn_decode<128, 4>), grid, dim3(64 * kAttnWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_decode<128, kAttnNB>), grid, dim3(64 * kAttnWaves), 0, s, a);
   } else if (a.hd == 64) {
-    hipLaunchKernelGGL((k_attn_decode<64, 4>), grid, dim3(64 * kAttnWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_decode<64, kAttnNB>), grid, dim3(64 * kAttnWaves), 0, s, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int D, int NB>
+__global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a) {
+  constexpr int KC = D / 32;  // K chunks (1 KiB) per block
+  constexpr int VC = D / 16;  // V chunks (512 B) per block
+  __shared__ int32_t tbl[kMaxPfxBps];
+
+  const int hk = blockIdx.y;
+  const int32_t* it = a.items + static_cast<size_t>(blockIdx.x) * 5;
+  const int grp = it[0], col0 = it[1], b_lo = it[2], b_hi = it[3], split = it[4];
+  const int roff = a.grp_info[4 * grp], n_cols = a.grp_info[4 * grp + 1] * a.G;
+  const int32_t* ptbl = a.pfx_tbl + a.grp_info[4 * grp + 3];
+  const int G = a.G;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int h = lane & 15, quad = lane >> 4;
+  for (int i = tid; i < b_hi - b_lo; i += blockDim.x) tbl[i] = ptbl[b_lo + i];
+
+  // this lane's column: pair (group row c / G, query head c % G)
+  const int c = col0 + 16 * w + h;
+  const bool cvalid = c < n_cols;
+  const int row = cvalid ? a.grp_rows[roff + c / G] : 0;
+  const int qh = cvalid ? c % G : 0;
+  u32x4 qf[KC];
+  {
+    const uint16_t* qrow = a.q + static_cast<size_t>(row) * a.Nq + static_cast<size_t>(hk * G + qh) * D;
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+      qf[k] = cvalid ? *reinterpret_cast<const u32x4*>(qrow + 32 * k + 8 * quad) : u32x4{0u, 0u, 0u, 0u};
+  }
+  const float sc = a.scale_log2;
+  float m = -INFINITY, l = 0.f;
+  f32x4 o[VC];
+#pragma unroll
+  for (int k = 0; k < VC; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const size_t kv_stride = static_cast<size_t>(a.Hkv) * kBlock * D;
+  const uint16_t* kbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 0) * a.n_blocks * kv_stride +
+                          static_cast<size_t>(hk) * kBlock * D;
+  const uint16_t* vbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks * kv_stride +
+                          static_cast<size_t>(hk) * kBlock * D;
+
+  // one 16-token block, every token inside the prefix: S = K q, online
+  // softmax, O^T += V^T P^T (P as bf16 high + low parts)
+  auto process = [&](const u32x4 (&kf)[KC], const u32x2 (&vf)[VC]) {
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < KC; ++k) s = mfma_16x16x32(kf[k], qf[k], s);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      s[r] *= sc;
+      mx = fmaxf(mx, s[r]);
+    }
+    mx = fmaxf(mx, shfl_xor(mx, 16));
+    mx = fmaxf(mx, shfl_xor(mx, 32));
+    const float m_new = fmaxf(m, mx);
+    const float alpha = exp2f(m - m_new);
+    float p[4], ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      p[r] = exp2f(s[r] - m_new);
+      ps += p[r];
+    }
+    ps += shfl_xor(ps, 16);
+    ps += shfl_xor(ps, 32);
+    l = l * alpha + ps;
+    m = m_new;
+    u32x2 pf, pl;
+    pf[0] = pack_bf2(p[0], p[1]);
+    pf[1] = pack_bf2(p[2], p[3]);
+    pl[0] = pack_bf2(p[0] - bf2f(pf[0] & 0xffffu), p[1] - bf2f(pf[0] >> 16));
+    pl[1] = pack_bf2(p[2] - bf2f(pf[1] & 0xffffu), p[3] - bf2f(pf[1] >> 16));
+#pragma unroll
+    for (int k = 0; k < VC; ++k) {
+      o[k] *= alpha;
+      o[k] = mfma_16x16x16(vf[k], pf, o[k]);
+      o[k] = mfma_16x16x16(vf[k], pl, o[k]);
+    }
+  };
+  auto load = [&](u32x4 (&kf)[KC], u32x2 (&vf)[VC], int32_t tb) {
+    const size_t blk = static_cast<size_t>(tb);
+    const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
+    const u32x2* vp = reinterpret_cast<const u32x2*>(vbase + blk * kv_stride) + lane;
+#pragma unroll
+    for (int k = 0; k < KC; ++k) kf[k] = kp[k * 64];
+#pragma unroll
+    for (int k = 0; k < VC; ++k) vf[k] = vp[k * 64];
+  };
+
+  __syncthreads();  // tbl
+  if (col0 + 16 * w >= n_cols) return;  // no column of this wave is in the group
+  // every wave walks all blocks of the item, NB blocks of loads ahead;
+  // loads past the end re-read the last block and the final round is peeled
+  const int cnt = b_hi - b_lo;
+  u32x4 kf[NB][KC];
+  u32x2 vf[NB][VC];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) load(kf[i], vf[i], tbl[min(i, cnt - 1)]);
+  int base = 0;
+  for (; base + NB < cnt; base += NB) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      process(kf[i], vf[i]);
+      load(kf[i], vf[i], tbl[min(base + i + NB, cnt - 1)]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+    if (base + i < cnt) process(kf[i], vf[i]);
+
+  // this item's partial of each valid column, as split `split` of its row;
+  // the decode kernel, launched after this one, reads them
+  if (cvalid) {
+    const size_t rh = static_cast<size_t>(row) * a.Hkv + hk;
+    float* po = a.part_o + ((rh * a.split_stride + split) * G + qh) * D;
+#pragma unroll
+    for (int k = 0; k < VC; ++k)
+      *reinterpret_cast<float4*>(po + 16 * k + 4 * quad) = make_float4(o[k][0], o[k][1], o[k][2], o[k][3]);
+    if (quad == 0) a.part_ml[(rh * a.split_stride + split) * G + qh] = make_float2(m, l);
+  }
+}
+
+hipError_t launch_attn_prefix(const AttnPrefixArgs& a, int n_items, int head_dim, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  dim3 grid(n_items, a.Hkv);
+  if (head_dim == 128) {
+    hipLaunchKernelGGL((k_attn_prefix<128, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
+  } else if (head_dim == 64) {
+    hipLaunchKernelGGL((k_attn_prefix<64, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }

@@ -617,6 +617,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
       aa.scale_log2 = a.scale_log2;
       aa.bps = a.bps;
       aa.max_splits = a.max_splits;
+      aa.split_stride = a.max_splits;
       aa.part_o = a.part_o;
       aa.part_ml = a.part_ml;
       aa.counter = a.att_cnt;
@@ -628,8 +629,8 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
       for (int v = blockIdx.x; v < n_items; v += gridDim.x) {
         const int rem = v % (a.Hkv * R);
         __syncthreads();
-        attn_unit<D, kAttnBlocksInFlight, true>(aa, rem / a.Hkv, rem % a.Hkv, v / (a.Hkv * R),
-                                                *reinterpret_cast<AttnLds<D>*>(lds));
+        attn_unit<D, kAttnBlocksInFlight, true, kWaves>(aa, rem / a.Hkv, rem % a.Hkv, v / (a.Hkv * R),
+                                                        *reinterpret_cast<AttnLds<D, kWaves>*>(lds));
       }
     }
     // ---- O projection + residual
@@ -685,7 +686,7 @@ bool step_shape_ok(const vsk_model_cfg& c) {
 
 size_t step_lds_bytes(const vsk_model_cfg& c) {
   const size_t gemm = static_cast<size_t>(c.hidden / 256) * kWaves * 1024 + kLdsRed + kStepMaxRows * 8;
-  const size_t attn = c.head_dim == 128 ? sizeof(AttnLds<128>) : sizeof(AttnLds<64>);
+  const size_t attn = c.head_dim == 128 ? sizeof(AttnLds<128, kWaves>) : sizeof(AttnLds<64, kWaves>);
   return std::max<size_t>(std::max(gemm, attn), 256);
 }
 

