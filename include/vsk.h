@@ -238,7 +238,12 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        2 two tiles everywhere; 3 a 2 x 2 grid of waves over four tiles.
  * key 4: shared prefixes of a decode pass (vsk_batch_prefix_info): 1 (the
  *        default) reads each group's prefix blocks once for the group, 0 reads
- *        them once per sequence. */
+ *        them once per sequence.
+ * key 5: residual projections (O, down) of passes of at most 128 rows: the
+ *        workgroup count their K split aims for (1..4096), or 0 / -1 (the
+ *        default) for no split.  Split products are added to the residual in
+ *        split order by the RMSNorm that follows (measured: no faster than
+ *        one workgroup per output tile, which is why it is off). */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

@@ -73,6 +73,8 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   // x^2 partials: at most one per 16 columns of the hidden size, per row
   w.ssq = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
   w.ssq_c = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
+  // residual projections with K split over workgroups: one product per split
+  w.ypart = o; o = align_up(o + static_cast<size_t>(kMaxResidSplits) * std::min(max_rows, 128) * H * 4);
   // lm_head argmax partials: n_groups x rows
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
@@ -530,6 +532,11 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       if (value < 0 || value > 1) return fail(h, VSK_E_ARG, "shared-prefix switch must be 0 or 1");
       h->shared_prefix = value;
       return VSK_OK;
+    case 5:
+      if (value < -1 || value > 4096)
+        return fail(h, VSK_E_ARG, "residual split target must be -1 (no split), 0 (default) or 1..4096");
+      h->resid_target = value;
+      return VSK_OK;
     default:
       return fail(h, VSK_E_ARG, "unknown tuning key");
   }
@@ -772,20 +779,44 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ap.part_o = aa.part_o;
   ap.part_ml = aa.part_ml;
 
+  const int rt = h.resid_target < 0 ? 0 : h.resid_target > 0 ? h.resid_target : kResidTargetWgs;
   const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape);
-  const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape);
+  const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape, rt);
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape);
-  const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape);
+  const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape, rt);
+  float* ypart = reinterpret_cast<float*>(ws + wl.ypart);
 
   // RMSNorm: one pass over x using the x^2 partials of the step that wrote it
   auto norm = [&](const uint16_t* gain, const float* xin, int rows, int rg, const double* sq, int parts) {
     return launch_rmsnorm_frags(xin, gain, sq, parts, rows, H, c.rms_eps, fb, rg, s);
   };
+  // a residual projection: in place (x += y, with x^2 partials), or with K
+  // split over workgroups and the splits added by k_resid_norm, which also
+  // normalises the rows with `next_gain` (null: no norm follows here)
+  bool normed = false;  // fb already holds the normalised input of the next projection
+  auto resid = [&](int cls, const GemmPlan& p, const uint16_t* next_gain) -> hipError_t {
+    hipError_t re;
+    if (p.ksplit > 1) {
+      ga.ypart = ypart;
+      ga.ssq_out = nullptr;
+      if ((re = probed(cls, [&] { return launch_gemm(ga, p, EPI_RESID, s); })) != hipSuccess) return re;
+      ga.ypart = nullptr;
+      if ((re = launch_resid_norm(x, ypart, p.ksplit, R, H, next_gain, c.rms_eps, fb, Rg, s)) != hipSuccess) return re;
+      normed = next_gain != nullptr;
+    } else {
+      ga.ypart = nullptr;
+      ga.ssq_out = ssq;
+      if ((re = probed(cls, [&] { return launch_gemm(ga, p, EPI_RESID, s); })) != hipSuccess) return re;
+      ssq_parts = p.n_groups;
+      normed = false;
+    }
+    return hipSuccess;
+  };
   ga.X = reinterpret_cast<const u4*>(fb);
   for (int l = 0; l < n_run; ++l) {
     const uint8_t* L = P + h.pl.layer_bytes * l;
     // attention block
-    TRY(norm(norm_gain(l, false), x, R, Rg, ssq, ssq_parts));
+    if (!normed) TRY(norm(norm_gain(l, false), x, R, Rg, ssq, ssq_parts));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wqkv);
     ga.X = reinterpret_cast<const u4*>(fb);
     ga.Kt = H / 32;
@@ -800,16 +831,14 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
       TRY(launch_attn_prefix(ap, b.n_pfx_items, d, s));
     }
     TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
-    // O projection: x += o Wo^T, with the x^2 partials of the updated rows
+    // O projection: x += o Wo^T, then the MLP's RMSNorm
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);
     ga.X = reinterpret_cast<const u4*>(fa);
     ga.Kt = Nq / 32;
     ga.N = H;
-    ga.ssq_out = ssq;
-    TRY(probed(3, [&] { return launch_gemm(ga, p_o, EPI_RESID, s); }));
-    ssq_parts = p_o.n_groups;
+    TRY(resid(3, p_o, norm_gain(l, true)));
     // MLP block
-    TRY(norm(norm_gain(l, true), x, R, Rg, ssq, ssq_parts));
+    if (!normed) TRY(norm(norm_gain(l, true), x, R, Rg, ssq, ssq_parts));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wgu);
     ga.X = reinterpret_cast<const u4*>(fb);
     ga.Kt = H / 32;
@@ -817,13 +846,15 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     ga.ssq_out = nullptr;
     ga.out = fc;
     TRY(probed(0, [&] { return launch_gemm(ga, p_gu, EPI_SWIGLU, s); }));
+    // down projection: x += a Wd^T, then the next layer's RMSNorm (or the
+    // final one of a decode pass, whose rows all return logits)
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wd);
     ga.X = reinterpret_cast<const u4*>(fc);
     ga.Kt = F / 32;
     ga.N = H;
-    ga.ssq_out = ssq;
-    TRY(probed(1, [&] { return launch_gemm(ga, p_d, EPI_RESID, s); }));
-    ssq_parts = p_d.n_groups;
+    const uint16_t* next_gain =
+        l + 1 < n_run ? norm_gain(l + 1, false) : (pa.logit_rows == nullptr ? final_gain : nullptr);
+    TRY(resid(1, p_d, next_gain));
   }
   // final norm over the logit rows, lm_head, greedy argmax
   const int Ro = pa.n_logit_rows;
@@ -833,7 +864,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     double* ssq_c = reinterpret_cast<double*>(ws + wl.ssq_c);
     TRY(launch_gather_rows(x, R, pa.logit_rows, Ro, H, x_c, ssq_c, s));
     TRY(norm(final_gain, x_c, Ro, Rgo, ssq_c, 1));
-  } else {
+  } else if (!normed) {
     TRY(norm(final_gain, x, Ro, Rgo, ssq, ssq_parts));
   }
   const GemmPlan p_lm = plan_gemm(c.vocab, H, Ro, EPI_LOGITS, h.gemm_shape);

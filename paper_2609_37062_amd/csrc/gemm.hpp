@@ -25,6 +25,7 @@ struct GemmArgs {
   const float2* rope;  // [max_pos][hd/2] (cos, sin)
   float* am_val;       // LOGITS: [n_groups][R]
   int* am_idx;
+  float* ypart;  // RESID with K split over workgroups: y[split][R][N] instead of x += y
 };
 
 struct GemmPlan {
@@ -33,10 +34,15 @@ struct GemmPlan {
   int n_groups = 1;  // workgroups along N (also the number of x^2 partials a RESID emits)
   int nt = 1;        // N tiles per wave
   int wn = 1;        // waves side by side along N
+  int ksplit = 1;    // RESID: workgroups along K, their products added by k_resid_norm
 };
 
+constexpr int kMaxResidSplits = 8;
+constexpr int kResidTargetWgs = 0;  // default split-K target of the residual projections (0: no split)
+
 // shape: launch shape for 4 or 8 row groups (0 default; see k_gemm.hip)
-GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0);
+// resid_target: workgroups a residual projection's K split aims for (0: no split)
+GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0, int resid_target = 0);
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s);
 
 }  // namespace vsk

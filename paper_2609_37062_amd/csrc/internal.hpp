@@ -92,6 +92,7 @@ struct BatchDev {
 struct WsLayout {
   int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
   size_t x, x_c, fa, fb, fc, q, att_o, att_ml, att_cnt, ssq, ssq_c, am_part, total;
+  size_t ypart = 0;  // products of residual projections with K split over workgroups
   // persistent decode step (present when max_rows <= kStepMaxRows and the
   // model shape is covered): per-layer activations, sync flags, error word, epoch
   bool step = false;
@@ -134,6 +135,7 @@ struct Handle {
   int exec_mode = 0;   // 0 automatic, 1 one kernel per operation, 2 persistent step kernel
   int gemm_shape = 0;  // projection launch shape for 4 or 8 row groups (0 default)
   int shared_prefix = 1;  // read shared prefixes once per group (decode passes)
+  int resid_target = 0;   // residual projections: split-K workgroup target (0 default, -1 no split)
   int step_wgs = -1;   // workgroups of a persistent launch on this device (0: not runnable; -1: not queried)
   uint64_t* step_trace = nullptr;  // measurement: timestamp buffer of the persistent kernel
   size_t step_trace_cap = 0;       // its capacity in uint64

@@ -23,6 +23,7 @@
 //   SWIGLU : a = silu(gate) * up -> bf16 frags for the down projection
 //            (the SwiGLU product of Algorithm 1's RUN cohort step)
 //   LOGITS : bf16 logits + per-workgroup (max, lowest index)
+#include <algorithm>
 #include <climits>
 
 #include "dev.hpp"
@@ -42,8 +43,11 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wn = w % WN, wk = w / WN;
-  const int ng = blockIdx.x, mt = blockIdx.z;
+  const int ng = blockIdx.x, ks = blockIdx.y, mt = blockIdx.z;
   const int n_tiles = a.N >> 4;
+  // RESID with K split over workgroups (gridDim.y splits): this workgroup
+  // takes K steps [k_lo, k_hi) and stores its product, unreduced
+  const bool split_out = EPI == EPI_RESID && a.ypart != nullptr;
   const int nt0 = (ng * WN + wn) * NT;
   const int g0 = mt * MG;
   const int rsub = lane & 15;
@@ -59,8 +63,10 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 #pragma unroll
   for (int j = 0; j < NT; ++j) tvalid[j] = (nt0 + j) < n_tiles;
 
-  const int first = wk;
-  const int n_it = first < a.Kt ? (a.Kt - first + WK - 1) / WK : 0;
+  const int kc = (a.Kt + gridDim.y - 1) / gridDim.y;
+  const int k_lo = ks * kc, k_hi = min(a.Kt, k_lo + kc);
+  const int first = k_lo + wk;
+  const int n_it = first < k_hi ? (k_hi - first + WK - 1) / WK : 0;
   // Out-of-range tiles and rows read a valid one (their sums are never
   // stored) and the stream past the last K step re-reads the last one, so
   // every load in the main loop is unconditional: the compiler can then keep
@@ -95,6 +101,7 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   auto epi_loads_a = [&]() {
     if (wk != 0) return;
     if constexpr (EPI == EPI_RESID) {
+      if (split_out) return;
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
         const int n0 = 16 * (nt0 + j) + nq;
@@ -194,6 +201,20 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 
   // ---- epilogues (waves with wk == 0 hold the sums)
   if constexpr (EPI == EPI_RESID) {
+    if (split_out) {
+      if (wk == 0) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int g = 0; g < MG; ++g) {
+            const int row = 16 * (g0 + g) + rsub;
+            if (!tvalid[j] || row >= a.R) continue;
+            const int n0 = 16 * (nt0 + j) + nq;
+            *reinterpret_cast<f32x4*>(a.ypart + (static_cast<size_t>(ks) * a.R + row) * a.N + n0) = acc[j][g];
+          }
+      }
+      return;
+    }
     // x += y; this workgroup's share of sum x^2 per row
     if (wk == 0) {
 #pragma unroll
@@ -348,9 +369,9 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 
 // ---------------------------------------------------------------- launcher
 template <int MG, int NT, int WN, int WK, int PF, int EPI>
-static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, hipStream_t s) {
+static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStream_t s) {
   const int n_groups = (a.N / 16 + NT * WN - 1) / (NT * WN);
-  dim3 grid(n_groups, 1, m_tiles);
+  dim3 grid(n_groups, ksplit, m_tiles);
   const size_t smem = (WK > 1 ? (WK - 1) : 0) * WN * NT * MG * 64 * sizeof(f32x4);
   hipLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI>), grid, dim3(64 * WN * WK), smem, s, a);
   return hipGetLastError();
@@ -364,37 +385,36 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, hipStream_t s) {
 // For 4..8 row groups (shape 0, the default) each workgroup is one column of
 // K-split waves (8; 4 for two tiles of 8 row groups, whose cross-wave sums
 // would not fit 64 KiB of LDS) over one N tile (residual, QKV) or two
-// (gate/up, lm_head):
-// N = hidden then still gives 192-256 workgroups.  Shape 1 takes one N tile
-// everywhere, shape 2 two, shape 3 is a 2 x 2 wave grid over four N tiles
-// (fewer workgroups, each X chunk feeding four tiles).
+// (gate/up, lm_head): N = hidden then still gives 192-256 workgroups.
+// Shape 1 takes one N tile everywhere, shape 2 two, shape 3 is a 2 x 2 wave
+// grid over four N tiles (fewer workgroups, each X chunk feeding four tiles).
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
   switch (p.mg) {
     case 1:
-      if (p.nt == 4) return launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, s);
-      if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, s);
-      return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
-    case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, s);
+      if (p.nt == 4) return launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
+      if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
+      return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s);
+    case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s);
     case 4:
-      if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
-      if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, s);
-      return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, s);
+      if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s);
+      if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
+      return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
     default:
-      if (p.wn == 2) return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, s);
-      if (p.nt == 2) return launch_cfg<8, 2, 1, 4, 2, EPI>(a, p.m_tiles, s);
-      return launch_cfg<8, 1, 1, 8, 4, EPI>(a, p.m_tiles, s);
+      if (p.wn == 2) return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s);
+      if (p.nt == 2) return launch_cfg<8, 2, 1, 4, 2, EPI>(a, p.m_tiles, p.ksplit, s);
+      return launch_cfg<8, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
   }
 }
 
-GemmPlan plan_gemm(int N, int K, int R, int epi, int shape) {
-  (void)K;
+GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   GemmPlan p;
   const int Rg = (R + 15) / 16;
   p.mg = Rg <= 1 ? 1 : Rg <= 2 ? 2 : Rg <= 4 ? 4 : 8;
   p.m_tiles = (Rg + p.mg - 1) / p.mg;
   p.nt = 1;
   p.wn = 1;
+  int wk = 8;
   if (p.mg == 1) {
     if (epi != EPI_RESID) p.nt = epi == EPI_LOGITS ? 4 : 2;
   } else if (p.mg >= 4) {
@@ -402,12 +422,24 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape) {
     if (shape == 3) {
       p.nt = 2;
       p.wn = 2;
+      wk = 2;
     } else {
       p.nt = shape == 1 ? 1 : shape == 2 ? 2 : (wide_n ? 2 : 1);
+      wk = p.mg == 8 && p.nt == 2 ? 4 : 8;
     }
   }
   const int cols_per_group = 16 * p.nt * p.wn;
   p.n_groups = (N / 16 * 16 + cols_per_group - 1) / cols_per_group;
+  // a residual projection of one row tile splits K until the workgroups
+  // reach resid_target, keeping at least 4 K steps per wave; k_resid_norm
+  // then adds the splits' products into the residual
+  if (epi == EPI_RESID && resid_target > 0 && p.m_tiles == 1) {
+    const int Kt = K / 32;
+    int ks = std::min({(resid_target + p.n_groups - 1) / p.n_groups, kMaxResidSplits, std::max(1, Kt / (4 * wk))});
+    ks = std::max(ks, 1);
+    const int kc = (Kt + ks - 1) / ks;  // equal splits
+    p.ksplit = (Kt + kc - 1) / kc;
+  }
   return p;
 }
 

@@ -126,6 +126,80 @@ __global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ 
   *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
 }
 
+// ---------------------------------------------------------------- residual sum + RMSNorm
+// A residual projection whose K was split over workgroups leaves one fp32
+// partial product per split (y[split][row][col]).  One workgroup per row adds
+// them to the residual in split order, x += ((y0 + y1) + y2) + ..., stores
+// x, and (gain non-null) normalises the row into bf16 frags of
+// x * g / sqrt(mean(x^2) + eps) -- the sum of squares in double, added in a
+// fixed order, the product in double and rounded once.
+__global__ __launch_bounds__(256) void k_resid_norm(float* __restrict__ x, const float* __restrict__ y, int splits,
+                                                    int R, int H, const uint16_t* __restrict__ g, float eps,
+                                                    uint16_t* __restrict__ hg, int Rg) {
+  __shared__ double s_ss[4];
+  constexpr int kMaxPieces = 4;  // 8-column pieces per thread: H <= 8192
+  const int r = blockIdx.x;
+  float e[kMaxPieces][8];
+  double ss = 0.0;
+  float* xr = x + static_cast<size_t>(r) * H;
+#pragma unroll
+  for (int k = 0; k < kMaxPieces; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 8;
+    if (c >= H) break;
+    float4 a = *reinterpret_cast<const float4*>(xr + c);
+    float4 b = *reinterpret_cast<const float4*>(xr + c + 4);
+    float4 sa = make_float4(0.f, 0.f, 0.f, 0.f), sb = sa;
+    for (int sp = 0; sp < splits; ++sp) {
+      const float* yr = y + (static_cast<size_t>(sp) * R + r) * H + c;
+      const float4 ya = *reinterpret_cast<const float4*>(yr);
+      const float4 yb = *reinterpret_cast<const float4*>(yr + 4);
+      if (sp == 0) {
+        sa = ya;
+        sb = yb;
+      } else {
+        sa.x += ya.x; sa.y += ya.y; sa.z += ya.z; sa.w += ya.w;
+        sb.x += yb.x; sb.y += yb.y; sb.z += yb.z; sb.w += yb.w;
+      }
+    }
+    a.x += sa.x; a.y += sa.y; a.z += sa.z; a.w += sa.w;
+    b.x += sb.x; b.y += sb.y; b.z += sb.z; b.w += sb.w;
+    *reinterpret_cast<float4*>(xr + c) = a;
+    *reinterpret_cast<float4*>(xr + c + 4) = b;
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      e[k][q] = v[q];
+      ss += static_cast<double>(v[q]) * v[q];
+    }
+  }
+  if (g == nullptr) return;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+  if ((threadIdx.x & 63) == 0) s_ss[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const double tot = (s_ss[0] + s_ss[1]) + (s_ss[2] + s_ss[3]);
+  const double rr = 1.0 / sqrt(tot / static_cast<double>(H) + static_cast<double>(eps));
+#pragma unroll
+  for (int k = 0; k < kMaxPieces; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 8;
+    if (c >= H) break;
+    const u32x4 gv = *reinterpret_cast<const u32x4*>(g + c);
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      o[q] = d2bf(static_cast<double>(e[k][2 * q]) * bf2f(gv[q] & 0xffffu) * rr) |
+             (d2bf(static_cast<double>(e[k][2 * q + 1]) * bf2f(gv[q] >> 16) * rr) << 16);
+    *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
+  }
+}
+
+hipError_t launch_resid_norm(float* x, const float* y, int splits, int R, int H, const uint16_t* g, float eps,
+                             uint16_t* hg, int Rg, hipStream_t s) {
+  if (H % 8 != 0 || H > 8192) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_resid_norm, dim3(R), dim3(256), 0, s, x, y, splits, R, H, g, eps, hg, Rg);
+  return hipGetLastError();
+}
+
 hipError_t launch_rmsnorm_frags(const float* x, const uint16_t* g, const double* ssq, int parts, int R, int H,
                                 float eps, uint16_t* hg, int Rg, hipStream_t s) {
   hipLaunchKernelGGL(k_rmsnorm_frags, dim3((H + 511) / 512, R), dim3(64), 0, s, x, g, ssq, parts, R, H, eps, hg, Rg);

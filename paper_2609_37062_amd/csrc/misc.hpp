@@ -9,6 +9,8 @@ hipError_t launch_embed(const uint16_t* E, const int32_t* ids, int R, int H, int
                         hipStream_t s);
 hipError_t launch_gather_rows(const float* x_in, int R_in, const int32_t* rows, int Ro, int H, float* x_out,
                               double* ssq_out, hipStream_t s);
+hipError_t launch_resid_norm(float* x, const float* y, int splits, int R, int H, const uint16_t* g, float eps,
+                             uint16_t* hg, int Rg, hipStream_t s);
 hipError_t launch_rmsnorm_frags(const float* x, const uint16_t* g, const double* ssq, int parts, int R, int H,
                                 float eps, uint16_t* hg, int Rg, hipStream_t s);
 hipError_t launch_argmax_partials(const float* pv, const int* pi, int n_groups, int R, int32_t* ids,

@@ -76,16 +76,38 @@ def test_mid_attention_splits(bps):
     print(st)
 
 
-@pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3), (100, 0), (100, 1), (100, 2), (100, 3)])
+@pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3),
+                                     (100, 0), (100, 1), (100, 2), (100, 3), (130, 0)])
 def test_mid_projection_shapes(B, shape):
     """Every launch shape of the projections for 3 and 7 row groups (one or
-    two 16-column tiles per wave column, or a 2 x 2 wave grid)."""
+    two 16-column tiles per wave column, or a 2 x 2 wave grid) and a
+    row-tiled pass (130 rows: 8 + 1 row groups)."""
     from paper_2609_37062_amd.runner import DeviceRun
     ctx = np.random.default_rng(100 + B).integers(0, 400, size=B)
     w = decode_workload(MID, ctx, seed=13, name=f"mid-shape-b{B}-s{shape}")
     print(f"[gpu] {w.name}", flush=True)
     d = DeviceRun(w, poison_pool=True)
     d.eng.set_tuning(3, shape)
+    d.step()
+    lg, ids = d.results()
+    d.step()
+    lg2, ids2 = d.results()
+    assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
+    st, *_ = _check(w, lg, ids, list(range(0, B, max(1, B // 12))))
+    print(st)
+
+
+@pytest.mark.parametrize("B,target", [(9, -1), (9, 4096), (40, -1), (40, 4096), (100, 64), (100, 4096)])
+def test_mid_residual_k_splits(B, target):
+    """Residual projections with K split over workgroups (the splits added
+    into the residual, in split order, by the RMSNorm that follows): no split
+    (-1), a few, and the most the rule allows."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    ctx = np.random.default_rng(200 + B).integers(0, 400, size=B)
+    w = decode_workload(MID, ctx, seed=17, name=f"mid-rsplit-b{B}-t{target}")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(5, target)
     d.step()
     lg, ids = d.results()
     d.step()
