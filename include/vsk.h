@@ -234,8 +234,9 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  * key 3: launch shape of the per-operation projections for 33..128 rows
  *        (and longer row-tiled passes): 0 (default) one column of eight
  *        K-split waves per workgroup over one 16-column tile (residual and
- *        QKV projections) or two (gate/up, lm_head); 1 one tile everywhere;
- *        2 two tiles everywhere; 3 a 2 x 2 grid of waves over four tiles.
+ *        QKV projections) or two (gate/up, lm_head), and for passes of more
+ *        than 128 rows shape 3; 1 one tile everywhere; 2 two tiles
+ *        everywhere; 3 a 2 x 2 grid of waves over four tiles.
  * key 4: shared prefixes of a decode pass (vsk_batch_prefix_info): 1 (the
  *        default) reads each group's prefix blocks once for the group, 0 reads
  *        them once per sequence.
@@ -243,7 +244,11 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        workgroup count their K split aims for (1..4096), or 0 / -1 (the
  *        default) for no split.  Split products are added to the residual in
  *        split order by the RMSNorm that follows (measured: no faster than
- *        one workgroup per output tile, which is why it is off). */
+ *        one workgroup per output tile, which is why it is off).
+ * key 6: rows of a sequence with several new rows (a prefill chunk): 1 (the
+ *        default) one causal work item per run of up to 128 (row, query
+ *        head) pairs reading each key block once for all of them; 0 one
+ *        work item per row, as for decode rows. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

@@ -229,6 +229,24 @@ void plan_prefix_items(BatchHost& b, int32_t group_size, int32_t n_kv_heads, int
   }
 }
 
+void plan_prefill_items(BatchHost& b, int32_t group_size) {
+  b.pre_items.clear();
+  b.dec_rows.clear();
+  if (b.max_q_len <= 1) return;
+  const int32_t per = std::max(1, kPfxCols / group_size);
+  for (int32_t i = 0; i < b.n_seqs; ++i) {
+    const int32_t r0 = b.cu_q[i], r1 = b.cu_q[i + 1];
+    if (r1 - r0 == 1) {
+      b.dec_rows.push_back(r0);
+      continue;
+    }
+    for (int32_t r = r0; r < r1; r += per) {
+      const int32_t it[3] = {i, r, std::min(per, r1 - r)};
+      b.pre_items.insert(b.pre_items.end(), it, it + 3);
+    }
+  }
+}
+
 void find_shared_prefixes(BatchHost& b, int32_t block, int32_t min_blocks) {
   b.pfx_blocks.assign(b.n_rows, 0);
   b.grp_rows.clear();

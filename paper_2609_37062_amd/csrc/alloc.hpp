@@ -79,7 +79,18 @@ struct BatchHost {
   std::vector<int32_t> pfx_items;    // [n_items][5]: group, first column, first block, end block, split
   int32_t max_pfx_splits = 0;
   int32_t n_pfx_items() const { return static_cast<int32_t>(pfx_items.size() / 5); }
+  // Attention work of a pass with prefill rows (plan_prefill_items)
+  std::vector<int32_t> pre_items;    // [n][3]: sequence, first row, rows -- runs of a sequence's new rows
+  std::vector<int32_t> dec_rows;     // rows of one-row sequences
+  int32_t n_pre_items() const { return static_cast<int32_t>(pre_items.size() / 3); }
 };
+
+// A pass with prefill rows (a sequence with more than one new row): each
+// such sequence's rows are cut into runs of at most kPfxCols / group_size
+// rows (one causal-attention work item each); the rows of one-row sequences
+// are listed for the decode attention.  A pass of one-row sequences only
+// gets no items.
+void plan_prefill_items(BatchHost& b, int32_t group_size);
 
 // Columns (row, query head) of one shared-prefix work item: 8 waves x 16.
 constexpr int32_t kPfxCols = 128;

@@ -339,6 +339,7 @@ int vsk_batch_build(vsk_handle* h, const int64_t* seqs_host, const int32_t* q_le
   int st = build_batch(h->alloc, seqs_host, q_lens_host, n_seqs, b, h->err);
   if (st != VSK_OK) return st;
   plan_prefix_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads, h->cfg.n_kv_heads);
+  plan_prefill_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads);
   h->bh = std::move(b);
   h->batch_built = true;
   h->batch_uploaded = false;
@@ -379,7 +380,8 @@ int vsk_batch_prefix_info(const vsk_handle* h, int32_t* pfx_blocks_host, int32_t
 static size_t meta_bytes(const BatchHost& b) {
   auto sz = [](const std::vector<int32_t>& v) { return align_up(std::max<size_t>(v.size(), 1) * 4); };
   return sz(b.block_table) + sz(b.kv_len) + sz(b.cu_q) + sz(b.row_seq) + sz(b.pos) + sz(b.slot) +
-         sz(b.pfx_blocks) + sz(b.pfx_splits) + sz(b.pfx_items) + sz(b.grp_rows) + sz(b.grp_info) + sz(b.pfx_tbl);
+         sz(b.pfx_blocks) + sz(b.pfx_splits) + sz(b.pfx_items) + sz(b.grp_rows) + sz(b.grp_info) + sz(b.pfx_tbl) +
+         sz(b.pre_items) + sz(b.dec_rows);
 }
 
 size_t vsk_batch_device_bytes(const vsk_handle* h) {
@@ -414,6 +416,10 @@ int vsk_batch_upload(vsk_handle* h, void* meta_dev, size_t bytes, void* stream) 
   put(b.grp_rows, &d.grp_rows);
   put(b.grp_info, &d.grp_info);
   put(b.pfx_tbl, &d.pfx_tbl);
+  put(b.pre_items, &d.pre_items);
+  put(b.dec_rows, &d.dec_rows);
+  d.n_pre_items = b.n_pre_items();
+  d.n_dec_rows = static_cast<int32_t>(b.dec_rows.size());
   d.n_pfx_items = b.n_pfx_items();
   d.max_pfx_splits = b.max_pfx_splits;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -531,6 +537,10 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
     case 4:
       if (value < 0 || value > 1) return fail(h, VSK_E_ARG, "shared-prefix switch must be 0 or 1");
       h->shared_prefix = value;
+      return VSK_OK;
+    case 6:
+      if (value < 0 || value > 1) return fail(h, VSK_E_ARG, "prefill attention switch must be 0 or 1");
+      h->prefill_attn = value;
       return VSK_OK;
     case 5:
       if (value < -1 || value > 4096)
@@ -778,6 +788,23 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ap.split_stride = aa.split_stride;
   ap.part_o = aa.part_o;
   ap.part_ml = aa.part_ml;
+  // prefill rows: causal multi-row work items (keys staged per item in LDS)
+  const bool prefill = h.prefill_attn != 0 && b.n_pre_items > 0 && b.max_kv_len <= kMaxPrefillBlocks * kBlock;
+  AttnPrefillArgs pf{};
+  pf.q = q;
+  pf.pool = h.pool;
+  pf.n_blocks = h.n_blocks;
+  pf.Hkv = c.n_kv_heads;
+  pf.G = aa.G;
+  pf.Nq = Nq;
+  pf.block_table = b.block_table;
+  pf.max_blocks = b.max_blocks;
+  pf.kv_len = b.kv_len;
+  pf.pos = b.pos;
+  pf.items = b.pre_items;
+  pf.scale_log2 = aa.scale_log2;
+  pf.out = fa;
+  pf.out_Rg = Rg;
 
   const int rt = h.resid_target < 0 ? 0 : h.resid_target > 0 ? h.resid_target : kResidTargetWgs;
   const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape);
@@ -830,7 +857,15 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
       ap.layer = l;
       TRY(launch_attn_prefix(ap, b.n_pfx_items, d, s));
     }
-    TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
+    if (prefill) {
+      pf.layer = l;
+      TRY(launch_attn_prefill(pf, b.n_pre_items, d, s));
+      aa.rows = b.dec_rows;
+      if (b.n_dec_rows > 0) TRY(probed(4, [&] { return launch_attn_decode(aa, b.n_dec_rows, s); }));
+    } else {
+      aa.rows = nullptr;
+      TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
+    }
     // O projection: x += o Wo^T, then the MLP's RMSNorm
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);
     ga.X = reinterpret_cast<const u4*>(fa);

@@ -27,6 +27,23 @@ struct AttnArgs {
   // 0..pfx_splits[row]-1 and its first split starts from them
   const int32_t* pfx_blocks;  // [R]
   const int32_t* pfx_splits;  // [R]
+  const int32_t* rows;        // nullable: the rows of the launch (grid z indexes it), else all rows
+};
+
+// Causal attention of prefill rows (see k_attn_prefill).
+constexpr int kMaxPrefillBlocks = 512;  // key blocks a prefill work item can stage (8192 positions)
+struct AttnPrefillArgs {
+  const uint16_t* q;  // [R][Nq] bf16
+  const uint16_t* pool;
+  int layer, n_blocks, Hkv, G, Nq;
+  const int32_t* block_table;  // [n_seqs][max_blocks]
+  int max_blocks;
+  const int32_t* kv_len;       // [n_seqs]
+  const int32_t* pos;          // [R]
+  const int32_t* items;        // [n_items][3]: sequence, first row, rows
+  float scale_log2;
+  uint16_t* out;  // o frags (K = Nq)
+  int out_Rg;
 };
 
 // Shared-prefix attention: each work item reads a run of a group's prefix
@@ -50,5 +67,6 @@ struct AttnPrefixArgs {
 
 hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s);
 hipError_t launch_attn_prefix(const AttnPrefixArgs& a, int n_items, int head_dim, hipStream_t s);
+hipError_t launch_attn_prefill(const AttnPrefillArgs& a, int n_items, int head_dim, hipStream_t s);
 
 }  // namespace vsk

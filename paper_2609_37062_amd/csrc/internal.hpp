@@ -86,6 +86,10 @@ struct BatchDev {
   const int32_t* grp_info = nullptr;
   const int32_t* pfx_tbl = nullptr;
   int32_t n_pfx_items = 0, max_pfx_splits = 0;
+  // prefill rows: causal work items, and the rows left to the decode kernel
+  const int32_t* pre_items = nullptr;
+  const int32_t* dec_rows = nullptr;
+  int32_t n_pre_items = 0, n_dec_rows = 0;
 };
 
 // ---------------------------------------------------------------- workspace
@@ -136,6 +140,7 @@ struct Handle {
   int gemm_shape = 0;  // projection launch shape for 4 or 8 row groups (0 default)
   int shared_prefix = 1;  // read shared prefixes once per group (decode passes)
   int resid_target = 0;   // residual projections: split-K workgroup target (0 default, -1 no split)
+  int prefill_attn = 1;   // prefill rows through the causal multi-row kernel (0: one row per work item)
   int step_wgs = -1;   // workgroups of a persistent launch on this device (0: not runnable; -1: not queried)
   uint64_t* step_trace = nullptr;  // measurement: timestamp buffer of the persistent kernel
   size_t step_trace_cap = 0;       // its capacity in uint64

@@ -23,7 +23,8 @@ constexpr int kPfxWaves = kPfxCols / 16;  // waves of a shared-prefix work item 
 template <int D, int NB>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   __shared__ AttnLds<D, kAttnWaves> sm;
-  attn_unit<D, NB, false, kAttnWaves>(a, blockIdx.z, blockIdx.y, blockIdx.x, sm);
+  attn_unit<D, NB, false, kAttnWaves>(a, a.rows != nullptr ? a.rows[blockIdx.z] : static_cast<int>(blockIdx.z),
+                                      blockIdx.y, blockIdx.x, sm);
 }
 
 hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s) {
@@ -38,66 +39,52 @@ hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int D, int NB>
-__global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a) {
+// Walk of one wave over a run of 16-token blocks for 16 query columns (each
+// lane's column h = lane % 16): S = K q on the matrix cores, online softmax
+// in base 2, O^T += V^T P^T with P split into bf16 high and low parts.  The
+// block ids are tbl[0..cnt) (in LDS), block tbl[i] holding key positions
+// 16 (b0 + i) ..; with MASK, key t counts for this lane's column only when
+// t <= lim, and V rows at positions >= kv_end are zeroed (stale slots of the
+// last block may hold NaN patterns).  NB blocks of loads stay in flight.
+template <int D, int NB, bool MASK>
+__device__ __forceinline__ void mq_walk(const u32x4 (&qf)[D / 32], const uint16_t* kbase, const uint16_t* vbase,
+                                        size_t kv_stride, const int32_t* tbl, int cnt, int b0, int lim, int kv_end,
+                                        float sc, float& m, float& l, f32x4 (&o)[D / 16]) {
   constexpr int KC = D / 32;  // K chunks (1 KiB) per block
   constexpr int VC = D / 16;  // V chunks (512 B) per block
-  __shared__ int32_t tbl[kMaxPfxBps];
-
-  const int hk = blockIdx.y;
-  const int32_t* it = a.items + static_cast<size_t>(blockIdx.x) * 5;
-  const int grp = it[0], col0 = it[1], b_lo = it[2], b_hi = it[3], split = it[4];
-  const int roff = a.grp_info[4 * grp], n_cols = a.grp_info[4 * grp + 1] * a.G;
-  const int32_t* ptbl = a.pfx_tbl + a.grp_info[4 * grp + 3];
-  const int G = a.G;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6;
-  const int h = lane & 15, quad = lane >> 4;
-  for (int i = tid; i < b_hi - b_lo; i += blockDim.x) tbl[i] = ptbl[b_lo + i];
-
-  // this lane's column: pair (group row c / G, query head c % G)
-  const int c = col0 + 16 * w + h;
-  const bool cvalid = c < n_cols;
-  const int row = cvalid ? a.grp_rows[roff + c / G] : 0;
-  const int qh = cvalid ? c % G : 0;
-  u32x4 qf[KC];
-  {
-    const uint16_t* qrow = a.q + static_cast<size_t>(row) * a.Nq + static_cast<size_t>(hk * G + qh) * D;
+  const int lane = threadIdx.x & 63, quad = lane >> 4;
+  auto process = [&](const u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {
+    const int t_lane = 16 * b + 4 * quad;  // first key position of this lane's quarter
+    if constexpr (MASK) {
+      if (t_lane + 3 >= kv_end) {
+        const uint32_t m01 = (t_lane + 0 < kv_end ? 0x0000ffffu : 0u) | (t_lane + 1 < kv_end ? 0xffff0000u : 0u);
+        const uint32_t m23 = (t_lane + 2 < kv_end ? 0x0000ffffu : 0u) | (t_lane + 3 < kv_end ? 0xffff0000u : 0u);
 #pragma unroll
-    for (int k = 0; k < KC; ++k)
-      qf[k] = cvalid ? *reinterpret_cast<const u32x4*>(qrow + 32 * k + 8 * quad) : u32x4{0u, 0u, 0u, 0u};
-  }
-  const float sc = a.scale_log2;
-  float m = -INFINITY, l = 0.f;
-  f32x4 o[VC];
-#pragma unroll
-  for (int k = 0; k < VC; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const size_t kv_stride = static_cast<size_t>(a.Hkv) * kBlock * D;
-  const uint16_t* kbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 0) * a.n_blocks * kv_stride +
-                          static_cast<size_t>(hk) * kBlock * D;
-  const uint16_t* vbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks * kv_stride +
-                          static_cast<size_t>(hk) * kBlock * D;
-
-  // one 16-token block, every token inside the prefix: S = K q, online
-  // softmax, O^T += V^T P^T (P as bf16 high + low parts)
-  auto process = [&](const u32x4 (&kf)[KC], const u32x2 (&vf)[VC]) {
+        for (int k = 0; k < VC; ++k) {
+          vf[k][0] &= m01;
+          vf[k][1] &= m23;
+        }
+      }
+    }
     f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k = 0; k < KC; ++k) s = mfma_16x16x32(kf[k], qf[k], s);
     float mx = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      s[r] *= sc;
+      if constexpr (MASK) s[r] = t_lane + r <= lim ? s[r] * sc : -INFINITY;
+      else s[r] *= sc;
       mx = fmaxf(mx, s[r]);
     }
     mx = fmaxf(mx, shfl_xor(mx, 16));
     mx = fmaxf(mx, shfl_xor(mx, 32));
     const float m_new = fmaxf(m, mx);
-    const float alpha = exp2f(m - m_new);
+    // a column with no valid key yet keeps m = -inf: its factors must be 0, not NaN
+    const float alpha = m_new == -INFINITY ? 1.f : exp2f(m - m_new);
     float p[4], ps = 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      p[r] = exp2f(s[r] - m_new);
+      p[r] = m_new == -INFINITY ? 0.f : exp2f(s[r] - m_new);
       ps += p[r];
     }
     ps += shfl_xor(ps, 16);
@@ -125,12 +112,8 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a
 #pragma unroll
     for (int k = 0; k < VC; ++k) vf[k] = vp[k * 64];
   };
-
-  __syncthreads();  // tbl
-  if (col0 + 16 * w >= n_cols) return;  // no column of this wave is in the group
-  // every wave walks all blocks of the item, NB blocks of loads ahead;
+  if (cnt <= 0) return;
   // loads past the end re-read the last block and the final round is peeled
-  const int cnt = b_hi - b_lo;
   u32x4 kf[NB][KC];
   u32x2 vf[NB][VC];
 #pragma unroll
@@ -139,13 +122,58 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a
   for (; base + NB < cnt; base += NB) {
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      process(kf[i], vf[i]);
+      process(kf[i], vf[i], b0 + base + i);
       load(kf[i], vf[i], tbl[min(base + i + NB, cnt - 1)]);
     }
   }
 #pragma unroll
   for (int i = 0; i < NB; ++i)
-    if (base + i < cnt) process(kf[i], vf[i]);
+    if (base + i < cnt) process(kf[i], vf[i], b0 + base + i);
+}
+
+template <int D, int NB>
+__global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a) {
+  constexpr int KC = D / 32;
+  constexpr int VC = D / 16;
+  __shared__ int32_t tbl[kMaxPfxBps];
+
+  const int hk = blockIdx.y;
+  const int32_t* it = a.items + static_cast<size_t>(blockIdx.x) * 5;
+  const int grp = it[0], col0 = it[1], b_lo = it[2], b_hi = it[3], split = it[4];
+  const int roff = a.grp_info[4 * grp], n_cols = a.grp_info[4 * grp + 1] * a.G;
+  const int32_t* ptbl = a.pfx_tbl + a.grp_info[4 * grp + 3];
+  const int G = a.G;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int h = lane & 15, quad = lane >> 4;
+  for (int i = tid; i < b_hi - b_lo; i += blockDim.x) tbl[i] = ptbl[b_lo + i];
+
+  // this lane's column: pair (group row c / G, query head c % G)
+  const int c = col0 + 16 * w + h;
+  const bool cvalid = c < n_cols;
+  const int row = cvalid ? a.grp_rows[roff + c / G] : 0;
+  const int qh = cvalid ? c % G : 0;
+  u32x4 qf[KC];
+  {
+    const uint16_t* qrow = a.q + static_cast<size_t>(row) * a.Nq + static_cast<size_t>(hk * G + qh) * D;
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+      qf[k] = cvalid ? *reinterpret_cast<const u32x4*>(qrow + 32 * k + 8 * quad) : u32x4{0u, 0u, 0u, 0u};
+  }
+  float m = -INFINITY, l = 0.f;
+  f32x4 o[VC];
+#pragma unroll
+  for (int k = 0; k < VC; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const size_t kv_stride = static_cast<size_t>(a.Hkv) * kBlock * D;
+  const uint16_t* kbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 0) * a.n_blocks * kv_stride +
+                          static_cast<size_t>(hk) * kBlock * D;
+  const uint16_t* vbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks * kv_stride +
+                          static_cast<size_t>(hk) * kBlock * D;
+
+  __syncthreads();  // tbl
+  if (col0 + 16 * w >= n_cols) return;  // no column of this wave is in the group
+  // every wave walks all blocks of the item (all keys lie inside the prefix)
+  mq_walk<D, NB, false>(qf, kbase, vbase, kv_stride, tbl, b_hi - b_lo, b_lo, 0, 0, a.scale_log2, m, l, o);
 
   // this item's partial of each valid column, as split `split` of its row;
   // the decode kernel, launched after this one, reads them
@@ -157,6 +185,90 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a
       *reinterpret_cast<float4*>(po + 16 * k + 4 * quad) = make_float4(o[k][0], o[k][1], o[k][2], o[k][3]);
     if (quad == 0) a.part_ml[(rh * a.split_stride + split) * G + qh] = make_float2(m, l);
   }
+}
+
+// Causal attention of a prefill chunk: one work item per (run of a
+// sequence's consecutive new rows, KV head), its columns the (row, query
+// head) pairs of the run, 16 per wave.  Row r at position p attends keys
+// 0..p of its sequence; its own chunk's keys were written by the QKV
+// projection before this kernel runs (every layer writes its own KV).  A
+// wave walks the blocks up to its last row's position; each lane masks the
+// keys past its own row.  The output is normalised and stored as the O
+// projection's input frags.
+template <int D, int NB>
+__global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefill(AttnPrefillArgs a) {
+  constexpr int KC = D / 32;
+  constexpr int VC = D / 16;
+  __shared__ int32_t tbl[kMaxPrefillBlocks];
+
+  const int hk = blockIdx.y;
+  const int32_t* it = a.items + static_cast<size_t>(blockIdx.x) * 3;
+  const int seq = it[0], row0 = it[1], n_rows = it[2];
+  const int G = a.G;
+  const int n_cols = n_rows * G;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int h = lane & 15, quad = lane >> 4;
+  const int kv_end = a.kv_len[seq];
+  const int p_last = a.pos[row0 + n_rows - 1];
+  const int nb = p_last / kBlock + 1;  // blocks any row of the item reads
+  const int32_t* table = a.block_table + static_cast<size_t>(seq) * a.max_blocks;
+  for (int i = tid; i < nb; i += blockDim.x) tbl[i] = table[i];
+
+  const int c = 16 * w + h;
+  const bool cvalid = c < n_cols;
+  const int row = row0 + (cvalid ? c / G : 0);
+  const int qh = cvalid ? c % G : 0;
+  const int lim = cvalid ? a.pos[row] : -1;
+  u32x4 qf[KC];
+  {
+    const uint16_t* qrow = a.q + static_cast<size_t>(row) * a.Nq + static_cast<size_t>(hk * G + qh) * D;
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+      qf[k] = cvalid ? *reinterpret_cast<const u32x4*>(qrow + 32 * k + 8 * quad) : u32x4{0u, 0u, 0u, 0u};
+  }
+  float m = -INFINITY, l = 0.f;
+  f32x4 o[VC];
+#pragma unroll
+  for (int k = 0; k < VC; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const size_t kv_stride = static_cast<size_t>(a.Hkv) * kBlock * D;
+  const uint16_t* kbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 0) * a.n_blocks * kv_stride +
+                          static_cast<size_t>(hk) * kBlock * D;
+  const uint16_t* vbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks * kv_stride +
+                          static_cast<size_t>(hk) * kBlock * D;
+
+  __syncthreads();  // tbl
+  if (16 * w >= n_cols) return;
+  // this wave's last column decides how far it walks
+  const int c_last = min(16 * w + 15, n_cols - 1);
+  const int w_blocks = a.pos[row0 + c_last / G] / kBlock + 1;
+  mq_walk<D, NB, true>(qf, kbase, vbase, kv_stride, tbl, w_blocks, 0, lim, kv_end, a.scale_log2, m, l, o);
+
+  if (cvalid) {
+    const float inv = 1.f / l;
+    const int col0 = (hk * G + qh) * D;
+#pragma unroll
+    for (int k = 0; k < VC; ++k) {
+      const int e = 16 * k + 4 * quad;
+      u32x2 pk;
+      pk[0] = pack_bf2(o[k][0] * inv, o[k][1] * inv);
+      pk[1] = pack_bf2(o[k][2] * inv, o[k][3] * inv);
+      *reinterpret_cast<u32x2*>(a.out + frag_index(row, col0 + e, a.out_Rg)) = pk;
+    }
+  }
+}
+
+hipError_t launch_attn_prefill(const AttnPrefillArgs& a, int n_items, int head_dim, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  dim3 grid(n_items, a.Hkv);
+  if (head_dim == 128) {
+    hipLaunchKernelGGL((k_attn_prefill<128, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
+  } else if (head_dim == 64) {
+    hipLaunchKernelGGL((k_attn_prefill<64, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_attn_prefix(const AttnPrefixArgs& a, int n_items, int head_dim, hipStream_t s) {

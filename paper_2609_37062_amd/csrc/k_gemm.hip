@@ -385,9 +385,10 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 // For 4..8 row groups (shape 0, the default) each workgroup is one column of
 // K-split waves (8; 4 for two tiles of 8 row groups, whose cross-wave sums
 // would not fit 64 KiB of LDS) over one N tile (residual, QKV) or two
-// (gate/up, lm_head): N = hidden then still gives 192-256 workgroups.
-// Shape 1 takes one N tile everywhere, shape 2 two, shape 3 is a 2 x 2 wave
-// grid over four N tiles (fewer workgroups, each X chunk feeding four tiles).
+// (gate/up, lm_head): N = hidden then still gives 192-256 workgroups; a
+// row-tiled pass takes shape 3.  Shape 1 takes one N tile everywhere, shape 2
+// two, shape 3 is a 2 x 2 wave grid over four N tiles (fewer workgroups, each
+// X chunk feeding four tiles).
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
   switch (p.mg) {
@@ -419,7 +420,10 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
     if (epi != EPI_RESID) p.nt = epi == EPI_LOGITS ? 4 : 2;
   } else if (p.mg >= 4) {
     const bool wide_n = epi == EPI_SWIGLU || epi == EPI_LOGITS;
-    if (shape == 3) {
+    // a row-tiled pass (more than 128 rows) re-streams the weights once per
+    // row tile: there the 2 x 2 wave grid, each X chunk feeding four N
+    // tiles, is the faster default
+    if (shape == 3 || (shape == 0 && p.m_tiles > 1)) {
       p.nt = 2;
       p.wn = 2;
       wk = 2;

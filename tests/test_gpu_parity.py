@@ -10,7 +10,8 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
-from workloads.configs import ModelCfg, decode_workload, mixed_workload, prefix_groups_workload, workload  # noqa: E402
+from workloads.configs import (ModelCfg, SeqSpec, Workload, decode_workload, mixed_workload,  # noqa: E402
+                               prefix_groups_workload, workload)
 
 from helpers import compare_logits, oracle_run  # noqa: E402
 
@@ -156,6 +157,40 @@ def test_mid_mixed_prefill_decode():
     d, lg, ids = _run(w)
     st, out, kv, sub, idx = _check(w, lg, ids)
     # every prefill row wrote its own K,V at every layer
+    for l in range(MID.n_layers):
+        K, V = d.read_kv(l, sub["slot"])
+        Ko, Vo = kv.read(l, sub["slot"])
+        assert np.abs(K - Ko).max() <= 0.05 and np.abs(V - Vo).max() <= 0.05
+    print(st)
+
+
+@pytest.mark.parametrize("prefill_kernel", [1, 0])
+def test_mid_chunked_prefill_with_context(prefill_kernel):
+    """Prefill chunks that continue cached sequences (rows at positions
+    ctx..ctx+q-1 attend the cache and the chunk's own earlier rows), a fresh
+    prompt, a two-row chunk and decode rows in one pass; the causal
+    multi-row kernel (1) and one work item per row (0)."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    rng = np.random.default_rng(31)
+    specs = [(100, 37), (0, 50), (300, 1), (17, 2), (33, 1), (250, 45)]
+    n_pool = 120
+    perm = [int(b) for b in rng.permutation(n_pool)]
+    seqs, pos = [], 0
+    for i, (ctx, q) in enumerate(specs):
+        nb = (ctx + 15) // 16
+        seqs.append(SeqSpec(ctx, q, perm[pos:pos + nb], [(0, ctx, i)] if ctx else []))
+        pos += nb
+    tokens = rng.integers(0, MID.vocab, size=sum(q for _, q in specs)).astype(np.int32)
+    w = Workload(0, f"mid-chunked-{prefill_kernel}", MID, seqs, n_pool, tokens, 5)
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(6, prefill_kernel)
+    d.step()
+    lg, ids = d.results()
+    d.step()
+    lg2, ids2 = d.results()
+    assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
+    st, out, kv, sub, idx = _check(w, lg, ids)
     for l in range(MID.n_layers):
         K, V = d.read_kv(l, sub["slot"])
         Ko, Vo = kv.read(l, sub["slot"])
