@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--mode", type=int, default=0,
                     help="execution path: 0 automatic, 1 one kernel per operation, 2 persistent step kernel")
+    ap.add_argument("--tune", action="append", default=[], metavar="KEY=VALUE",
+                    help="launch-shape tuning passed to vsk_set_tuning before timing (repeatable)")
     ap.add_argument("--trace", action="store_true",
                     help="print the persistent kernel's per-phase timeline (stderr) after the timed steps")
     ap.add_argument("--profile-pass", action="store_true",
@@ -173,11 +175,18 @@ def step_timeline(torch, d, reps=3):
     return out
 
 
-def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False):
+def apply_tuning(d, mode, tune):
+    d.eng.set_tuning(2, mode)
+    for kv in tune:
+        k, v = kv.split("=")
+        d.eng.set_tuning(int(k), int(v))
+
+
+def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False, tune=()):
     from paper_2609_37062_amd.runner import DeviceRun
     print(f"[bench] setting up {w.name}", file=sys.stderr, flush=True)
     d = DeviceRun(w)
-    d.eng.set_tuning(2, mode)
+    apply_tuning(d, mode, tune)
     stream = torch.cuda.current_stream()
     res = {}
     ms_eager, wall_eager = time_steps(torch, d.step, steps, warmup, stream)
@@ -295,7 +304,7 @@ def main():
     if a.profile_pass:
         from paper_2609_37062_amd.runner import DeviceRun
         d = DeviceRun(w)
-        d.eng.set_tuning(2, a.mode)
+        apply_tuning(d, a.mode, a.tune)
         src = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         src.fill_(1)
@@ -308,7 +317,7 @@ def main():
         print(f"[bench] profile pass: {w.name}, {a.steps} steps, calibration copy {CALIB_BYTES} bytes",
               file=sys.stderr)
         return
-    r = measure(torch, w, a.steps, a.warmup, not a.no_graph, mode=a.mode, trace=a.trace)
+    r = measure(torch, w, a.steps, a.warmup, not a.no_graph, mode=a.mode, trace=a.trace, tune=a.tune)
     ms = min(r["ms_eager"], r.get("ms_graph", float("inf")))
     tokps = w.n_rows / (ms / 1e3)
     sb = step_bytes(w)
@@ -353,7 +362,8 @@ def main():
         out["timeline"] = r["timeline"]
     if not a.no_batch64 and a.workload == 2:
         w3 = workload(3)
-        r3 = measure(torch, w3, a.steps, a.warmup, not a.no_graph, probe=False, mode=a.mode if a.mode != 2 else 0)
+        r3 = measure(torch, w3, a.steps, a.warmup, not a.no_graph, probe=False, mode=a.mode if a.mode != 2 else 0,
+                     tune=a.tune)
         ms3 = min(r3["ms_eager"], r3.get("ms_graph", float("inf")))
         sb3 = step_bytes(w3)
         out["batch64_shared_prefix"] = {

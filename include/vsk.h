@@ -236,7 +236,10 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        K-split waves per workgroup over one 16-column tile (residual and
  *        QKV projections) or two (gate/up, lm_head), and for passes of more
  *        than 128 rows shape 3; 1 one tile everywhere; 2 two tiles
- *        everywhere; 3 a 2 x 2 grid of waves over four tiles.
+ *        everywhere; 3 a 2 x 2 grid of waves over four tiles; 4 the
+ *        activation chunks staged in LDS by a ninth wave and shared by eight
+ *        weight-streaming waves on four tiles (two for QKV), residual
+ *        projections with K split over workgroups.
  * key 4: shared prefixes of a decode pass (vsk_batch_prefix_info): 1 (the
  *        default) reads each group's prefix blocks once for the group, 0 reads
  *        them once per sequence.

@@ -35,6 +35,7 @@ struct GemmPlan {
   int nt = 1;        // N tiles per wave
   int wn = 1;        // waves side by side along N
   int ksplit = 1;    // RESID: workgroups along K, their products added by k_resid_norm
+  bool xl = false;   // X chunks staged in LDS by a loader wave, shared by the compute waves
 };
 
 constexpr int kMaxResidSplits = 8;

@@ -25,6 +25,7 @@
 //   LOGITS : bf16 logits + per-workgroup (max, lowest index)
 #include <algorithm>
 #include <climits>
+#include <utility>
 
 #include "dev.hpp"
 #include "gemm.hpp"
@@ -33,8 +34,15 @@ namespace vsk {
 
 __device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v)); }
 
-template <int MG, int NT, int WN, int WK, int PF, int EPI>
-__global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds + 16 l (the LDS address must be the same for the whole wave)
+__device__ __forceinline__ void lds_load16(const u32x4* g, u32x4* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL>
+__global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs a) {
+  static_assert(!XL || (NT == 1 && WN * WK == 8 && (WK == 2 || WK == 4)), "X in LDS: 8 compute waves, one N tile each");
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ float s_amv[WN][MG][16];
   __shared__ int s_ami[WN][MG][16];
@@ -42,7 +50,10 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int wn = w % WN, wk = w / WN;
+  // XL: wave WN * WK only loads X into LDS (wk = -1 keeps it out of every
+  // K-split role: it holds no sums and runs no epilogue)
+  const bool loader = XL && w == WN * WK;
+  const int wn = w % WN, wk = loader ? -1 : w / WN;
   const int ng = blockIdx.x, ks = blockIdx.y, mt = blockIdx.z;
   const int n_tiles = a.N >> 4;
   // RESID with K split over workgroups (gridDim.y splits): this workgroup
@@ -143,34 +154,136 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
   };
   if constexpr (kHoist) epi_loads_a();
 
-  if (n_it > 0) {
-#pragma unroll
-    for (int st = 0; st < PF; ++st) load(fa[st], fb[st], st);
-  }
+  if constexpr (!XL) {
+    if (n_it > 0) {
+  #pragma unroll
+      for (int st = 0; st < PF; ++st) load(fa[st], fb[st], st);
+    }
 
-  if constexpr (kHoist) epi_loads_b();
+    if constexpr (kHoist) epi_loads_b();
 
-  auto step = [&](int st) {
-#pragma unroll
-    for (int j = 0; j < NT; ++j)
-#pragma unroll
-      for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
-  };
+    auto step = [&](int st) {
+  #pragma unroll
+      for (int j = 0; j < NT; ++j)
+  #pragma unroll
+        for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st][j], fb[st][g], acc[j][g]);
+    };
 
-  int it = 0;
-  for (; it + PF < n_it; it += PF) {
+    int it = 0;
+    for (; it + PF < n_it; it += PF) {
+  #pragma unroll
+      for (int st = 0; st < PF; ++st) {
+        step(st);
+        load(fa[st], fb[st], it + st + PF);
+        // keep each step's refill next to its use instead of batching a
+        // whole round of loads at the end of the loop body
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  #pragma unroll
+    for (int st = 0; st < PF; ++st)
+      if (it + st < n_it) step(st);
+  } else {
+    // ---- X staged in LDS by a loader wave.  The WN waves of a K parity
+    // class take the same K steps for different N tiles, so each X chunk
+    // (kCK K steps x MG row groups) is loaded once per workgroup.  All vector
+    // loads of a wave complete in issue order, so X loads mixed into the
+    // weight stream would make every X wait drain the weight ring; here a
+    // ninth wave issues only X loads (global -> LDS, no registers) into LDS
+    // buffers, and the eight compute waves issue only
+    // weight loads, PF tiles ahead, and read X from LDS.  One workgroup
+    // barrier per chunk; the loader runs two chunks ahead (three buffers), so
+    // a chunk's X latency is hidden behind two chunks of weight streaming.
+    constexpr int kCK = MG <= 4 ? 8 : 4;       // K steps per X chunk (32 KiB)
+    constexpr int SPW = kCK / WK;              // a compute wave's K steps per chunk
+    constexpr int NR = PF / SPW;               // chunks per round of the weight ring
+    constexpr int kLead = 2;                   // chunks the loader runs ahead
+    constexpr int kBuf = kLead + 1;            // X chunk buffers in LDS
+    constexpr int kLPC = kCK * MG;             // loads per chunk (at most 63 may stay outstanding)
+    static_assert(PF % SPW == 0, "weight ring spans whole chunks");
+    static_assert((kLead - 1) * kLPC <= 63, "outstanding loads beyond the wait counter");
+    u32x4* xs = reinterpret_cast<u32x4*>(smem);  // [kBuf][kCK][MG][64]
+    const int n_chunks = (k_hi - k_lo + kCK - 1) / kCK;
+    if (loader) {
+      // chunk c -> buffer c % kBuf: one 1 KiB load per (K step, row group),
+      // lane l's 16 bytes landing at LDS piece l
+      auto xload = [&](int c) {
+        const int buf = c % kBuf;
 #pragma unroll
-    for (int st = 0; st < PF; ++st) {
-      step(st);
-      load(fa[st], fb[st], it + st + PF);
-      // keep each step's refill next to its use instead of batching a
-      // whole round of loads at the end of the loop body
-      __builtin_amdgcn_sched_barrier(0);
+        for (int kc = 0; kc < kCK; ++kc) {
+          const int kt = min(k_lo + c * kCK + kc, k_hi - 1);
+#pragma unroll
+          for (int g = 0; g < MG; ++g)
+            lds_load16(a.X + (static_cast<size_t>(kt) * a.Rg + gc[g]) * 64 + lane,
+                       xs + (static_cast<size_t>(buf * kCK + kc) * MG + g) * 64);
+        }
+      };
+      // wait until chunk c has landed: the chunks issued after it may stay
+      // in flight when there are kLead - 1 of them, else wait for all
+      auto wait_for = [&](int c) {
+        if (c + kLead - 1 < n_chunks) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kLead - 1) * kLPC) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      };
+#pragma unroll
+      for (int d = 0; d < kLead; ++d)
+        if (d < n_chunks) xload(d);
+      wait_for(0);
+      __syncthreads();
+      for (int c = 0; c < n_chunks; ++c) {
+        // buffer (c + kLead) % kBuf was last read in chunk c - 1
+        if (c + kLead < n_chunks) xload(c + kLead);
+        if (c + 1 < n_chunks) wait_for(c + 1);
+        __syncthreads();
+      }
+    } else {
+      auto wload = [&](u32x4& r, int i) {
+        const int kt = first + min(i, n_it - 1) * WK;
+        r = Wbase[(static_cast<size_t>(ntc[0]) * a.Kt + kt) * 64];
+      };
+      if (n_it > 0) {
+#pragma unroll
+        for (int st = 0; st < PF; ++st) wload(fa[st][0], st);
+      }
+      __syncthreads();
+      // one chunk from ring slots st0.. (compile-time: the ring lives in
+      // registers); FULL: every wave has all SPW steps, so nothing in it is
+      // conditional (a condition would make the compiler drain the load
+      // queue before each step)
+      auto chunk = [&](int c, auto st0_c, auto full_c) {
+        constexpr int st0 = decltype(st0_c)::value;
+        constexpr bool FULL = decltype(full_c)::value;
+#pragma unroll
+        for (int i = 0; i < SPW; ++i) {
+          const int it = c * SPW + i;
+          if (FULL || it < n_it) {
+            const u32x4* xb = xs + (static_cast<size_t>((c % kBuf) * kCK + wk + i * WK) * MG) * 64 + lane;
+            // all MG reads of the step before its MFMAs: one LDS wait per
+            // step instead of one per row group
+            u32x4 xv[MG];
+#pragma unroll
+            for (int g = 0; g < MG; ++g) xv[g] = xb[g * 64];
+#pragma unroll
+            for (int g = 0; g < MG; ++g) acc[0][g] = mfma_16x16x32(fa[st0 + i][0], xv[g], acc[0][g]);
+            wload(fa[st0 + i][0], it + PF);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        __syncthreads();
+      };
+      const int n_full = (k_hi - k_lo) / kCK;  // chunks in which every wave has SPW steps
+      int c = 0;
+      for (; c + NR <= n_full; c += NR) {
+        [&]<int... CC>(std::integer_sequence<int, CC...>) {
+          (chunk(c + CC, std::integral_constant<int, CC * SPW>{}, std::true_type{}), ...);
+        }(std::make_integer_sequence<int, NR>{});
+      }
+      // the rest of the chunks (fewer than a round), guarded
+      [&]<int... CC>(std::integer_sequence<int, CC...>) {
+        ((c + CC < n_chunks ? chunk(c + CC, std::integral_constant<int, CC * SPW>{}, std::false_type{}) : void()),
+         ...);
+      }(std::make_integer_sequence<int, NR>{});
     }
   }
-#pragma unroll
-  for (int st = 0; st < PF; ++st)
-    if (it + st < n_it) step(st);
 
   if constexpr (!kHoist) {
     epi_loads_a();
@@ -368,12 +481,22 @@ __global__ __launch_bounds__(64 * WN * WK) void k_gemm(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------- launcher
-template <int MG, int NT, int WN, int WK, int PF, int EPI>
+template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL = false>
 static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStream_t s) {
   const int n_groups = (a.N / 16 + NT * WN - 1) / (NT * WN);
   dim3 grid(n_groups, ksplit, m_tiles);
-  const size_t smem = (WK > 1 ? (WK - 1) : 0) * WN * NT * MG * 64 * sizeof(f32x4);
-  hipLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI>), grid, dim3(64 * WN * WK), smem, s, a);
+  // cross-wave reduction; with X in LDS the same space first holds the X chunks
+  size_t smem = (WK > 1 ? (WK - 1) : 0) * WN * NT * MG * 64 * sizeof(f32x4);
+  if constexpr (XL) {
+    smem = std::max<size_t>(smem, 3 * (MG <= 4 ? 8 : 4) * MG * 64 * sizeof(u32x4));
+    // with the static arrays this is more than 64 KiB of LDS: allow it once
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&k_gemm<MG, NT, WN, WK, PF, EPI, XL>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
+    if (attr != hipSuccess) return attr;
+  }
+  hipLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI, XL>), grid, dim3(64 * (WN * WK + (XL ? 1 : 0))), smem, s,
+                     a);
   return hipGetLastError();
 }
 
@@ -398,10 +521,18 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s);
     case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s);
     case 4:
+      if (p.xl) {
+        if (p.wn == 4) return launch_cfg<4, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
+        return launch_cfg<4, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
+      }
       if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s);
       if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
       return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
     default:
+      if (p.xl) {
+        if (p.wn == 4) return launch_cfg<8, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
+        return launch_cfg<8, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
+      }
       if (p.wn == 2) return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s);
       if (p.nt == 2) return launch_cfg<8, 2, 1, 4, 2, EPI>(a, p.m_tiles, p.ksplit, s);
       return launch_cfg<8, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
@@ -427,6 +558,11 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
       p.nt = 2;
       p.wn = 2;
       wk = 2;
+    } else if (shape == 4) {
+      // X in LDS: four N tiles per workgroup (two for QKV, whose N is small)
+      p.xl = true;
+      p.wn = epi == EPI_QKV ? 2 : 4;
+      wk = 8 / p.wn;
     } else {
       p.nt = shape == 1 ? 1 : shape == 2 ? 2 : (wide_n ? 2 : 1);
       wk = p.mg == 8 && p.nt == 2 ? 4 : 8;
@@ -437,9 +573,10 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   // a residual projection of one row tile splits K until the workgroups
   // reach resid_target, keeping at least 4 K steps per wave; k_resid_norm
   // then adds the splits' products into the residual
-  if (epi == EPI_RESID && resid_target > 0 && p.m_tiles == 1) {
+  const int target = p.xl ? std::max(resid_target, 384) : resid_target;
+  if (epi == EPI_RESID && target > 0 && p.m_tiles == 1) {
     const int Kt = K / 32;
-    int ks = std::min({(resid_target + p.n_groups - 1) / p.n_groups, kMaxResidSplits, std::max(1, Kt / (4 * wk))});
+    int ks = std::min({(target + p.n_groups - 1) / p.n_groups, kMaxResidSplits, std::max(1, Kt / (4 * wk))});
     ks = std::max(ks, 1);
     const int kc = (Kt + ks - 1) / ks;  // equal splits
     p.ksplit = (Kt + kc - 1) / kc;

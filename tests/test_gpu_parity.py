@@ -77,12 +77,12 @@ def test_mid_attention_splits(bps):
     print(st)
 
 
-@pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3),
-                                     (100, 0), (100, 1), (100, 2), (100, 3), (130, 0)])
+@pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3), (40, 4),
+                                     (100, 0), (100, 1), (100, 2), (100, 3), (100, 4), (130, 0), (130, 4)])
 def test_mid_projection_shapes(B, shape):
     """Every launch shape of the projections for 3 and 7 row groups (one or
-    two 16-column tiles per wave column, or a 2 x 2 wave grid) and a
-    row-tiled pass (130 rows: 8 + 1 row groups)."""
+    two 16-column tiles per wave column, a 2 x 2 wave grid, X staged in LDS
+    by a loader wave) and a row-tiled pass (130 rows: 8 + 1 row groups)."""
     from paper_2609_37062_amd.runner import DeviceRun
     ctx = np.random.default_rng(100 + B).integers(0, 400, size=B)
     w = decode_workload(MID, ctx, seed=13, name=f"mid-shape-b{B}-s{shape}")
