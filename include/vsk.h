@@ -232,14 +232,16 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        2048, with hidden at most 4096, and returns VSK_E_UNSUPPORTED for
  *        other passes.  Both paths compute the same values.
  * key 3: launch shape of the per-operation projections for 33..128 rows
- *        (and longer row-tiled passes): 0 (default) one column of eight
- *        K-split waves per workgroup over one 16-column tile (residual and
- *        QKV projections) or two (gate/up, lm_head), and for passes of more
- *        than 128 rows shape 3; 1 one tile everywhere; 2 two tiles
- *        everywhere; 3 a 2 x 2 grid of waves over four tiles; 4 the
- *        activation chunks staged in LDS by a ninth wave and shared by eight
- *        weight-streaming waves on four tiles (two for QKV), residual
- *        projections with K split over workgroups.
+ *        (and longer row-tiled passes): 0 (default) for 65 rows or more
+ *        shape 5 except for QKV; otherwise one column of eight K-split waves
+ *        per workgroup over one 16-column tile (residual and QKV projections)
+ *        or two (gate/up, lm_head), and for passes of more than 128 rows
+ *        shape 3; 1 one tile everywhere; 2 two tiles everywhere; 3 a 2 x 2
+ *        grid of waves over four tiles; 4 the activation chunks staged in
+ *        LDS by a ninth wave and shared by eight weight-streaming waves on
+ *        four tiles (two for QKV), residual projections with K split over
+ *        workgroups; 5 for 65 rows or more (QKV aside) the same staging with
+ *        two tiles per wave (eight per workgroup), everything else shape 3.
  * key 4: shared prefixes of a decode pass (vsk_batch_prefix_info): 1 (the
  *        default) reads each group's prefix blocks once for the group, 0 reads
  *        them once per sequence.

@@ -42,7 +42,7 @@ __device__ __forceinline__ void lds_load16(const u32x4* g, u32x4* lds) {
 
 template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL>
 __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs a) {
-  static_assert(!XL || (NT == 1 && WN * WK == 8 && (WK == 2 || WK == 4)), "X in LDS: 8 compute waves, one N tile each");
+  static_assert(!XL || (WN * WK == 8 && (WK == 2 || WK == 4)), "X in LDS: 8 compute waves");
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ float s_amv[WN][MG][16];
   __shared__ int s_ami[WN][MG][16];
@@ -236,13 +236,14 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
         __syncthreads();
       }
     } else {
-      auto wload = [&](u32x4& r, int i) {
+      auto wload = [&](u32x4 (&r)[NT], int i) {
         const int kt = first + min(i, n_it - 1) * WK;
-        r = Wbase[(static_cast<size_t>(ntc[0]) * a.Kt + kt) * 64];
+#pragma unroll
+        for (int j = 0; j < NT; ++j) r[j] = Wbase[(static_cast<size_t>(ntc[j]) * a.Kt + kt) * 64];
       };
       if (n_it > 0) {
 #pragma unroll
-        for (int st = 0; st < PF; ++st) wload(fa[st][0], st);
+        for (int st = 0; st < PF; ++st) wload(fa[st], st);
       }
       __syncthreads();
       // one chunk from ring slots st0.. (compile-time: the ring lives in
@@ -263,8 +264,10 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
             for (int g = 0; g < MG; ++g) xv[g] = xb[g * 64];
 #pragma unroll
-            for (int g = 0; g < MG; ++g) acc[0][g] = mfma_16x16x32(fa[st0 + i][0], xv[g], acc[0][g]);
-            wload(fa[st0 + i][0], it + PF);
+            for (int j = 0; j < NT; ++j)
+#pragma unroll
+              for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st0 + i][j], xv[g], acc[j][g]);
+            wload(fa[st0 + i], it + PF);
           }
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -509,9 +512,12 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 // K-split waves (8; 4 for two tiles of 8 row groups, whose cross-wave sums
 // would not fit 64 KiB of LDS) over one N tile (residual, QKV) or two
 // (gate/up, lm_head): N = hidden then still gives 192-256 workgroups; a
-// row-tiled pass takes shape 3.  Shape 1 takes one N tile everywhere, shape 2
+// row-tiled pass takes shape 3.  8 row groups other than QKV take shape 5's
+// X-in-LDS layout instead.  Shape 1 takes one N tile everywhere, shape 2
 // two, shape 3 is a 2 x 2 wave grid over four N tiles (fewer workgroups, each
-// X chunk feeding four tiles).
+// X chunk feeding four tiles), shape 4 stages X in LDS for four N tiles (two
+// for QKV), shape 5 for eight (two per wave) at 8 row groups, QKV and 4 row
+// groups taking the 2 x 2 grid.
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
   switch (p.mg) {
@@ -530,6 +536,9 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
     default:
       if (p.xl) {
+        // (QKV never takes it: its rotary factors would spill)
+        if constexpr (EPI != EPI_QKV)
+          if (p.nt == 2) return launch_cfg<8, 2, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s);
         if (p.wn == 4) return launch_cfg<8, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
         return launch_cfg<8, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
       }
@@ -554,7 +563,15 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
     // a row-tiled pass (more than 128 rows) re-streams the weights once per
     // row tile: there the 2 x 2 wave grid, each X chunk feeding four N
     // tiles, is the faster default
-    if (shape == 3 || (shape == 0 && p.m_tiles > 1)) {
+    if ((shape == 0 || shape == 5) && p.mg == 8 && epi != EPI_QKV) {
+      // X in LDS, two N tiles per wave: eight N tiles per workgroup, each X
+      // chunk read once from L2 for all of them (measured the fastest for 8
+      // row groups, one row tile or several)
+      p.xl = true;
+      p.nt = 2;
+      p.wn = 4;
+      wk = 2;
+    } else if (shape == 3 || shape == 5 || (shape == 0 && p.m_tiles > 1)) {
       p.nt = 2;
       p.wn = 2;
       wk = 2;

@@ -77,8 +77,9 @@ def test_mid_attention_splits(bps):
     print(st)
 
 
-@pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3), (40, 4),
-                                     (100, 0), (100, 1), (100, 2), (100, 3), (100, 4), (130, 0), (130, 4)])
+@pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3), (40, 4), (40, 5),
+                                     (100, 0), (100, 1), (100, 2), (100, 3), (100, 4), (100, 5),
+                                     (130, 0), (130, 4), (130, 5)])
 def test_mid_projection_shapes(B, shape):
     """Every launch shape of the projections for 3 and 7 row groups (one or
     two 16-column tiles per wave column, a 2 x 2 wave grid, X staged in LDS
