@@ -128,75 +128,77 @@ __global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ 
 
 // ---------------------------------------------------------------- residual sum + RMSNorm
 // A residual projection whose K was split over workgroups leaves one fp32
-// partial product per split (y[split][row][col]).  One workgroup per row adds
-// them to the residual in split order, x += ((y0 + y1) + y2) + ..., stores
-// x, and (gain non-null) normalises the row into bf16 frags of
-// x * g / sqrt(mean(x^2) + eps) -- the sum of squares in double, added in a
-// fixed order, the product in double and rounded once.
-__global__ __launch_bounds__(256) void k_resid_norm(float* __restrict__ x, const float* __restrict__ y, int splits,
-                                                    int R, int H, const uint16_t* __restrict__ g, float eps,
-                                                    uint16_t* __restrict__ hg, int Rg) {
-  __shared__ double s_ss[4];
-  constexpr int kMaxPieces = 4;  // 8-column pieces per thread: H <= 8192
+// partial product per split (y[split][row][col]).  One workgroup per row,
+// one thread per 8 columns, adds them to the residual in split order,
+// x += ((y0 + y1) + y2) + ..., stores x, and (gain non-null) normalises the
+// row into bf16 frags of x * g / sqrt(mean(x^2) + eps) -- the sum of squares
+// in double, added in a fixed order, the product in double and rounded once.
+// Every load of a thread (x, all splits, g) is issued before the first add,
+// so the row costs one memory round trip, not one per split.
+constexpr int kResidNormMaxSplits = 8;
+__global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ x, const float* __restrict__ y, int splits,
+                                                     int R, int H, const uint16_t* __restrict__ g, float eps,
+                                                     uint16_t* __restrict__ hg, int Rg) {
+  __shared__ double s_ss[16];
   const int r = blockIdx.x;
-  float e[kMaxPieces][8];
+  const int c = threadIdx.x * 8;
+  const bool on = c < H;
+  float* xr = x + static_cast<size_t>(r) * H + c;
+  float e[8];
+  u32x4 gv = u32x4{0u, 0u, 0u, 0u};
   double ss = 0.0;
-  float* xr = x + static_cast<size_t>(r) * H;
+  if (on) {
+    float4 a = *reinterpret_cast<const float4*>(xr);
+    float4 b = *reinterpret_cast<const float4*>(xr + 4);
+    float4 ya[kResidNormMaxSplits], yb[kResidNormMaxSplits];
 #pragma unroll
-  for (int k = 0; k < kMaxPieces; ++k) {
-    const int c = (threadIdx.x + 256 * k) * 8;
-    if (c >= H) break;
-    float4 a = *reinterpret_cast<const float4*>(xr + c);
-    float4 b = *reinterpret_cast<const float4*>(xr + c + 4);
-    float4 sa = make_float4(0.f, 0.f, 0.f, 0.f), sb = sa;
-    for (int sp = 0; sp < splits; ++sp) {
-      const float* yr = y + (static_cast<size_t>(sp) * R + r) * H + c;
-      const float4 ya = *reinterpret_cast<const float4*>(yr);
-      const float4 yb = *reinterpret_cast<const float4*>(yr + 4);
-      if (sp == 0) {
-        sa = ya;
-        sb = yb;
-      } else {
-        sa.x += ya.x; sa.y += ya.y; sa.z += ya.z; sa.w += ya.w;
-        sb.x += yb.x; sb.y += yb.y; sb.z += yb.z; sb.w += yb.w;
+    for (int sp = 0; sp < kResidNormMaxSplits; ++sp) {
+      if (sp < splits) {
+        const float* yr = y + (static_cast<size_t>(sp) * R + r) * H + c;
+        ya[sp] = *reinterpret_cast<const float4*>(yr);
+        yb[sp] = *reinterpret_cast<const float4*>(yr + 4);
+      }
+    }
+    if (g != nullptr) gv = *reinterpret_cast<const u32x4*>(g + c);
+    float4 sa = ya[0], sb = yb[0];
+#pragma unroll
+    for (int sp = 1; sp < kResidNormMaxSplits; ++sp) {
+      if (sp < splits) {
+        sa.x += ya[sp].x; sa.y += ya[sp].y; sa.z += ya[sp].z; sa.w += ya[sp].w;
+        sb.x += yb[sp].x; sb.y += yb[sp].y; sb.z += yb[sp].z; sb.w += yb[sp].w;
       }
     }
     a.x += sa.x; a.y += sa.y; a.z += sa.z; a.w += sa.w;
     b.x += sb.x; b.y += sb.y; b.z += sb.z; b.w += sb.w;
-    *reinterpret_cast<float4*>(xr + c) = a;
-    *reinterpret_cast<float4*>(xr + c + 4) = b;
-    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    *reinterpret_cast<float4*>(xr) = a;
+    *reinterpret_cast<float4*>(xr + 4) = b;
+    e[0] = a.x; e[1] = a.y; e[2] = a.z; e[3] = a.w;
+    e[4] = b.x; e[5] = b.y; e[6] = b.z; e[7] = b.w;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      e[k][q] = v[q];
-      ss += static_cast<double>(v[q]) * v[q];
-    }
+    for (int q = 0; q < 8; ++q) ss += static_cast<double>(e[q]) * e[q];
   }
   if (g == nullptr) return;
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
   if ((threadIdx.x & 63) == 0) s_ss[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const double tot = (s_ss[0] + s_ss[1]) + (s_ss[2] + s_ss[3]);
+  double tot = 0.0;
+  for (int w = 0; w < static_cast<int>(blockDim.x >> 6); ++w) tot += s_ss[w];
   const double rr = 1.0 / sqrt(tot / static_cast<double>(H) + static_cast<double>(eps));
+  if (!on) return;
+  u32x4 o;
 #pragma unroll
-  for (int k = 0; k < kMaxPieces; ++k) {
-    const int c = (threadIdx.x + 256 * k) * 8;
-    if (c >= H) break;
-    const u32x4 gv = *reinterpret_cast<const u32x4*>(g + c);
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      o[q] = d2bf(static_cast<double>(e[k][2 * q]) * bf2f(gv[q] & 0xffffu) * rr) |
-             (d2bf(static_cast<double>(e[k][2 * q + 1]) * bf2f(gv[q] >> 16) * rr) << 16);
-    *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
-  }
+  for (int q = 0; q < 4; ++q)
+    o[q] = d2bf(static_cast<double>(e[2 * q]) * bf2f(gv[q] & 0xffffu) * rr) |
+           (d2bf(static_cast<double>(e[2 * q + 1]) * bf2f(gv[q] >> 16) * rr) << 16);
+  *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
 }
 
 hipError_t launch_resid_norm(float* x, const float* y, int splits, int R, int H, const uint16_t* g, float eps,
                              uint16_t* hg, int Rg, hipStream_t s) {
-  if (H % 8 != 0 || H > 8192) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_resid_norm, dim3(R), dim3(256), 0, s, x, y, splits, R, H, g, eps, hg, Rg);
+  if (H % 8 != 0 || H > 8192 || splits < 1 || splits > kResidNormMaxSplits) return hipErrorInvalidValue;
+  const int threads = (H / 8 + 63) / 64 * 64;
+  hipLaunchKernelGGL(k_resid_norm, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg);
   return hipGetLastError();
 }
 
