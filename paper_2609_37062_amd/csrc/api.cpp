@@ -770,6 +770,23 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   aa.split_stride = aa.max_splits + (cascade ? b.max_pfx_splits : 0);
   aa.pfx_blocks = cascade ? b.pfx_blocks : nullptr;
   aa.pfx_splits = cascade ? b.pfx_splits : nullptr;
+  // decode work items launched per (row, KV head): the most splits any
+  // decode row has after its shared prefix (the rest would exit at once)
+  int dec_splits = 1;
+  {
+    const BatchHost& bh = h.bh;
+    auto row_splits = [&](int r) {
+      const int nb = (bh.pos[r] + 1 + kBlock - 1) / kBlock;
+      const int P = cascade ? bh.pfx_blocks[r] : 0;
+      dec_splits = std::max(dec_splits, (nb - P + aa.bps - 1) / aa.bps);
+    };
+    if (h.prefill_attn != 0 && b.n_pre_items > 0 && b.max_kv_len <= kMaxPrefillBlocks * kBlock) {
+      for (int32_t r : bh.dec_rows) row_splits(r);
+    } else {
+      for (int r = 0; r < R; ++r) row_splits(r);
+    }
+  }
+  const int pfx_fold = cascade ? b.max_pfx_splits : 0;
   AttnPrefixArgs ap{};
   ap.q = q;
   ap.pool = h.pool;
@@ -861,10 +878,11 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
       pf.layer = l;
       TRY(launch_attn_prefill(pf, b.n_pre_items, d, s));
       aa.rows = b.dec_rows;
-      if (b.n_dec_rows > 0) TRY(probed(4, [&] { return launch_attn_decode(aa, b.n_dec_rows, s); }));
+      if (b.n_dec_rows > 0)
+        TRY(probed(4, [&] { return launch_attn_decode(aa, b.n_dec_rows, dec_splits, pfx_fold, s); }));
     } else {
       aa.rows = nullptr;
-      TRY(probed(4, [&] { return launch_attn_decode(aa, R, s); }));
+      TRY(probed(4, [&] { return launch_attn_decode(aa, R, dec_splits, pfx_fold, s); }));
     }
     // O projection: x += o Wo^T, then the MLP's RMSNorm
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);

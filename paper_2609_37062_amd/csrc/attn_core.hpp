@@ -55,7 +55,10 @@ __device__ __forceinline__ int attn_row_splits(int kv_len, int bps) {
 
 // WT: the attention output is stored write-through (sc1), so that other
 // workgroups of the same launch read it from memory, not from a stale L2.
-template <int D, int NB, bool WT, int NW>
+// FOLD2: a wave loads two shared-prefix partials before folding either (one
+// round trip per two; 186 instead of 167 registers at head_dim 128), for
+// passes with more prefix partials per row than waves.
+template <int D, int NB, bool WT, int NW, bool FOLD2 = false>
 __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, int split, AttnLds<D, NW>& sm) {
   constexpr int KC = D / 32;  // K chunks (1 KiB) per block
   constexpr int VC = D / 16;  // V chunks (512 B) per block
@@ -180,12 +183,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   // just issued, whose latency they share)
   if (split == 0 && n_ps > 0 && h < G) {
     const size_t rh0 = static_cast<size_t>(row) * a.Hkv + hk;
-    for (int sp = w; sp < n_ps; sp += NW) {
-      const float* po = a.part_o + ((rh0 * a.split_stride + sp) * G + h) * D;
-      const float2 ml = a.part_ml[(rh0 * a.split_stride + sp) * G + h];
-      f32x4 op[VC];
-#pragma unroll
-      for (int c = 0; c < VC; ++c) op[c] = *reinterpret_cast<const f32x4*>(po + 16 * c + 4 * quad);
+    auto fold = [&](const f32x4 (&op)[VC], float2 ml) {
       const float M = fmaxf(m, ml.x);
       const float f0 = m == -INFINITY ? 0.f : exp2f(m - M);
       const float f1 = exp2f(ml.x - M);
@@ -193,6 +191,23 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
 #pragma unroll
       for (int c = 0; c < VC; ++c) o[c] = o[c] * f0 + op[c] * f1;
       m = M;
+    };
+    for (int sp = w; sp < n_ps; sp += (FOLD2 ? 2 : 1) * NW) {
+      const bool two = FOLD2 && sp + NW < n_ps;
+      const float* po0 = a.part_o + ((rh0 * a.split_stride + sp) * G + h) * D;
+      const float* po1 = po0 + (two ? static_cast<size_t>(NW) * G * D : 0);
+      const float2 ml0 = a.part_ml[(rh0 * a.split_stride + sp) * G + h];
+      const float2 ml1 = a.part_ml[(rh0 * a.split_stride + sp + (two ? NW : 0)) * G + h];
+      f32x4 op0[VC], op1[VC];
+#pragma unroll
+      for (int c = 0; c < VC; ++c) op0[c] = *reinterpret_cast<const f32x4*>(po0 + 16 * c + 4 * quad);
+      if constexpr (FOLD2) {
+#pragma unroll
+        for (int c = 0; c < VC; ++c) op1[c] = *reinterpret_cast<const f32x4*>(po1 + 16 * c + 4 * quad);
+      }
+      fold(op0, ml0);
+      if constexpr (FOLD2)
+        if (two) fold(op1, ml1);
     }
   }
   if (cnt > 0) {

@@ -20,22 +20,26 @@ namespace vsk {
 constexpr int kAttnNB = 2;                // K/V blocks in flight per wave (decode work items)
 constexpr int kPfxWaves = kPfxCols / 16;  // waves of a shared-prefix work item (16 columns each)
 
-template <int D, int NB>
+template <int D, int NB, bool FOLD2>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   __shared__ AttnLds<D, kAttnWaves> sm;
-  attn_unit<D, NB, false, kAttnWaves>(a, a.rows != nullptr ? a.rows[blockIdx.z] : static_cast<int>(blockIdx.z),
-                                      blockIdx.y, blockIdx.x, sm);
+  attn_unit<D, NB, false, kAttnWaves, FOLD2>(
+      a, a.rows != nullptr ? a.rows[blockIdx.z] : static_cast<int>(blockIdx.z), blockIdx.y, blockIdx.x, sm);
 }
 
-hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, hipStream_t s) {
-  dim3 grid(a.max_splits, a.Hkv, n_rows);
-  if (a.hd == 128) {
-    hipLaunchKernelGGL((k_attn_decode<128, kAttnNB>), grid, dim3(64 * kAttnWaves), 0, s, a);
-  } else if (a.hd == 64) {
-    hipLaunchKernelGGL((k_attn_decode<64, kAttnNB>), grid, dim3(64 * kAttnWaves), 0, s, a);
-  } else {
-    return hipErrorInvalidValue;
-  }
+template <int D>
+static void launch_decode_d(const AttnArgs& a, dim3 grid, bool fold2, hipStream_t s) {
+  if (fold2) hipLaunchKernelGGL((k_attn_decode<D, kAttnNB, true>), grid, dim3(64 * kAttnWaves), 0, s, a);
+  else hipLaunchKernelGGL((k_attn_decode<D, kAttnNB, false>), grid, dim3(64 * kAttnWaves), 0, s, a);
+}
+
+hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, int max_pfx_splits, hipStream_t s) {
+  if (grid_splits < 1 || grid_splits > a.max_splits) return hipErrorInvalidValue;
+  dim3 grid(grid_splits, a.Hkv, n_rows);
+  const bool fold2 = a.pfx_splits != nullptr && max_pfx_splits > kAttnWaves;
+  if (a.hd == 128) launch_decode_d<128>(a, grid, fold2, s);
+  else if (a.hd == 64) launch_decode_d<64>(a, grid, fold2, s);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
