@@ -73,6 +73,32 @@ __device__ __forceinline__ void store_wt16(void* p, uint32_t v) {
 // phase of a persistent kernel are then computed in that phase instead of
 // being hoisted out of the surrounding loop and held in registers across
 // every other phase.
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds + 16 l (the LDS address must be the same for the whole wave).  The
+// load counts in the wave's vector-memory counter until its bytes are in LDS.
+__device__ __forceinline__ void lds_load16(const u32x4* g, u32x4* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+// Workgroup barrier without a memory fence, for rings filled by
+// global-to-LDS loads.  __syncthreads() also fences, and before the fence the
+// compiler waits for every outstanding load into LDS, which would drain the
+// loads issued ahead.  Here a loading wave waits explicitly (s_waitcnt
+// vmcnt(N)) for exactly the loads that must have landed, and a reading wave
+// waits for its own LDS reads (lgkmcnt(0)) before the slot can be refilled.
+// The empty asm statements keep the compiler from moving memory accesses
+// across the barrier.
+__device__ __forceinline__ void barrier_after_lds_reads() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void barrier_no_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __device__ __forceinline__ int opaque_tid() {
   int t;
   asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"(static_cast<int>(threadIdx.x)));

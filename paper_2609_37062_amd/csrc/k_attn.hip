@@ -43,20 +43,39 @@ hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, in
   return hipGetLastError();
 }
 
-// Walk of one wave over a run of 16-token blocks for 16 query columns (each
-// lane's column h = lane % 16): S = K q on the matrix cores, online softmax
-// in base 2, O^T += V^T P^T with P split into bf16 high and low parts.  The
-// block ids are tbl[0..cnt) (in LDS), block tbl[i] holding key positions
-// 16 (b0 + i) ..; with MASK, key t counts for this lane's column only when
-// t <= lim, and V rows at positions >= kv_end are zeroed (stale slots of the
-// last block may hold NaN patterns).  NB blocks of loads stay in flight.
-template <int D, int NB, bool MASK>
+// Walk of a workgroup over a run of 16-token blocks: NW compute waves, each
+// for its own 16 query columns (each lane's column h = lane % 16), and one
+// loader wave (wave NW).  Per block a compute wave takes S = K q on the matrix
+// cores, an online softmax in base 2, and O^T += V^T P^T with P split into
+// bf16 high and low parts.  The block ids are tbl[0..cnt) (in LDS), block
+// tbl[i] holding key positions 16 (b0 + i) ..; every wave of the workgroup
+// calls this with the same cnt.  The loader brings each block's K and V
+// (D / 16 chunks of 1 KiB) once for the workgroup straight into a ring of
+// kWalkSlots LDS slots, kWalkLead blocks ahead; one workgroup barrier per
+// block hands a landed block to the compute waves and the slot they read in
+// the previous step back to the loader.  (The compute waves issue no
+// global-to-LDS loads themselves: the compiler would then drain every
+// outstanding one before each LDS read.)  A compute wave computes only the
+// first my_cnt blocks.  With MASK, key t counts for this lane's column only
+// when t <= lim, and V rows at positions >= kv_end are zeroed (stale slots
+// of the last block may hold NaN patterns).
+constexpr int kWalkLead = 4;
+constexpr int kWalkSlots = kWalkLead + 1;
+template <int D>
+struct WalkLds {
+  u32x4 ring[kWalkSlots][D / 16][64];  // per slot: D / 32 chunks of K, then D / 32 of V
+};
+
+template <int D, int NW, bool MASK>
 __device__ __forceinline__ void mq_walk(const u32x4 (&qf)[D / 32], const uint16_t* kbase, const uint16_t* vbase,
-                                        size_t kv_stride, const int32_t* tbl, int cnt, int b0, int lim, int kv_end,
-                                        float sc, float& m, float& l, f32x4 (&o)[D / 16]) {
-  constexpr int KC = D / 32;  // K chunks (1 KiB) per block
-  constexpr int VC = D / 16;  // V chunks (512 B) per block
-  const int lane = threadIdx.x & 63, quad = lane >> 4;
+                                        size_t kv_stride, const int32_t* tbl, int cnt, int my_cnt, int b0, int lim,
+                                        int kv_end, float sc, float& m, float& l, f32x4 (&o)[D / 16],
+                                        WalkLds<D>& sm) {
+  constexpr int KC = D / 32;   // K chunks (1 KiB) per block
+  constexpr int VC = D / 16;   // V chunks (512 B) per block
+  constexpr int NCH = 2 * KC;  // 1 KiB chunks per block
+  static_assert((kWalkLead - 1) * NCH <= 63, "outstanding loads beyond the wait counter");
+  const int lane = threadIdx.x & 63, quad = lane >> 4, w = threadIdx.x >> 6;
   auto process = [&](const u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {
     const int t_lane = 16 * b + 4 * quad;  // first key position of this lane's quarter
     if constexpr (MASK) {
@@ -107,39 +126,52 @@ __device__ __forceinline__ void mq_walk(const u32x4 (&qf)[D / 32], const uint16_
       o[k] = mfma_16x16x16(vf[k], pl, o[k]);
     }
   };
-  auto load = [&](u32x4 (&kf)[KC], u32x2 (&vf)[VC], int32_t tb) {
-    const size_t blk = static_cast<size_t>(tb);
-    const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
-    const u32x2* vp = reinterpret_cast<const u32x2*>(vbase + blk * kv_stride) + lane;
-#pragma unroll
-    for (int k = 0; k < KC; ++k) kf[k] = kp[k * 64];
-#pragma unroll
-    for (int k = 0; k < VC; ++k) vf[k] = vp[k * 64];
-  };
   if (cnt <= 0) return;
-  // loads past the end re-read the last block and the final round is peeled
-  u32x4 kf[NB][KC];
-  u32x2 vf[NB][VC];
+  if (w == NW) {
+    // block i (past the run: its last block again, into a slot nobody reads)
+    // -> slot i % kWalkSlots, one 1 KiB load per chunk
+    auto issue = [&](int i) {
+      const size_t blk = static_cast<size_t>(tbl[min(i, cnt - 1)]);
+      const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
+      const u32x4* vp = reinterpret_cast<const u32x4*>(vbase + blk * kv_stride) + lane;
 #pragma unroll
-  for (int i = 0; i < NB; ++i) load(kf[i], vf[i], tbl[min(i, cnt - 1)]);
-  int base = 0;
-  for (; base + NB < cnt; base += NB) {
+      for (int g = 0; g < NCH; ++g) lds_load16((g < KC ? kp : vp) + (g % KC) * 64, &sm.ring[i % kWalkSlots][g][0]);
+    };
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      process(kf[i], vf[i], b0 + base + i);
-      load(kf[i], vf[i], tbl[min(base + i + NB, cnt - 1)]);
+    for (int i = 0; i < kWalkLead; ++i) issue(i);
+    for (int i = 0; i < cnt; ++i) {
+      // block i has landed once at most the loads of the kWalkLead - 1 blocks
+      // after it are outstanding; the barrier then publishes it and frees the
+      // slot of block i - 1 for block i + kWalkLead
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kWalkLead - 1) * NCH) : "memory");
+      barrier_no_fence();
+      issue(i + kWalkLead);
+    }
+    // the loads past the run must land before the workgroup ends
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else {
+    for (int i = 0; i < cnt; ++i) {
+      barrier_after_lds_reads();
+      if (i < my_cnt) {
+        const u32x4* slot = &sm.ring[i % kWalkSlots][0][0];
+        u32x4 kf[KC];
+        u32x2 vf[VC];
+#pragma unroll
+        for (int k = 0; k < KC; ++k) kf[k] = slot[k * 64 + lane];
+#pragma unroll
+        for (int k = 0; k < VC; ++k) vf[k] = reinterpret_cast<const u32x2*>(slot + KC * 64)[k * 64 + lane];
+        process(kf, vf, b0 + i);
+      }
     }
   }
-#pragma unroll
-  for (int i = 0; i < NB; ++i)
-    if (base + i < cnt) process(kf[i], vf[i], b0 + base + i);
 }
 
-template <int D, int NB>
-__global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a) {
+template <int D>
+__global__ __launch_bounds__(64 * (kPfxWaves + 1)) void k_attn_prefix(AttnPrefixArgs a) {
   constexpr int KC = D / 32;
   constexpr int VC = D / 16;
   __shared__ int32_t tbl[kMaxPfxBps];
+  __shared__ WalkLds<D> ring;
 
   const int hk = blockIdx.y;
   const int32_t* it = a.items + static_cast<size_t>(blockIdx.x) * 5;
@@ -153,8 +185,9 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a
   for (int i = tid; i < b_hi - b_lo; i += blockDim.x) tbl[i] = ptbl[b_lo + i];
 
   // this lane's column: pair (group row c / G, query head c % G)
+  // (wave kPfxWaves only loads blocks: no column)
   const int c = col0 + 16 * w + h;
-  const bool cvalid = c < n_cols;
+  const bool cvalid = w < kPfxWaves && c < n_cols;
   const int row = cvalid ? a.grp_rows[roff + c / G] : 0;
   const int qh = cvalid ? c % G : 0;
   u32x4 qf[KC];
@@ -175,9 +208,12 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a
                           static_cast<size_t>(hk) * kBlock * D;
 
   __syncthreads();  // tbl
-  if (col0 + 16 * w >= n_cols) return;  // no column of this wave is in the group
-  // every wave walks all blocks of the item (all keys lie inside the prefix)
-  mq_walk<D, NB, false>(qf, kbase, vbase, kv_stride, tbl, b_hi - b_lo, b_lo, 0, 0, a.scale_log2, m, l, o);
+  // every wave walks all blocks of the item (all keys lie inside the prefix);
+  // a wave with no column in the group only loads its share of the blocks
+  const int cnt = b_hi - b_lo;
+  const int my_cnt = w < kPfxWaves && col0 + 16 * w < n_cols ? cnt : 0;
+  mq_walk<D, kPfxWaves, false>(qf, kbase, vbase, kv_stride, tbl, cnt, my_cnt, b_lo, 0, 0, a.scale_log2, m, l, o,
+                               ring);
 
   // this item's partial of each valid column, as split `split` of its row;
   // the decode kernel, launched after this one, reads them
@@ -199,11 +235,12 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefix(AttnPrefixArgs a
 // wave walks the blocks up to its last row's position; each lane masks the
 // keys past its own row.  The output is normalised and stored as the O
 // projection's input frags.
-template <int D, int NB>
-__global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefill(AttnPrefillArgs a) {
+template <int D>
+__global__ __launch_bounds__(64 * (kPfxWaves + 1)) void k_attn_prefill(AttnPrefillArgs a) {
   constexpr int KC = D / 32;
   constexpr int VC = D / 16;
   __shared__ int32_t tbl[kMaxPrefillBlocks];
+  __shared__ WalkLds<D> ring;
 
   const int hk = blockIdx.y;
   const int32_t* it = a.items + static_cast<size_t>(blockIdx.x) * 3;
@@ -220,7 +257,7 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefill(AttnPrefillArgs
   for (int i = tid; i < nb; i += blockDim.x) tbl[i] = table[i];
 
   const int c = 16 * w + h;
-  const bool cvalid = c < n_cols;
+  const bool cvalid = w < kPfxWaves && c < n_cols;  // (wave kPfxWaves only loads blocks)
   const int row = row0 + (cvalid ? c / G : 0);
   const int qh = cvalid ? c % G : 0;
   const int lim = cvalid ? a.pos[row] : -1;
@@ -242,11 +279,13 @@ __global__ __launch_bounds__(64 * kPfxWaves) void k_attn_prefill(AttnPrefillArgs
                           static_cast<size_t>(hk) * kBlock * D;
 
   __syncthreads();  // tbl
-  if (16 * w >= n_cols) return;
-  // this wave's last column decides how far it walks
+  // the workgroup walks the blocks of its last row; each wave computes up to
+  // its own last column's block (none if it has no column)
   const int c_last = min(16 * w + 15, n_cols - 1);
-  const int w_blocks = a.pos[row0 + c_last / G] / kBlock + 1;
-  mq_walk<D, NB, true>(qf, kbase, vbase, kv_stride, tbl, w_blocks, 0, lim, kv_end, a.scale_log2, m, l, o);
+  const int w_blocks = w < kPfxWaves && 16 * w < n_cols ? a.pos[row0 + c_last / G] / kBlock + 1 : 0;
+  mq_walk<D, kPfxWaves, true>(qf, kbase, vbase, kv_stride, tbl, nb, w_blocks, 0, lim, kv_end, a.scale_log2, m, l, o,
+                              ring);
+  if (!(w < kPfxWaves && 16 * w < n_cols)) return;
 
   if (cvalid) {
     const float inv = 1.f / l;
@@ -266,9 +305,9 @@ hipError_t launch_attn_prefill(const AttnPrefillArgs& a, int n_items, int head_d
   if (n_items <= 0) return hipSuccess;
   dim3 grid(n_items, a.Hkv);
   if (head_dim == 128) {
-    hipLaunchKernelGGL((k_attn_prefill<128, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_prefill<128>), grid, dim3(64 * (kPfxWaves + 1)), 0, s, a);
   } else if (head_dim == 64) {
-    hipLaunchKernelGGL((k_attn_prefill<64, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_prefill<64>), grid, dim3(64 * (kPfxWaves + 1)), 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }
@@ -279,9 +318,9 @@ hipError_t launch_attn_prefix(const AttnPrefixArgs& a, int n_items, int head_dim
   if (n_items <= 0) return hipSuccess;
   dim3 grid(n_items, a.Hkv);
   if (head_dim == 128) {
-    hipLaunchKernelGGL((k_attn_prefix<128, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_prefix<128>), grid, dim3(64 * (kPfxWaves + 1)), 0, s, a);
   } else if (head_dim == 64) {
-    hipLaunchKernelGGL((k_attn_prefix<64, 4>), grid, dim3(64 * kPfxWaves), 0, s, a);
+    hipLaunchKernelGGL((k_attn_prefix<64>), grid, dim3(64 * (kPfxWaves + 1)), 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }

@@ -34,12 +34,6 @@ namespace vsk {
 
 __device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v)); }
 
-// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
-// at lds + 16 l (the LDS address must be the same for the whole wave)
-__device__ __forceinline__ void lds_load16(const u32x4* g, u32x4* lds) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
-}
-
 template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL>
 __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs a) {
   static_assert(!XL || (WN * WK == 8 && (WK == 2 || WK == 4)), "X in LDS: 8 compute waves");
@@ -228,12 +222,12 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
       for (int d = 0; d < kLead; ++d)
         if (d < n_chunks) xload(d);
       wait_for(0);
-      __syncthreads();
+      barrier_no_fence();
       for (int c = 0; c < n_chunks; ++c) {
         // buffer (c + kLead) % kBuf was last read in chunk c - 1
         if (c + kLead < n_chunks) xload(c + kLead);
         if (c + 1 < n_chunks) wait_for(c + 1);
-        __syncthreads();
+        barrier_no_fence();
       }
     } else {
       auto wload = [&](u32x4 (&r)[NT], int i) {
@@ -271,7 +265,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
           }
           __builtin_amdgcn_sched_barrier(0);
         }
-        __syncthreads();
+        barrier_after_lds_reads();
       };
       const int n_full = (k_hi - k_lo) / kCK;  // chunks in which every wave has SPW steps
       int c = 0;
