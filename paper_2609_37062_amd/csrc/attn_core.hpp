@@ -8,15 +8,18 @@
 // sequence's block table (paper, "Invariants": each layer reads its own
 // cached K,V; Algorithm 1 keeps attention's launch shape).  The NW waves
 // take the split's 16-token blocks as contiguous ranges.  The split's
-// block-table entries are staged in LDS first; each wave then keeps NB
-// blocks of K/V loads in flight ahead of the block it processes.  Per block
-// a wave computes S = K q with v_mfma_f32_16x16x32_bf16 (16 tokens x up to
-// 16 heads), an online softmax in the base-2 domain, and O^T += V^T P^T with
-// v_mfma_f32_16x16x16_bf16, so the softmax row lives in the same lanes as the
-// output it rescales.  The waves merge in LDS; with several splits the last
-// workgroup to finish a (row, KV head) merges the splits' (m, l, O) partials
-// in split order.  Decode attention reads about group-size flops per byte of
-// KV, so it is bound by HBM, not by the matrix cores.
+// block-table entries are staged in LDS first; each wave then walks its
+// range two blocks (32 keys) at a time, the next pair's K and V loads issued
+// while the current pair is processed.  Per pair a wave computes S = K q with
+// v_mfma_f32_16x16x32_bf16 (two groups of 16 keys x up to 16 heads), an
+// online softmax in the base-2 domain, and O^T += V^T P^T with
+// v_mfma_f32_16x16x32_bf16 over the 32 keys, so the softmax row lives in the
+// same lanes as the output it rescales.  The waves merge in LDS; with several
+// splits the last workgroup to finish a (row, KV head) merges the splits'
+// (m, l, O) partials in split order.  Decode attention reads about
+// group-size flops per byte of KV; on this chip the matrix-core and softmax
+// instructions per byte still set its pace (measured: the same kernel without
+// them ran in less than half the time), hence 32-key steps.
 #pragma once
 
 #include <cmath>
@@ -39,10 +42,7 @@ struct AttnLds {
   int last;
 };
 
-// agent-scope (all XCDs) coherent accesses for the split partials
-__device__ __forceinline__ void st_agent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+// agent-scope (all XCDs) coherent loads of the split partials
 __device__ __forceinline__ float ld_agent(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -53,12 +53,119 @@ __device__ __forceinline__ int attn_row_splits(int kv_len, int bps) {
   return (nb + bps - 1) / bps;
 }
 
+// ---- 32-key steps.  Two 16-token blocks, A (keys 0..15 of the step) and B
+// (keys 16..31), are processed together, so that O^T += V^T P^T runs on
+// v_mfma_f32_16x16x32_bf16 (32 keys per MFMA) instead of two
+// v_mfma_f32_16x16x16_bf16, which take as many cycles each.  S = K q is taken
+// in two MFMA groups whose 16 rows are the step's keys 8 (r / 4) + r % 4
+// (group 0) and 8 (r / 4) + 4 + r % 4 (group 1): lane (column h, quarter q)
+// then holds S of keys 8q .. 8q + 3 and 8q + 4 .. 8q + 7, exactly the eight
+// probabilities P^T's operand asks of that lane, with no exchange between
+// lanes.  The softmax's cross-lane max and sum and the rescale of O run once
+// per 32 keys.
+//
+// K operand of group G: the block (0: A, 1: B) and the 16-byte index within
+// each 1 KiB K chunk (stored in the 16 x 16 x 32 A-operand order of one block:
+// piece key + 16 x dim-group) of the row this lane feeds.
+__device__ __forceinline__ int pair_k_block(int lane) { return (lane & 15) >> 3; }
+__device__ __forceinline__ int pair_k_index(int lane, int grp) {
+  return 8 * ((lane >> 2) & 1) + 4 * grp + (lane & 3) + 16 * (lane >> 4);
+}
+// V^T operand: lane (dim i, quarter q) takes keys 8q .. 8q + 7, i.e. block
+// q / 2, as two 8-byte pieces of each 512-byte V chunk (stored in the
+// 16 x 16 x 16 A-operand order of one block): index below, and index + 16.
+__device__ __forceinline__ int pair_v_block(int lane) { return lane >> 5; }
+__device__ __forceinline__ int pair_v_index(int lane) { return (lane & 15) + 32 * ((lane >> 4) & 1); }
+
+// One step over the keys at positions t0 .. t0 + 31, in two phases so that a
+// caller streaming K and V through registers can reload K as soon as the
+// scores are taken and V as soon as P V is issued.
+// pair_scores: S = K q from kg[G][c] (the K operands of group G), the online
+// softmax update of (m, l), and P = P_hi + P_lo (both bf16, about 16
+// significant bits, so the probabilities are not cut to bf16 precision before
+// P V) as the B operands ph, pl; alpha rescales O.  Keys at t >= t_end do not
+// count; with MASK a key also needs t <= lim.  Base 2 (sc = log2(e) /
+// sqrt(D)).  A column with no valid key yet keeps m = -inf and contributes
+// nothing.
+template <int D, bool MASK>
+__device__ __forceinline__ void pair_scores(const u32x4 (&qf)[D / 32], const u32x4 (&kg)[2][D / 32], int t0,
+                                            int t_end, int lim, float sc, float& m, float& l, u32x4& ph, u32x4& pl,
+                                            float& alpha) {
+  constexpr int KC = D / 32;
+  const int tv = t0 + 8 * ((threadIdx.x & 63) >> 4);  // this lane's first key (of 8)
+  f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+  for (int c = 0; c < KC; ++c) s0 = mfma_16x16x32(kg[0][c], qf[c], s0);
+#pragma unroll
+  for (int c = 0; c < KC; ++c) s1 = mfma_16x16x32(kg[1][c], qf[c], s1);
+  float mx = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int ta = tv + r, tb = tv + 4 + r;
+    bool va = ta < t_end, vb = tb < t_end;
+    if constexpr (MASK) {
+      va = va && ta <= lim;
+      vb = vb && tb <= lim;
+    }
+    s0[r] = va ? s0[r] * sc : -INFINITY;
+    s1[r] = vb ? s1[r] * sc : -INFINITY;
+    mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+  }
+  mx = fmaxf(mx, shfl_xor(mx, 16));
+  mx = fmaxf(mx, shfl_xor(mx, 32));
+  const float m_new = fmaxf(m, mx);
+  alpha = m_new == -INFINITY ? 1.f : exp2f(m - m_new);
+  float p[8], ps = 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    p[r] = m_new == -INFINITY ? 0.f : exp2f(s0[r] - m_new);
+    p[4 + r] = m_new == -INFINITY ? 0.f : exp2f(s1[r] - m_new);
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ps += p[j];
+  ps += shfl_xor(ps, 16);
+  ps += shfl_xor(ps, 32);
+  l = l * alpha + ps;
+  m = m_new;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    ph[j] = pack_bf2(p[2 * j], p[2 * j + 1]);
+    pl[j] = pack_bf2(p[2 * j] - bf2f(ph[j] & 0xffffu), p[2 * j + 1] - bf2f(ph[j] >> 16));
+  }
+}
+
+// pair_pv: O = alpha O + V^T P^T from vt[c] (the V^T operands).  V rows of
+// keys at t >= t_end are zeroed first: a slot past the end of a sequence may
+// hold a NaN pattern, and a zero probability times NaN is NaN.
+template <int D>
+__device__ __forceinline__ void pair_pv(u32x4 (&vt)[D / 16], int t0, int t_end, const u32x4& ph, const u32x4& pl,
+                                        float alpha, f32x4 (&o)[D / 16]) {
+  constexpr int VC = D / 16;
+  const int tv = t0 + 8 * ((threadIdx.x & 63) >> 4);
+  if (tv + 7 >= t_end) {
+    uint32_t mk[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      mk[j] = (tv + 2 * j < t_end ? 0x0000ffffu : 0u) | (tv + 2 * j + 1 < t_end ? 0xffff0000u : 0u);
+#pragma unroll
+    for (int c = 0; c < VC; ++c)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) vt[c][j] &= mk[j];
+  }
+#pragma unroll
+  for (int c = 0; c < VC; ++c) {
+    o[c] *= alpha;
+    o[c] = mfma_16x16x32(vt[c], ph, o[c]);  // lane holds O[column lane % 16][dim 16c + 4 (lane / 16) + r]
+    o[c] = mfma_16x16x32(vt[c], pl, o[c]);
+  }
+}
+
 // WT: the attention output is stored write-through (sc1), so that other
 // workgroups of the same launch read it from memory, not from a stale L2.
 // FOLD2: a wave loads two shared-prefix partials before folding either (one
 // round trip per two; 186 instead of 167 registers at head_dim 128), for
 // passes with more prefix partials per row than waves.
-template <int D, int NB, bool WT, int NW, bool FOLD2 = false>
+template <int D, bool WT, int NW, bool FOLD2 = false>
 __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, int split, AttnLds<D, NW>& sm) {
   constexpr int KC = D / 32;  // K chunks (1 KiB) per block
   constexpr int VC = D / 16;  // V chunks (512 B) per block
@@ -103,80 +210,52 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   const uint16_t* vbase = a.pool + (static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks * kv_stride +
                           static_cast<size_t>(hk) * kBlock * D;
 
-  // one 16-token block: S = K q, online softmax, O^T += V^T P^T
-  auto process = [&](const u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {
-    // slots past kv_len in the last block hold whatever was there: zero their
-    // V (a masked probability of 0 times a NaN pattern would still be NaN)
-    const int t_lane = b * kBlock + 4 * quad;  // first token of this lane's quarter
-    if (t_lane + 3 >= kv_len) {
-      const uint32_t m01 = (t_lane + 0 < kv_len ? 0x0000ffffu : 0u) | (t_lane + 1 < kv_len ? 0xffff0000u : 0u);
-      const uint32_t m23 = (t_lane + 2 < kv_len ? 0x0000ffffu : 0u) | (t_lane + 3 < kv_len ? 0xffff0000u : 0u);
+  // K and V operands of blocks 2p, 2p + 1 of this wave's range (a block past
+  // the range: its last block again, whose keys the step then masks)
+  auto pair_blocks = [&](int p, int cnt, int w_lo, size_t& bA, size_t& bB) {
+    bA = static_cast<size_t>(sm.tbl[w_lo + min(2 * p, cnt - 1)]);
+    bB = static_cast<size_t>(sm.tbl[w_lo + min(2 * p + 1, cnt - 1)]);
+  };
+  auto load_k = [&](u32x4 (&kg)[2][KC], int p, int cnt, int w_lo) {
+    size_t bA, bB;
+    pair_blocks(p, cnt, w_lo, bA, bB);
+    const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + (pair_k_block(lane) ? bB : bA) * kv_stride);
+    const int k0 = pair_k_index(lane, 0), k1 = pair_k_index(lane, 1);
 #pragma unroll
-      for (int c = 0; c < VC; ++c) {
-        vf[c][0] &= m01;
-        vf[c][1] &= m23;
-      }
-    }
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < KC; ++c) s = mfma_16x16x32(kf[c], qf[c], s);
-    // lane holds S[token 4*quad + r][head h]
-    float mx = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      s[r] = (t_lane + r < kv_len) ? s[r] * sc : -INFINITY;
-      mx = fmaxf(mx, s[r]);
-    }
-    mx = fmaxf(mx, shfl_xor(mx, 16));
-    mx = fmaxf(mx, shfl_xor(mx, 32));
-    const float m_new = fmaxf(m, mx);
-    const float alpha = exp2f(m - m_new);
-    float p[4], ps = 0.f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      p[r] = exp2f(s[r] - m_new);
-      ps += p[r];
-    }
-    ps += shfl_xor(ps, 16);
-    ps += shfl_xor(ps, 32);
-    l = l * alpha + ps;
-    m = m_new;
-    // P = P_hi + P_lo with both parts bf16 (about 16 significant bits), so the
-    // probabilities are not cut to bf16 precision before P V
-    u32x2 pf, pl;
-    pf[0] = pack_bf2(p[0], p[1]);
-    pf[1] = pack_bf2(p[2], p[3]);
-    pl[0] = pack_bf2(p[0] - bf2f(pf[0] & 0xffffu), p[1] - bf2f(pf[0] >> 16));
-    pl[1] = pack_bf2(p[2] - bf2f(pf[1] & 0xffffu), p[3] - bf2f(pf[1] >> 16));
-#pragma unroll
-    for (int c = 0; c < VC; ++c) {
-      o[c] *= alpha;
-      o[c] = mfma_16x16x16(vf[c], pf, o[c]);  // lane holds O[head h][dim 16c + 4*quad + r]
-      o[c] = mfma_16x16x16(vf[c], pl, o[c]);
+    for (int c = 0; c < KC; ++c) {
+      kg[0][c] = kp[c * 64 + k0];
+      kg[1][c] = kp[c * 64 + k1];
     }
   };
-  auto load = [&](u32x4 (&kf)[KC], u32x2 (&vf)[VC], int32_t tb) {
-    const size_t blk = static_cast<size_t>(tb);
-    const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
-    const u32x2* vp = reinterpret_cast<const u32x2*>(vbase + blk * kv_stride) + lane;
+  auto load_v = [&](u32x4 (&vt)[VC], int p, int cnt, int w_lo) {
+    size_t bA, bB;
+    pair_blocks(p, cnt, w_lo, bA, bB);
+    const u32x2* vp =
+        reinterpret_cast<const u32x2*>(vbase + (pair_v_block(lane) ? bB : bA) * kv_stride) + pair_v_index(lane);
 #pragma unroll
-    for (int c = 0; c < KC; ++c) kf[c] = kp[c * 64];
-#pragma unroll
-    for (int c = 0; c < VC; ++c) vf[c] = vp[c * 64];
+    for (int c = 0; c < VC; ++c) {
+      const u32x2 lo = vp[c * 64], hi = vp[c * 64 + 16];
+      vt[c] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+    }
   };
 
   __syncthreads();  // sm.tbl
-  // this wave's blocks: a contiguous range of the split, kept NB blocks ahead.
-  // Loads past the range re-read its last block and the final round is
-  // peeled, so the loop's loads are unconditional and stay in flight.
+  // this wave's blocks: a contiguous range of the split, taken two at a time.
+  // One pair's K and V live in registers: the next pair's K is loaded as soon
+  // as the scores are taken and its V as soon as P V is issued, so a load is
+  // always in flight.  Loads past the range re-read its last block, so the
+  // loop's loads are unconditional.
   const int per = (b_hi - b_lo + NW - 1) / NW;
   const int w_lo = min(b_hi - b_lo, w * per);
   const int cnt = min(b_hi - b_lo, w_lo + per) - w_lo;
-  u32x4 kf[NB][KC];
-  u32x2 vf[NB][VC];
+  const int n_pairs = (cnt + 1) / 2;
+  const int t_first = kBlock * (b_lo + w_lo);                   // first key of the range
+  const int t_end = min(kv_len, kBlock * (b_lo + w_lo + cnt));  // keys past it belong to others
+  u32x4 kg[2][KC];
+  u32x4 vt[VC];
   if (cnt > 0) {
-#pragma unroll
-    for (int i = 0; i < NB; ++i) load(kf[i], vf[i], sm.tbl[w_lo + min(i, cnt - 1)]);
+    load_k(kg, 0, cnt, w_lo);
+    load_v(vt, 0, cnt, w_lo);
   }
   // the first split starts from the group's shared-prefix partials: wave w
   // folds in partials w, w + NW, ... (their loads wait behind the K/V loads
@@ -210,18 +289,22 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
         if (two) fold(op1, ml1);
     }
   }
-  if (cnt > 0) {
-    int base = 0;
-    for (; base + NB < cnt; base += NB) {
-#pragma unroll
-      for (int i = 0; i < NB; ++i) {
-        process(kf[i], vf[i], b_lo + w_lo + base + i);
-        load(kf[i], vf[i], sm.tbl[w_lo + min(base + i + NB, cnt - 1)]);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < NB; ++i)
-      if (base + i < cnt) process(kf[i], vf[i], b_lo + w_lo + base + i);
+  // (the last pair is peeled so that the loop's loads are unconditional)
+  for (int p = 0; p + 1 < n_pairs; ++p) {
+    const int t0 = t_first + 2 * kBlock * p;
+    u32x4 ph, pl;
+    float alpha;
+    pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, ph, pl, alpha);
+    load_k(kg, p + 1, cnt, w_lo);
+    pair_pv<D>(vt, t0, t_end, ph, pl, alpha, o);
+    load_v(vt, p + 1, cnt, w_lo);
+  }
+  if (n_pairs > 0) {
+    const int t0 = t_first + 2 * kBlock * (n_pairs - 1);
+    u32x4 ph, pl;
+    float alpha;
+    pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, ph, pl, alpha);
+    pair_pv<D>(vt, t0, t_end, ph, pl, alpha, o);
   }
 
   // ---- merge the waves of this workgroup
@@ -273,22 +356,19 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
 
   // ---- several splits: publish this split's (m, l, O); the workgroup that
   // completes a (row, KV head) last merges all of them in split order.
-  // Partials are written and read with agent-scope atomic accesses, which
-  // bypass the non-coherent per-XCD L2 copies; a store is complete (visible
-  // at agent scope) once the wave's memory counter has drained, and only
-  // then is the arrival counted.  No workgroup waits for another.
+  // Partials are written with write-through stores (sc1, 16 bytes per lane)
+  // and read with agent-scope loads, which bypass the non-coherent per-XCD
+  // L2 copies; a store is complete (visible at agent scope) once the wave's
+  // memory counter has drained, and only then is the arrival counted.  No
+  // workgroup waits for another.
   const size_t rh = static_cast<size_t>(row) * a.Hkv + hk;
   if (w == 0 && h < G) {
     float* po = a.part_o + ((rh * a.split_stride + n_ps + split) * G + h) * D;
 #pragma unroll
-    for (int c = 0; c < VC; ++c)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) st_agent(po + 16 * c + 4 * quad + r, o[c][r]);
-    if (quad == 0) {
-      float* pm = reinterpret_cast<float*>(a.part_ml + (rh * a.split_stride + n_ps + split) * G + h);
-      st_agent(pm, m);
-      st_agent(pm + 1, l);
-    }
+    for (int c = 0; c < VC; ++c) store_wt(po + 16 * c + 4 * quad, __builtin_bit_cast(u32x4, o[c]));
+    if (quad == 0)
+      store_wt(a.part_ml + (rh * a.split_stride + n_ps + split) * G + h,
+               u32x2{__float_as_uint(m), __float_as_uint(l)});
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_waitcnt(0);
@@ -301,45 +381,60 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   if (!sm.last) return;
 
   // merge: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, in split order
-  // (this row's own splits, which follow its group's prefix partials)
-  constexpr int kC = 8;  // splits read with one round of independent loads
+  // (this row's own splits, which follow its group's prefix partials).  A
+  // thread takes outputs idx = tid, tid + blockDim.x, ... two at a time, and
+  // issues every load of a round of up to kC splits (both outputs' m, l and
+  // O) before the first is used: one memory round trip per round.
+  constexpr int kC = 8;  // splits per round
   const int n_all = n_splits;
   const float* pml = reinterpret_cast<const float*>(a.part_ml + (rh * a.split_stride + n_ps) * G);
   const float* pob = a.part_o + (rh * a.split_stride + n_ps) * G * D;
-  for (int idx = tid; idx < G * D; idx += blockDim.x) {
-    const int hh = idx / D, e = idx % D;
-    float acc = 0.f, L = 0.f, M = -INFINITY;
+  for (int i0 = tid; i0 < G * D; i0 += 2 * blockDim.x) {
+    const int i1 = i0 + blockDim.x;
+    const bool two = i1 < G * D;
+    const int hh[2] = {i0 / D, two ? i1 / D : i0 / D};
+    const int ee[2] = {i0 % D, two ? i1 % D : i0 % D};
+    float acc[2] = {0.f, 0.f}, L[2] = {0.f, 0.f}, M[2] = {-INFINITY, -INFINITY};
     for (int s0 = 0; s0 < n_all; s0 += kC) {
-      float mv[kC];
+      float mv[2][kC], lv[2][kC], ov[2][kC];
 #pragma unroll
-      for (int j = 0; j < kC; ++j)
-        mv[j] = s0 + j < n_all ? ld_agent(pml + 2 * ((s0 + j) * G + hh)) : -INFINITY;
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int j = 0; j < kC; ++j) M = fmaxf(M, mv[j]);
-    }
-    for (int s0 = 0; s0 < n_all; s0 += kC) {
-      float mv[kC], lv[kC], ov[kC];
-#pragma unroll
-      for (int j = 0; j < kC; ++j) {
-        const bool ok = s0 + j < n_all;
-        const int sj = s0 + j;
-        mv[j] = ok ? ld_agent(pml + 2 * (sj * G + hh)) : -INFINITY;
-        lv[j] = ok ? ld_agent(pml + 2 * (sj * G + hh) + 1) : 0.f;
-        ov[j] = ok ? ld_agent(pob + (static_cast<size_t>(sj) * G + hh) * D + e) : 0.f;
-      }
-#pragma unroll
-      for (int j = 0; j < kC; ++j) {
-        if (s0 + j < n_all) {
-          const float f = exp2f(mv[j] - M);
-          L += lv[j] * f;
-          acc += ov[j] * f;
+        for (int j = 0; j < kC; ++j) {
+          const int sj = min(s0 + j, n_all - 1);
+          mv[u][j] = ld_agent(pml + 2 * (sj * G + hh[u]));
+          lv[u][j] = ld_agent(pml + 2 * (sj * G + hh[u]) + 1);
+          ov[u][j] = ld_agent(pob + (static_cast<size_t>(sj) * G + hh[u]) * D + ee[u]);
         }
+      // rescale what earlier rounds summed to this round's running maximum
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        float Mn = M[u];
+#pragma unroll
+        for (int j = 0; j < kC; ++j)
+          if (s0 + j < n_all) Mn = fmaxf(Mn, mv[u][j]);
+        const float f0 = M[u] == -INFINITY ? 0.f : exp2f(M[u] - Mn);
+        L[u] *= f0;
+        acc[u] *= f0;
+#pragma unroll
+        for (int j = 0; j < kC; ++j) {
+          if (s0 + j < n_all) {
+            const float f = exp2f(mv[u][j] - Mn);
+            L[u] += lv[u][j] * f;
+            acc[u] += ov[u][j] * f;
+          }
+        }
+        M[u] = Mn;
       }
     }
-    const uint32_t ob = f2bf(acc * (1.f / L));
-    uint16_t* dst = a.out + frag_index(row, (hk * G + hh) * D + e, a.out_Rg);
-    if constexpr (WT) store_wt16(dst, ob);
-    else *dst = static_cast<uint16_t>(ob);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (u == 1 && !two) break;
+      const uint32_t ob = f2bf(acc[u] * (1.f / L[u]));
+      uint16_t* dst = a.out + frag_index(row, (hk * G + hh[u]) * D + ee[u], a.out_Rg);
+      if constexpr (WT) store_wt16(dst, ob);
+      else *dst = static_cast<uint16_t>(ob);
+    }
   }
   // ready for the next pass (or the next layer of a persistent pass)
   if (threadIdx.x == 0) __hip_atomic_store(a.counter + rh, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

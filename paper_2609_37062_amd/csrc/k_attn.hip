@@ -17,20 +17,19 @@
 
 namespace vsk {
 
-constexpr int kAttnNB = 2;                // K/V blocks in flight per wave (decode work items)
 constexpr int kPfxWaves = kPfxCols / 16;  // waves of a shared-prefix work item (16 columns each)
 
-template <int D, int NB, bool FOLD2>
+template <int D, bool FOLD2>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
   __shared__ AttnLds<D, kAttnWaves> sm;
-  attn_unit<D, NB, false, kAttnWaves, FOLD2>(
+  attn_unit<D, false, kAttnWaves, FOLD2>(
       a, a.rows != nullptr ? a.rows[blockIdx.z] : static_cast<int>(blockIdx.z), blockIdx.y, blockIdx.x, sm);
 }
 
 template <int D>
 static void launch_decode_d(const AttnArgs& a, dim3 grid, bool fold2, hipStream_t s) {
-  if (fold2) hipLaunchKernelGGL((k_attn_decode<D, kAttnNB, true>), grid, dim3(64 * kAttnWaves), 0, s, a);
-  else hipLaunchKernelGGL((k_attn_decode<D, kAttnNB, false>), grid, dim3(64 * kAttnWaves), 0, s, a);
+  if (fold2) hipLaunchKernelGGL((k_attn_decode<D, true>), grid, dim3(64 * kAttnWaves), 0, s, a);
+  else hipLaunchKernelGGL((k_attn_decode<D, false>), grid, dim3(64 * kAttnWaves), 0, s, a);
 }
 
 hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, int max_pfx_splits, hipStream_t s) {
@@ -45,122 +44,91 @@ hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, in
 
 // Walk of a workgroup over a run of 16-token blocks: NW compute waves, each
 // for its own 16 query columns (each lane's column h = lane % 16), and one
-// loader wave (wave NW).  Per block a compute wave takes S = K q on the matrix
-// cores, an online softmax in base 2, and O^T += V^T P^T with P split into
-// bf16 high and low parts.  The block ids are tbl[0..cnt) (in LDS), block
-// tbl[i] holding key positions 16 (b0 + i) ..; every wave of the workgroup
-// calls this with the same cnt.  The loader brings each block's K and V
-// (D / 16 chunks of 1 KiB) once for the workgroup straight into a ring of
-// kWalkSlots LDS slots, kWalkLead blocks ahead; one workgroup barrier per
-// block hands a landed block to the compute waves and the slot they read in
-// the previous step back to the loader.  (The compute waves issue no
+// loader wave (wave NW).  The compute waves take the blocks two at a time
+// (32-key steps: pair_scores and pair_pv).  The block ids are tbl[0..cnt) (in
+// LDS), block tbl[i] holding key positions 16 (b0 + i) ..; every wave of the
+// workgroup calls this with the same cnt.  The loader brings each pair's K and
+// V (2 x D / 16 chunks of 1 KiB) once for the workgroup straight into a ring
+// of kWalkSlots LDS slots, kWalkLead pairs ahead; one workgroup barrier per
+// pair hands a landed pair to the compute waves and the slot they read in the
+// previous step back to the loader.  (The compute waves issue no
 // global-to-LDS loads themselves: the compiler would then drain every
 // outstanding one before each LDS read.)  A compute wave computes only the
-// first my_cnt blocks.  With MASK, key t counts for this lane's column only
-// when t <= lim, and V rows at positions >= kv_end are zeroed (stale slots
-// of the last block may hold NaN patterns).
-constexpr int kWalkLead = 4;
+// pairs holding its first my_cnt blocks.  Keys at t >= t_end do not count
+// (their V is zeroed: stale slots may hold NaN patterns); with MASK a key
+// also needs t <= lim.
+constexpr int kWalkLead = 2;
 constexpr int kWalkSlots = kWalkLead + 1;
 template <int D>
 struct WalkLds {
-  u32x4 ring[kWalkSlots][D / 16][64];  // per slot: D / 32 chunks of K, then D / 32 of V
+  u32x4 ring[kWalkSlots][2][D / 16][64];  // per slot and block: D / 32 chunks of K, then D / 32 of V
 };
 
 template <int D, int NW, bool MASK>
 __device__ __forceinline__ void mq_walk(const u32x4 (&qf)[D / 32], const uint16_t* kbase, const uint16_t* vbase,
                                         size_t kv_stride, const int32_t* tbl, int cnt, int my_cnt, int b0, int lim,
-                                        int kv_end, float sc, float& m, float& l, f32x4 (&o)[D / 16],
+                                        int t_end, float sc, float& m, float& l, f32x4 (&o)[D / 16],
                                         WalkLds<D>& sm) {
   constexpr int KC = D / 32;   // K chunks (1 KiB) per block
   constexpr int VC = D / 16;   // V chunks (512 B) per block
   constexpr int NCH = 2 * KC;  // 1 KiB chunks per block
-  static_assert((kWalkLead - 1) * NCH <= 63, "outstanding loads beyond the wait counter");
-  const int lane = threadIdx.x & 63, quad = lane >> 4, w = threadIdx.x >> 6;
-  auto process = [&](const u32x4 (&kf)[KC], u32x2 (&vf)[VC], int b) {
-    const int t_lane = 16 * b + 4 * quad;  // first key position of this lane's quarter
-    if constexpr (MASK) {
-      if (t_lane + 3 >= kv_end) {
-        const uint32_t m01 = (t_lane + 0 < kv_end ? 0x0000ffffu : 0u) | (t_lane + 1 < kv_end ? 0xffff0000u : 0u);
-        const uint32_t m23 = (t_lane + 2 < kv_end ? 0x0000ffffu : 0u) | (t_lane + 3 < kv_end ? 0xffff0000u : 0u);
-#pragma unroll
-        for (int k = 0; k < VC; ++k) {
-          vf[k][0] &= m01;
-          vf[k][1] &= m23;
-        }
-      }
-    }
-    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int k = 0; k < KC; ++k) s = mfma_16x16x32(kf[k], qf[k], s);
-    float mx = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      if constexpr (MASK) s[r] = t_lane + r <= lim ? s[r] * sc : -INFINITY;
-      else s[r] *= sc;
-      mx = fmaxf(mx, s[r]);
-    }
-    mx = fmaxf(mx, shfl_xor(mx, 16));
-    mx = fmaxf(mx, shfl_xor(mx, 32));
-    const float m_new = fmaxf(m, mx);
-    // a column with no valid key yet keeps m = -inf: its factors must be 0, not NaN
-    const float alpha = m_new == -INFINITY ? 1.f : exp2f(m - m_new);
-    float p[4], ps = 0.f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      p[r] = m_new == -INFINITY ? 0.f : exp2f(s[r] - m_new);
-      ps += p[r];
-    }
-    ps += shfl_xor(ps, 16);
-    ps += shfl_xor(ps, 32);
-    l = l * alpha + ps;
-    m = m_new;
-    u32x2 pf, pl;
-    pf[0] = pack_bf2(p[0], p[1]);
-    pf[1] = pack_bf2(p[2], p[3]);
-    pl[0] = pack_bf2(p[0] - bf2f(pf[0] & 0xffffu), p[1] - bf2f(pf[0] >> 16));
-    pl[1] = pack_bf2(p[2] - bf2f(pf[1] & 0xffffu), p[3] - bf2f(pf[1] >> 16));
-#pragma unroll
-    for (int k = 0; k < VC; ++k) {
-      o[k] *= alpha;
-      o[k] = mfma_16x16x16(vf[k], pf, o[k]);
-      o[k] = mfma_16x16x16(vf[k], pl, o[k]);
-    }
-  };
+  static_assert((kWalkLead - 1) * 2 * NCH <= 63, "outstanding loads beyond the wait counter");
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int n_pairs = (cnt + 1) / 2;
   if (cnt <= 0) return;
   if (w == NW) {
-    // block i (past the run: its last block again, into a slot nobody reads)
-    // -> slot i % kWalkSlots, one 1 KiB load per chunk
-    auto issue = [&](int i) {
-      const size_t blk = static_cast<size_t>(tbl[min(i, cnt - 1)]);
-      const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
-      const u32x4* vp = reinterpret_cast<const u32x4*>(vbase + blk * kv_stride) + lane;
+    // pair p (past the run: its last block again, into a slot nobody reads or
+    // a half whose keys are masked) -> slot p % kWalkSlots
+    auto issue = [&](int p) {
 #pragma unroll
-      for (int g = 0; g < NCH; ++g) lds_load16((g < KC ? kp : vp) + (g % KC) * 64, &sm.ring[i % kWalkSlots][g][0]);
+      for (int hb = 0; hb < 2; ++hb) {
+        const size_t blk = static_cast<size_t>(tbl[min(2 * p + hb, cnt - 1)]);
+        const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
+        const u32x4* vp = reinterpret_cast<const u32x4*>(vbase + blk * kv_stride) + lane;
+#pragma unroll
+        for (int g = 0; g < NCH; ++g)
+          lds_load16((g < KC ? kp : vp) + (g % KC) * 64, &sm.ring[p % kWalkSlots][hb][g][0]);
+      }
     };
 #pragma unroll
-    for (int i = 0; i < kWalkLead; ++i) issue(i);
-    for (int i = 0; i < cnt; ++i) {
-      // block i has landed once at most the loads of the kWalkLead - 1 blocks
+    for (int p = 0; p < kWalkLead; ++p) issue(p);
+    for (int p = 0; p < n_pairs; ++p) {
+      // pair p has landed once at most the loads of the kWalkLead - 1 pairs
       // after it are outstanding; the barrier then publishes it and frees the
-      // slot of block i - 1 for block i + kWalkLead
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kWalkLead - 1) * NCH) : "memory");
+      // slot of pair p - 1 for pair p + kWalkLead
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((kWalkLead - 1) * 2 * NCH) : "memory");
       barrier_no_fence();
-      issue(i + kWalkLead);
+      issue(p + kWalkLead);
     }
     // the loads past the run must land before the workgroup ends
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   } else {
-    for (int i = 0; i < cnt; ++i) {
+    const int my_pairs = (my_cnt + 1) / 2;
+    const int kb = pair_k_block(lane), k0 = pair_k_index(lane, 0), k1 = pair_k_index(lane, 1);
+    const int vb = pair_v_block(lane), vi = pair_v_index(lane);
+    for (int p = 0; p < n_pairs; ++p) {
       barrier_after_lds_reads();
-      if (i < my_cnt) {
-        const u32x4* slot = &sm.ring[i % kWalkSlots][0][0];
-        u32x4 kf[KC];
-        u32x2 vf[VC];
+      if (p < my_pairs) {
+        const int slot = p % kWalkSlots;
+        const u32x4* kp = &sm.ring[slot][kb][0][0];
+        const u32x2* vp = reinterpret_cast<const u32x2*>(&sm.ring[slot][vb][KC][0]) + vi;
+        u32x4 kg[2][KC];
+        u32x4 vt[VC];
 #pragma unroll
-        for (int k = 0; k < KC; ++k) kf[k] = slot[k * 64 + lane];
+        for (int c = 0; c < KC; ++c) {
+          kg[0][c] = kp[c * 64 + k0];
+          kg[1][c] = kp[c * 64 + k1];
+        }
 #pragma unroll
-        for (int k = 0; k < VC; ++k) vf[k] = reinterpret_cast<const u32x2*>(slot + KC * 64)[k * 64 + lane];
-        process(kf, vf, b0 + i);
+        for (int c = 0; c < VC; ++c) {
+          const u32x2 lo = vp[c * 64], hi = vp[c * 64 + 16];
+          vt[c] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        }
+        const int t0 = kBlock * (b0 + 2 * p);
+        u32x4 ph, pl;
+        float alpha;
+        pair_scores<D, MASK>(qf, kg, t0, t_end, lim, sc, m, l, ph, pl, alpha);
+        pair_pv<D>(vt, t0, t_end, ph, pl, alpha, o);
       }
     }
   }
@@ -212,8 +180,8 @@ __global__ __launch_bounds__(64 * (kPfxWaves + 1)) void k_attn_prefix(AttnPrefix
   // a wave with no column in the group only loads its share of the blocks
   const int cnt = b_hi - b_lo;
   const int my_cnt = w < kPfxWaves && col0 + 16 * w < n_cols ? cnt : 0;
-  mq_walk<D, kPfxWaves, false>(qf, kbase, vbase, kv_stride, tbl, cnt, my_cnt, b_lo, 0, 0, a.scale_log2, m, l, o,
-                               ring);
+  mq_walk<D, kPfxWaves, false>(qf, kbase, vbase, kv_stride, tbl, cnt, my_cnt, b_lo, 0, kBlock * b_hi, a.scale_log2,
+                               m, l, o, ring);
 
   // this item's partial of each valid column, as split `split` of its row;
   // the decode kernel, launched after this one, reads them
@@ -283,8 +251,8 @@ __global__ __launch_bounds__(64 * (kPfxWaves + 1)) void k_attn_prefill(AttnPrefi
   // its own last column's block (none if it has no column)
   const int c_last = min(16 * w + 15, n_cols - 1);
   const int w_blocks = w < kPfxWaves && 16 * w < n_cols ? a.pos[row0 + c_last / G] / kBlock + 1 : 0;
-  mq_walk<D, kPfxWaves, true>(qf, kbase, vbase, kv_stride, tbl, nb, w_blocks, 0, lim, kv_end, a.scale_log2, m, l, o,
-                              ring);
+  mq_walk<D, kPfxWaves, true>(qf, kbase, vbase, kv_stride, tbl, nb, w_blocks, 0, lim, min(kv_end, kBlock * nb),
+                              a.scale_log2, m, l, o, ring);
   if (!(w < kPfxWaves && 16 * w < n_cols)) return;
 
   if (cvalid) {

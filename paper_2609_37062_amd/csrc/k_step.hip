@@ -54,7 +54,6 @@ constexpr int kWaves = 8;                 // waves per workgroup (the K split of
 constexpr int kPF = 8;                    // weight tiles in flight per wave
 constexpr unsigned kSpinLimit = 1u << 21; // a few seconds of polling before a wait is declared failed
 constexpr size_t kLdsRed = 2 * (kWaves - 1) * 1024;  // double-buffered cross-wave reduction
-constexpr int kAttnBlocksInFlight = 2;    // K/V blocks in flight per wave in the attention phase
 constexpr int kMaxParts = 256;            // sum-of-squares partials per row (hidden / 16, hidden <= 4096)
 
 __device__ __forceinline__ unsigned ld_agent_u32(const unsigned* p) {
@@ -629,7 +628,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
       for (int v = blockIdx.x; v < n_items; v += gridDim.x) {
         const int rem = v % (a.Hkv * R);
         __syncthreads();
-        attn_unit<D, kAttnBlocksInFlight, true, kWaves>(aa, rem / a.Hkv, rem % a.Hkv, v / (a.Hkv * R),
+        attn_unit<D, true, kWaves>(aa, rem / a.Hkv, rem % a.Hkv, v / (a.Hkv * R),
                                                         *reinterpret_cast<AttnLds<D, kWaves>*>(lds));
       }
     }
