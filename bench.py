@@ -11,8 +11,9 @@ resident in HBM before timing starts and the step is replayed idempotently.
 Prints ONE JSON line.  ``value`` is decode tokens/s (rows per step / step
 time, the faster of eager launches and a captured HIP graph of the step);
 ``roofline`` reports the gate/up projection (the largest kernel of a layer),
-timed live with HIP events around each of its launches during a timed pass
-loop; ``cpu_baseline`` times the float64 CPU oracle on a bounded sample of
+timed live with HIP events bound to each of its launches (hipExtLaunchKernel:
+the kernel's own start and end on the pass stream) during a timed pass loop;
+``cpu_baseline`` times the float64 CPU oracle on a bounded sample of
 the same workload.  The batch-64 shared-prefix workload is reported beside it.
 """
 from __future__ import annotations

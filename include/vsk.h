@@ -207,12 +207,15 @@ int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32
                       int32_t* ids_dev, void* stream);
 
 /* Timing probes (measurement only).  While set, the first n_pairs launches
- * of kernel class `which` in the following passes are each bracketed by
- * hipEventRecord(begin_events[i]) / hipEventRecord(end_events[i]) on the pass
- * stream, in launch order.  Classes: 0 gate/up projection, 1 down projection,
- * 2 QKV projection, 3 O projection, 4 attention, 5 lm_head projection.
- * Events are caller-created hipEvent_t handles; n_pairs = 0 clears the probe.
- * Do not set probes while a pass is being captured into a graph. */
+ * of kernel class `which` in the following passes are each launched with
+ * hipExtLaunchKernel bound to (begin_events[i], end_events[i]), in launch
+ * order: the events take that kernel's own start and end times on the pass
+ * stream (hipEventElapsedTime then gives its execution time, without the
+ * dispatch gap before it).  Classes: 0 gate/up projection, 1 down
+ * projection, 2 QKV projection, 3 O projection, 4 decode attention, 5
+ * lm_head projection.  Events are caller-created hipEvent_t handles (with
+ * timing); n_pairs = 0 clears the probe.  Do not set probes while a pass is
+ * being captured into a graph. */
 int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
                   void* const* end_events, int32_t n_pairs);
 

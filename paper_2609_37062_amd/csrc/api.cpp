@@ -714,17 +714,17 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   do {                                 \
     if ((e = (call)) != hipSuccess) return e; \
   } while (0)
-  // probe-bracketed launch of kernel class `cls`
+  // probed launch of kernel class `cls`: while probe events remain, the
+  // launch takes the next pair, bound to its dispatch (the kernel's own start
+  // and end times)
   auto probed = [&](int cls, auto&& launch) -> hipError_t {
-    const bool on = h.probe_i[cls] < h.probe_b[cls].size();
-    hipError_t pe;
-    if (on && (pe = hipEventRecord(h.probe_b[cls][h.probe_i[cls]], s)) != hipSuccess) return pe;
-    if ((pe = launch()) != hipSuccess) return pe;
-    if (on) {
-      if ((pe = hipEventRecord(h.probe_e[cls][h.probe_i[cls]], s)) != hipSuccess) return pe;
+    LaunchEvents ev;
+    if (h.probe_i[cls] < h.probe_b[cls].size()) {
+      ev.start = h.probe_b[cls][h.probe_i[cls]];
+      ev.stop = h.probe_e[cls][h.probe_i[cls]];
       ++h.probe_i[cls];
     }
-    return hipSuccess;
+    return launch(ev);
   };
 
   TRY(launch_embed(reinterpret_cast<const uint16_t*>(P + h.pl.embed), pa.ids, R, H, c.vocab, x, ssq, s));
@@ -843,14 +843,14 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     if (p.ksplit > 1) {
       ga.ypart = ypart;
       ga.ssq_out = nullptr;
-      if ((re = probed(cls, [&] { return launch_gemm(ga, p, EPI_RESID, s); })) != hipSuccess) return re;
+      if ((re = probed(cls, [&](LaunchEvents ev) { return launch_gemm(ga, p, EPI_RESID, s, ev); })) != hipSuccess) return re;
       ga.ypart = nullptr;
       if ((re = launch_resid_norm(x, ypart, p.ksplit, R, H, next_gain, c.rms_eps, fb, Rg, s)) != hipSuccess) return re;
       normed = next_gain != nullptr;
     } else {
       ga.ypart = nullptr;
       ga.ssq_out = ssq;
-      if ((re = probed(cls, [&] { return launch_gemm(ga, p, EPI_RESID, s); })) != hipSuccess) return re;
+      if ((re = probed(cls, [&](LaunchEvents ev) { return launch_gemm(ga, p, EPI_RESID, s, ev); })) != hipSuccess) return re;
       ssq_parts = p.n_groups;
       normed = false;
     }
@@ -868,7 +868,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     ga.ssq_out = nullptr;
     ga.out = q;
     ga.layer = l;
-    TRY(probed(2, [&] { return launch_gemm(ga, p_qkv, EPI_QKV, s); }));
+    TRY(probed(2, [&](LaunchEvents ev) { return launch_gemm(ga, p_qkv, EPI_QKV, s, ev); }));
     aa.layer = l;
     if (cascade) {
       ap.layer = l;
@@ -879,10 +879,10 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
       TRY(launch_attn_prefill(pf, b.n_pre_items, d, s));
       aa.rows = b.dec_rows;
       if (b.n_dec_rows > 0)
-        TRY(probed(4, [&] { return launch_attn_decode(aa, b.n_dec_rows, dec_splits, pfx_fold, s); }));
+        TRY(probed(4, [&](LaunchEvents ev) { return launch_attn_decode(aa, b.n_dec_rows, dec_splits, pfx_fold, s, ev); }));
     } else {
       aa.rows = nullptr;
-      TRY(probed(4, [&] { return launch_attn_decode(aa, R, dec_splits, pfx_fold, s); }));
+      TRY(probed(4, [&](LaunchEvents ev) { return launch_attn_decode(aa, R, dec_splits, pfx_fold, s, ev); }));
     }
     // O projection: x += o Wo^T, then the MLP's RMSNorm
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wo);
@@ -898,7 +898,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     ga.N = 2 * F;
     ga.ssq_out = nullptr;
     ga.out = fc;
-    TRY(probed(0, [&] { return launch_gemm(ga, p_gu, EPI_SWIGLU, s); }));
+    TRY(probed(0, [&](LaunchEvents ev) { return launch_gemm(ga, p_gu, EPI_SWIGLU, s, ev); }));
     // down projection: x += a Wd^T, then the next layer's RMSNorm (or the
     // final one of a decode pass, whose rows all return logits)
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wd);
@@ -932,7 +932,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ga.out_Rg = Rgo;
   ga.am_val = reinterpret_cast<float*>(ws + wl.am_part);
   ga.am_idx = reinterpret_cast<int*>(ws + wl.am_part + static_cast<size_t>((c.vocab + 15) / 16) * wl.max_rows * 4);
-  TRY(probed(5, [&] { return launch_gemm(ga, p_lm, EPI_LOGITS, s); }));
+  TRY(probed(5, [&](LaunchEvents ev) { return launch_gemm(ga, p_lm, EPI_LOGITS, s, ev); }));
   if (pa.next_ids) TRY(launch_argmax_partials(ga.am_val, ga.am_idx, p_lm.n_groups, Ro, pa.next_ids, s));
 #undef TRY
   h.counters[0] += 1;

@@ -68,7 +68,8 @@ struct AttnPrefixArgs {
 // grid_splits: split work items launched per (row, KV head), at least the
 // most any row has after its shared prefix and at most a.max_splits.
 // max_pfx_splits: the most prefix partials any row folds in.
-hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, int max_pfx_splits, hipStream_t s);
+hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, int max_pfx_splits, hipStream_t s,
+                              LaunchEvents ev = {});
 hipError_t launch_attn_prefix(const AttnPrefixArgs& a, int n_items, int head_dim, hipStream_t s);
 hipError_t launch_attn_prefill(const AttnPrefillArgs& a, int n_items, int head_dim, hipStream_t s);
 

@@ -44,6 +44,6 @@ constexpr int kResidTargetWgs = 0;  // default split-K target of the residual pr
 // shape: launch shape for 4 or 8 row groups (0 default; see k_gemm.hip)
 // resid_target: workgroups a residual projection's K split aims for (0: no split)
 GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0, int resid_target = 0);
-hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s);
+hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s, LaunchEvents ev = {});
 
 }  // namespace vsk

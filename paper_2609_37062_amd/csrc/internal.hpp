@@ -93,6 +93,12 @@ struct BatchDev {
 };
 
 // ---------------------------------------------------------------- workspace
+// Timing probes: events bound to one dispatch (hipExtLaunchKernel), which
+// take that kernel's own start and end times; null for an ordinary launch.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
 struct WsLayout {
   int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
   size_t x, x_c, fa, fb, fc, q, att_o, att_ml, att_cnt, ssq, ssq_c, am_part, total;

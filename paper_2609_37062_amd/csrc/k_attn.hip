@@ -13,6 +13,8 @@
 // waves starting their online softmax from the prefix partials.  Softmax over the
 // union of key sets is exactly the merge of the per-set partials, so this
 // only changes the summation order.
+#include <hip/hip_ext.h>
+
 #include "attn_core.hpp"
 
 namespace vsk {
@@ -26,18 +28,27 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn_decode(AttnArgs a) {
       a, a.rows != nullptr ? a.rows[blockIdx.z] : static_cast<int>(blockIdx.z), blockIdx.y, blockIdx.x, sm);
 }
 
-template <int D>
-static void launch_decode_d(const AttnArgs& a, dim3 grid, bool fold2, hipStream_t s) {
-  if (fold2) hipLaunchKernelGGL((k_attn_decode<D, true>), grid, dim3(64 * kAttnWaves), 0, s, a);
-  else hipLaunchKernelGGL((k_attn_decode<D, false>), grid, dim3(64 * kAttnWaves), 0, s, a);
+template <int D, bool FOLD2>
+static void launch_decode_k(const AttnArgs& a, dim3 grid, hipStream_t s, const LaunchEvents& ev) {
+  if (ev.start != nullptr || ev.stop != nullptr)  // events bound to this dispatch
+    hipExtLaunchKernelGGL((k_attn_decode<D, FOLD2>), grid, dim3(64 * kAttnWaves), 0u, s, ev.start, ev.stop, 0u, a);
+  else
+    hipLaunchKernelGGL((k_attn_decode<D, FOLD2>), grid, dim3(64 * kAttnWaves), 0, s, a);
 }
 
-hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, int max_pfx_splits, hipStream_t s) {
+template <int D>
+static void launch_decode_d(const AttnArgs& a, dim3 grid, bool fold2, hipStream_t s, const LaunchEvents& ev) {
+  if (fold2) launch_decode_k<D, true>(a, grid, s, ev);
+  else launch_decode_k<D, false>(a, grid, s, ev);
+}
+
+hipError_t launch_attn_decode(const AttnArgs& a, int n_rows, int grid_splits, int max_pfx_splits, hipStream_t s,
+                              LaunchEvents ev) {
   if (grid_splits < 1 || grid_splits > a.max_splits) return hipErrorInvalidValue;
   dim3 grid(grid_splits, a.Hkv, n_rows);
   const bool fold2 = a.pfx_splits != nullptr && max_pfx_splits > kAttnWaves;
-  if (a.hd == 128) launch_decode_d<128>(a, grid, fold2, s);
-  else if (a.hd == 64) launch_decode_d<64>(a, grid, fold2, s);
+  if (a.hd == 128) launch_decode_d<128>(a, grid, fold2, s, ev);
+  else if (a.hd == 64) launch_decode_d<64>(a, grid, fold2, s, ev);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -27,6 +27,8 @@
 #include <climits>
 #include <utility>
 
+#include <hip/hip_ext.h>
+
 #include "dev.hpp"
 #include "gemm.hpp"
 
@@ -479,7 +481,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 
 // ---------------------------------------------------------------- launcher
 template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL = false>
-static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStream_t s) {
+static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStream_t s, const LaunchEvents& ev) {
   const int n_groups = (a.N / 16 + NT * WN - 1) / (NT * WN);
   dim3 grid(n_groups, ksplit, m_tiles);
   // cross-wave reduction; with X in LDS the same space first holds the X chunks
@@ -492,8 +494,14 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
     if (attr != hipSuccess) return attr;
   }
-  hipLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI, XL>), grid, dim3(64 * (WN * WK + (XL ? 1 : 0))), smem, s,
-                     a);
+  const dim3 block(64 * (WN * WK + (XL ? 1 : 0)));
+  if (ev.start != nullptr || ev.stop != nullptr) {
+    // events bound to this dispatch: they take its start and end times
+    hipExtLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI, XL>), grid, block, static_cast<uint32_t>(smem), s, ev.start,
+                          ev.stop, 0u, a);
+  } else {
+    hipLaunchKernelGGL((k_gemm<MG, NT, WN, WK, PF, EPI, XL>), grid, block, smem, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -513,32 +521,32 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 // for QKV), shape 5 for eight (two per wave) at 8 row groups, QKV and 4 row
 // groups taking the 2 x 2 grid.
 template <int EPI>
-static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s, const LaunchEvents& ev) {
   switch (p.mg) {
     case 1:
-      if (p.nt == 4) return launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
-      if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
-      return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s);
-    case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s);
+      if (p.nt == 4) return launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+      if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+      return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+    case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s, ev);
     case 4:
       if (p.xl) {
-        if (p.wn == 4) return launch_cfg<4, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
-        return launch_cfg<4, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
+        if (p.wn == 4) return launch_cfg<4, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        return launch_cfg<4, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
       }
-      if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s);
-      if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
-      return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
+      if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+      if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+      return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
     default:
       if (p.xl) {
         // (QKV never takes it: its rotary factors would spill)
         if constexpr (EPI != EPI_QKV)
-          if (p.nt == 2) return launch_cfg<8, 2, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s);
-        if (p.wn == 4) return launch_cfg<8, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
-        return launch_cfg<8, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s);
+          if (p.nt == 2) return launch_cfg<8, 2, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        if (p.wn == 4) return launch_cfg<8, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        return launch_cfg<8, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
       }
-      if (p.wn == 2) return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s);
-      if (p.nt == 2) return launch_cfg<8, 2, 1, 4, 2, EPI>(a, p.m_tiles, p.ksplit, s);
-      return launch_cfg<8, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s);
+      if (p.wn == 2) return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+      if (p.nt == 2) return launch_cfg<8, 2, 1, 4, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+      return launch_cfg<8, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
   }
 }
 
@@ -595,12 +603,12 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   return p;
 }
 
-hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s) {
+hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s, LaunchEvents ev) {
   switch (epi) {
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, p, s);
-    case EPI_QKV: return launch_epi<EPI_QKV>(a, p, s);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, s);
-    default: return launch_epi<EPI_LOGITS>(a, p, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(a, p, s, ev);
+    case EPI_QKV: return launch_epi<EPI_QKV>(a, p, s, ev);
+    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, s, ev);
+    default: return launch_epi<EPI_LOGITS>(a, p, s, ev);
   }
 }
 
