@@ -103,16 +103,30 @@ def gateup_bytes(m, R):
     return 2 * m.ffn * m.hidden * 2 + R * m.hidden * 2 + R * m.ffn * 2
 
 
+def gemm_kernel_hash():
+    """First 16 hex digits of the SHA-256 of the projection kernel's own source:
+    the kernel template of k_gemm.hip (up to its launchers) and the headers it
+    uses.  Plan and launcher edits leave it unchanged."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2609_37062_amd", "csrc")
+    k = open(os.path.join(csrc, "k_gemm.hip"), "rb").read()
+    i = k.index(b"template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL>\n__global__")
+    j = k.index(b"// ---------------------------------------------------------------- launcher")
+    h = hashlib.sha256(k[i:j])
+    for f in ("dev.hpp", "gemm.hpp"):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
 def gateup_traffic():
     """Counter-measured HBM bytes per gate/up launch from profiles/, or None when
     the projection kernel's source has changed since the counters were taken."""
-    import hashlib
     try:
         prof = json.load(open(os.path.join(ROOT, "profiles", "gateup_3b_b16_traffic.json")))
-        src = open(os.path.join(ROOT, "paper_2609_37062_amd", "csrc", "k_gemm.hip"), "rb").read()
-    except OSError:
+        kh = gemm_kernel_hash()
+    except (OSError, ValueError):
         return None
-    if hashlib.sha256(src).hexdigest()[:16] != prof.get("k_gemm_source_sha256_16"):
+    if kh != prof.get("k_gemm_kernel_sha256_16"):
         return None
     return prof["traffic_bytes_per_launch"]
 

@@ -235,16 +235,21 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        2048, with hidden at most 4096, and returns VSK_E_UNSUPPORTED for
  *        other passes.  Both paths compute the same values.
  * key 3: launch shape of the per-operation projections for 33..128 rows
- *        (and longer row-tiled passes): 0 (default) for 65 rows or more
- *        shape 5 except for QKV; otherwise one column of eight K-split waves
- *        per workgroup over one 16-column tile (residual and QKV projections)
- *        or two (gate/up, lm_head), and for passes of more than 128 rows
- *        shape 3; 1 one tile everywhere; 2 two tiles everywhere; 3 a 2 x 2
- *        grid of waves over four tiles; 4 the activation chunks staged in
- *        LDS by a ninth wave and shared by eight weight-streaming waves on
- *        four tiles (two for QKV), residual projections with K split over
- *        workgroups; 5 for 65 rows or more (QKV aside) the same staging with
- *        two tiles per wave (eight per workgroup), everything else shape 3.
+ *        (and longer row-tiled passes).  0 (default): with one row tile the
+ *        activation chunks are staged in LDS by a ninth wave and shared by
+ *        eight weight-streaming waves for QKV (two 16-column tiles per
+ *        workgroup), gate/up and lm_head (four; eight, two per wave, for 65
+ *        rows or more), residual projections taking one column of eight
+ *        K-split waves per tile (33..64 rows) or the eight-tile staging with
+ *        K split over workgroups (65..128 rows); passes of more than 128 rows
+ *        take a 2 x 2 wave grid over four tiles for QKV and the eight-tile
+ *        staging elsewhere.  1 one column of K-split waves, one tile, every
+ *        projection; 2 the same with two tiles; 3 the 2 x 2 grid everywhere;
+ *        4 staging with four tiles (two for QKV) everywhere, residual
+ *        projections with K split over workgroups; 5 for 65 rows or more
+ *        (QKV aside) staging with eight tiles, everything else shape 3; 6 the
+ *        default's staging for every projection but the residual ones,
+ *        whatever the row tiling.
  * key 4: shared prefixes of a decode pass (vsk_batch_prefix_info): 1 (the
  *        default) reads each group's prefix blocks once for the group, 0 reads
  *        them once per sequence.

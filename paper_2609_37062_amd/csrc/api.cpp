@@ -531,7 +531,7 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       h->exec_mode = value;
       return VSK_OK;
     case 3:
-      if (value < 0 || value > 5) return fail(h, VSK_E_ARG, "projection shape must be 0..5");
+      if (value < 0 || value > 6) return fail(h, VSK_E_ARG, "projection shape must be 0..6");
       h->gemm_shape = value;
       return VSK_OK;
     case 4:

@@ -510,16 +510,19 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 //          flight (residual projections: N = hidden);
 //  pair    two N tiles per wave, 4 K steps in flight (QKV, gate/up);
 //  wide    four N tiles per wave (lm_head).
-// For 4..8 row groups (shape 0, the default) each workgroup is one column of
-// K-split waves (8; 4 for two tiles of 8 row groups, whose cross-wave sums
-// would not fit 64 KiB of LDS) over one N tile (residual, QKV) or two
-// (gate/up, lm_head): N = hidden then still gives 192-256 workgroups; a
-// row-tiled pass takes shape 3.  8 row groups other than QKV take shape 5's
-// X-in-LDS layout instead.  Shape 1 takes one N tile everywhere, shape 2
-// two, shape 3 is a 2 x 2 wave grid over four N tiles (fewer workgroups, each
-// X chunk feeding four tiles), shape 4 stages X in LDS for four N tiles (two
-// for QKV), shape 5 for eight (two per wave) at 8 row groups, QKV and 4 row
-// groups taking the 2 x 2 grid.
+// For 4..8 row groups the default (shape 0) is, with one row tile: X staged
+// in LDS by a ninth wave for QKV (two N tiles per workgroup), gate/up and
+// lm_head (four; at 8 row groups eight, two per wave), and for the residual
+// projections one column of 8 K-split waves per N tile at 4 row groups (N =
+// hidden then still gives 192-256 workgroups) or the eight-tile LDS layout
+// with K split over workgroups at 8.  A row-tiled pass (more than 128 rows)
+// takes the 2 x 2 wave grid for QKV and the eight-tile LDS layout elsewhere.
+// Shape 1 takes one N tile per wave column everywhere, shape 2 two, shape 3
+// is a 2 x 2 wave grid over four N tiles, shape 4 stages X in LDS for four N
+// tiles (two for QKV) everywhere, shape 5 for eight (two per wave) at 8 row
+// groups with QKV and 4 row groups on the 2 x 2 grid, shape 6 the default's
+// LDS layouts for every projection but the residual ones, whatever the row
+// tiling.
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s, const LaunchEvents& ev) {
   switch (p.mg) {
@@ -562,10 +565,9 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
     if (epi != EPI_RESID) p.nt = epi == EPI_LOGITS ? 4 : 2;
   } else if (p.mg >= 4) {
     const bool wide_n = epi == EPI_SWIGLU || epi == EPI_LOGITS;
-    // a row-tiled pass (more than 128 rows) re-streams the weights once per
-    // row tile: there the 2 x 2 wave grid, each X chunk feeding four N
-    // tiles, is the faster default
-    if ((shape == 0 || shape == 5) && p.mg == 8 && epi != EPI_QKV) {
+    const bool auto_shape = shape == 0;
+    const bool one_tile = p.m_tiles == 1;
+    if ((auto_shape || shape == 5 || shape == 6) && p.mg == 8 && epi != EPI_QKV) {
       // X in LDS, two N tiles per wave: eight N tiles per workgroup, each X
       // chunk read once from L2 for all of them (measured the fastest for 8
       // row groups, one row tile or several)
@@ -573,16 +575,22 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
       p.nt = 2;
       p.wn = 4;
       wk = 2;
-    } else if (shape == 3 || shape == 5 || (shape == 0 && p.m_tiles > 1)) {
+    } else if (shape == 3 || shape == 5 || (auto_shape && !one_tile)) {
+      // a row-tiled pass (more than 128 rows) re-streams the weights once per
+      // row tile: there the 2 x 2 wave grid, each X chunk feeding four N
+      // tiles, is the faster default
       p.nt = 2;
       p.wn = 2;
       wk = 2;
-    } else if (shape == 4) {
-      // X in LDS: four N tiles per workgroup (two for QKV, whose N is small)
+    } else if (shape == 4 || ((shape == 6 || auto_shape) && epi != EPI_RESID)) {
+      // X in LDS: four N tiles per workgroup (two for QKV, whose N is small);
+      // by default for QKV, gate/up and lm_head of one row tile
       p.xl = true;
       p.wn = epi == EPI_QKV ? 2 : 4;
       wk = 8 / p.wn;
     } else {
+      // one column of K-split waves: residual projections of 4 row groups
+      // (N = hidden gives 192-256 workgroups)
       p.nt = shape == 1 ? 1 : shape == 2 ? 2 : (wide_n ? 2 : 1);
       wk = p.mg == 8 && p.nt == 2 ? 4 : 8;
     }

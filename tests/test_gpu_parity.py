@@ -78,7 +78,7 @@ def test_mid_attention_splits(bps):
 
 
 @pytest.mark.parametrize("B,shape", [(40, 0), (40, 1), (40, 2), (40, 3), (40, 4), (40, 5),
-                                     (100, 0), (100, 1), (100, 2), (100, 3), (100, 4), (100, 5),
+                                     (100, 0), (100, 1), (100, 2), (100, 3), (100, 4), (100, 5), (100, 6), (40, 6),
                                      (130, 0), (130, 4), (130, 5)])
 def test_mid_projection_shapes(B, shape):
     """Every launch shape of the projections for 3 and 7 row groups (one or
