@@ -239,9 +239,9 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        activation chunks are staged in LDS by a ninth wave and shared by
  *        eight weight-streaming waves for QKV (two 16-column tiles per
  *        workgroup), gate/up and lm_head (four; eight, two per wave, for 65
- *        rows or more), residual projections taking one column of eight
- *        K-split waves per tile (33..64 rows) or the eight-tile staging with
- *        K split over workgroups (65..128 rows); passes of more than 128 rows
+ *        rows or more), residual projections taking the four-tile (33..64
+ *        rows) or eight-tile (65..128 rows) staging with K split over
+ *        workgroups (key 5); passes of more than 128 rows
  *        take a 2 x 2 wave grid over four tiles for QKV and the eight-tile
  *        staging elsewhere.  1 one column of K-split waves, one tile, every
  *        projection; 2 the same with two tiles; 3 the 2 x 2 grid everywhere;
@@ -254,10 +254,11 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        default) reads each group's prefix blocks once for the group, 0 reads
  *        them once per sequence.
  * key 5: residual projections (O, down) of passes of at most 128 rows: the
- *        workgroup count their K split aims for (1..4096), or 0 / -1 (the
- *        default) for no split.  Split products are added to the residual in
- *        split order by the RMSNorm that follows (measured: no faster than
- *        one workgroup per output tile, which is why it is off).
+ *        workgroup count their K split aims for (1..4096); 0 (the default):
+ *        192 workgroups in the activation-staged layout at 33..64 rows, 384
+ *        at 65..128, no split in the other layouts (1..32 rows: measured no
+ *        faster); -1: no split.  Split products are added to the residual in
+ *        split order by the RMSNorm that follows.
  * key 6: rows of a sequence with several new rows (a prefill chunk): 1 (the
  *        default) one causal work item per run of up to 128 (row, query
  *        head) pairs reading each key block once for all of them; 0 one

@@ -823,7 +823,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   pf.out = fa;
   pf.out_Rg = Rg;
 
-  const int rt = h.resid_target < 0 ? 0 : h.resid_target > 0 ? h.resid_target : kResidTargetWgs;
+  const int rt = h.resid_target;  // -1 no split, 0 the layout's default, else the target
   const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape);
   const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape, rt);
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape);

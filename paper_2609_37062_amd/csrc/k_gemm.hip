@@ -513,9 +513,8 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 // For 4..8 row groups the default (shape 0) is, with one row tile: X staged
 // in LDS by a ninth wave for QKV (two N tiles per workgroup), gate/up and
 // lm_head (four; at 8 row groups eight, two per wave), and for the residual
-// projections one column of 8 K-split waves per N tile at 4 row groups (N =
-// hidden then still gives 192-256 workgroups) or the eight-tile LDS layout
-// with K split over workgroups at 8.  A row-tiled pass (more than 128 rows)
+// projections the four-tile (4 row groups) or eight-tile (8) LDS layout
+// with K split over workgroups.  A row-tiled pass (more than 128 rows)
 // takes the 2 x 2 wave grid for QKV and the eight-tile LDS layout elsewhere.
 // Shape 1 takes one N tile per wave column everywhere, shape 2 two, shape 3
 // is a 2 x 2 wave grid over four N tiles, shape 4 stages X in LDS for four N
@@ -582,15 +581,15 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
       p.nt = 2;
       p.wn = 2;
       wk = 2;
-    } else if (shape == 4 || ((shape == 6 || auto_shape) && epi != EPI_RESID)) {
+    } else if (shape == 4 || ((shape == 6 || auto_shape) && epi != EPI_RESID) || auto_shape) {
       // X in LDS: four N tiles per workgroup (two for QKV, whose N is small);
-      // by default for QKV, gate/up and lm_head of one row tile
+      // the default for every projection of one row tile at 4 row groups
+      // (the residual ones with K split over workgroups)
       p.xl = true;
       p.wn = epi == EPI_QKV ? 2 : 4;
       wk = 8 / p.wn;
     } else {
-      // one column of K-split waves: residual projections of 4 row groups
-      // (N = hidden gives 192-256 workgroups)
+      // one column of K-split waves (N = hidden gives 192-256 workgroups)
       p.nt = shape == 1 ? 1 : shape == 2 ? 2 : (wide_n ? 2 : 1);
       wk = p.mg == 8 && p.nt == 2 ? 4 : 8;
     }
@@ -599,8 +598,13 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   p.n_groups = (N / 16 * 16 + cols_per_group - 1) / cols_per_group;
   // a residual projection of one row tile splits K until the workgroups
   // reach resid_target, keeping at least 4 K steps per wave; k_resid_norm
-  // then adds the splits' products into the residual
-  const int target = p.xl ? std::max(resid_target, 384) : resid_target;
+  // then adds the splits' products into the residual.  With X in LDS the
+  // default target is 192 workgroups at 4 row groups (4 splits at hidden
+  // 3072) and 384 at 8 (measured best of 96-384 and 128-384).
+  const int target = resid_target < 0    ? 0
+                     : resid_target > 0  ? resid_target
+                     : p.xl              ? (p.mg == 4 ? 192 : 384)
+                                         : kResidTargetWgs;
   if (epi == EPI_RESID && target > 0 && p.m_tiles == 1) {
     const int Kt = K / 32;
     int ks = std::min({(target + p.n_groups - 1) / p.n_groups, kMaxResidSplits, std::max(1, Kt / (4 * wk))});

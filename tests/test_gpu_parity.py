@@ -99,11 +99,11 @@ def test_mid_projection_shapes(B, shape):
     print(st)
 
 
-@pytest.mark.parametrize("B,target", [(9, -1), (9, 4096), (40, -1), (40, 4096), (100, 64), (100, 4096)])
+@pytest.mark.parametrize("B,target", [(9, -1), (9, 4096), (40, -1), (40, 0), (40, 4096), (100, -1), (100, 64), (100, 4096)])
 def test_mid_residual_k_splits(B, target):
     """Residual projections with K split over workgroups (the splits added
     into the residual, in split order, by the RMSNorm that follows): no split
-    (-1), a few, and the most the rule allows."""
+    (-1), the default (0), a few, and the most the rule allows."""
     from paper_2609_37062_amd.runner import DeviceRun
     ctx = np.random.default_rng(200 + B).integers(0, 400, size=B)
     w = decode_workload(MID, ctx, seed=17, name=f"mid-rsplit-b{B}-t{target}")
