@@ -114,12 +114,16 @@ __device__ __forceinline__ void pair_scores(const u32x4 (&qf)[D / 32], const u32
   mx = fmaxf(mx, shfl_xor(mx, 16));
   mx = fmaxf(mx, shfl_xor(mx, 32));
   const float m_new = fmaxf(m, mx);
-  alpha = m_new == -INFINITY ? 1.f : exp2f(m - m_new);
+  // v_exp_f32 directly: arguments are <= 0, and a probability below 2^-126
+  // (flushed to 0) is negligible beside the maximum's 1; both results are
+  // computed and selected, so there is no branch per exponential
+  const bool none = m_new == -INFINITY;
+  alpha = none ? 1.f : __builtin_amdgcn_exp2f(m - m_new);
   float p[8], ps = 0.f;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    p[r] = m_new == -INFINITY ? 0.f : exp2f(s0[r] - m_new);
-    p[4 + r] = m_new == -INFINITY ? 0.f : exp2f(s1[r] - m_new);
+    p[r] = none ? 0.f : __builtin_amdgcn_exp2f(s0[r] - m_new);
+    p[4 + r] = none ? 0.f : __builtin_amdgcn_exp2f(s1[r] - m_new);
   }
 #pragma unroll
   for (int j = 0; j < 8; ++j) ps += p[j];
