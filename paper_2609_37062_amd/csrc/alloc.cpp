@@ -233,7 +233,7 @@ void plan_prefill_items(BatchHost& b, int32_t group_size) {
   b.pre_items.clear();
   b.dec_rows.clear();
   if (b.max_q_len <= 1) return;
-  const int32_t per = std::max(1, kPfxCols / group_size);
+  const int32_t per = std::max(1, kPreCols / group_size);
   for (int32_t i = 0; i < b.n_seqs; ++i) {
     const int32_t r0 = b.cu_q[i], r1 = b.cu_q[i + 1];
     if (r1 - r0 == 1) {

@@ -86,20 +86,22 @@ struct BatchHost {
 };
 
 // A pass with prefill rows (a sequence with more than one new row): each
-// such sequence's rows are cut into runs of at most kPfxCols / group_size
+// such sequence's rows are cut into runs of at most kPreCols / group_size
 // rows (one causal-attention work item each); the rows of one-row sequences
 // are listed for the decode attention.  A pass of one-row sequences only
 // gets no items.
 void plan_prefill_items(BatchHost& b, int32_t group_size);
 
-// Columns (row, query head) of one shared-prefix work item: 8 waves x 16.
-constexpr int32_t kPfxCols = 128;
+// Columns (row, query head) of one shared-prefix work item: 4 tiles of 16,
+// each walked by two waves; of one prefill work item: 8 tiles of 16.
+constexpr int32_t kPfxCols = 64;
+constexpr int32_t kPreCols = 128;
 // Most prefix splits of one group, and the largest split (blocks).
 constexpr int32_t kMaxPfxSplits = 16;
 constexpr int32_t kMaxPfxBps = 512;
 // Split every group's prefix so that the work items of all groups and KV
 // heads come to about target_wgs workgroups (at least 2 blocks per split).
-void plan_prefix_items(BatchHost& b, int32_t group_size, int32_t n_kv_heads, int32_t target_wgs = 128);
+void plan_prefix_items(BatchHost& b, int32_t group_size, int32_t n_kv_heads, int32_t target_wgs = 192);
 
 // Smallest common prefix (in blocks) worth reading once for a group.
 constexpr int32_t kMinSharedPrefixBlocks = 4;

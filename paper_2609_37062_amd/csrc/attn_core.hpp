@@ -111,8 +111,7 @@ __device__ __forceinline__ void pair_scores(const u32x4 (&qf)[D / 32], const u32
     s1[r] = vb ? s1[r] * sc : -INFINITY;
     mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
   }
-  mx = fmaxf(mx, shfl_xor(mx, 16));
-  mx = fmaxf(mx, shfl_xor(mx, 32));
+  mx = max_xor32(max_xor16(mx));
   const float m_new = fmaxf(m, mx);
   // v_exp_f32 directly: arguments are <= 0, and a probability below 2^-126
   // (flushed to 0) is negligible beside the maximum's 1; both results are
@@ -127,8 +126,7 @@ __device__ __forceinline__ void pair_scores(const u32x4 (&qf)[D / 32], const u32
   }
 #pragma unroll
   for (int j = 0; j < 8; ++j) ps += p[j];
-  ps += shfl_xor(ps, 16);
-  ps += shfl_xor(ps, 32);
+  ps = add_xor32(add_xor16(ps));
   l = l * alpha + ps;
   m = m_new;
 #pragma unroll

@@ -107,6 +107,28 @@ __device__ __forceinline__ int opaque_tid() {
 }
 
 __device__ __forceinline__ float shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
+
+// A value combined with lane l ^ 16 (or l ^ 32) through the gfx950 lane
+// swaps (v_permlane16_swap / v_permlane32_swap: VALU, no LDS round trip).
+// Swapping v with itself leaves each lane the pair {v[l], v[l ^ 16]} (resp.
+// l ^ 32) in some order; max and + are symmetric, so both lanes of a pair
+// get the same bits, as with a shuffle.
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float add_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float add_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 __device__ __forceinline__ int shfl_xor(int v, int m) { return __shfl_xor(v, m, 64); }
 
 // (value, index) candidate for greedy argmax: larger value wins, equal values
