@@ -29,16 +29,15 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) { return f2bf(l
 // double -> bf16 bits, round to nearest even.  Rounds to float first; that
 // can only mislead the second rounding when the float lands exactly on a bf16
 // midpoint from a double that was not one, which is resolved toward the double.
+// (All three candidates are computed and one is selected: no branch.)
 __device__ __forceinline__ uint32_t d2bf(double d) {
   const float f = static_cast<float>(d);
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return ((u >> 16) | 0x40u) & 0xffffu;
-  if ((u & 0xffffu) == 0x8000u && static_cast<double>(f) != d) {
-    const bool away = fabs(d) > fabs(static_cast<double>(f));
-    return ((u >> 16) + (away ? 1u : 0u)) & 0xffffu;
-  }
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t quiet_nan = ((u >> 16) | 0x40u) & 0xffffu;
+  const bool tie = (u & 0xffffu) == 0x8000u && static_cast<double>(f) != d;
+  const uint32_t resolved = ((u >> 16) + (fabs(d) > fabs(static_cast<double>(f)) ? 1u : 0u)) & 0xffffu;
+  return (u & 0x7fffffffu) > 0x7f800000u ? quiet_nan : tie ? resolved : rounded;
 }
 
 // D(16x16,f32) += A(16x32) * B(32x16), bf16 operands, 8 per lane.

@@ -135,10 +135,15 @@ __global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ 
 // in double, added in a fixed order, the product in double and rounded once.
 // Every load of a thread (x, all splits, g) is issued before the first add,
 // so the row costs one memory round trip, not one per split.
+// NS > 0: exactly NS splits (compile-time: every load unconditional); NS = 0:
+// `splits` of them, at most kResidNormMaxSplits.
 constexpr int kResidNormMaxSplits = 8;
+template <int NS>
 __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ x, const float* __restrict__ y, int splits,
                                                      int R, int H, const uint16_t* __restrict__ g, float eps,
                                                      uint16_t* __restrict__ hg, int Rg) {
+  if constexpr (NS > 0) splits = NS;
+  constexpr int kMax = NS > 0 ? NS : kResidNormMaxSplits;
   __shared__ double s_ss[16];
   const int r = blockIdx.x;
   const int c = threadIdx.x * 8;
@@ -150,10 +155,10 @@ __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ x, cons
   if (on) {
     float4 a = *reinterpret_cast<const float4*>(xr);
     float4 b = *reinterpret_cast<const float4*>(xr + 4);
-    float4 ya[kResidNormMaxSplits], yb[kResidNormMaxSplits];
+    float4 ya[kMax], yb[kMax];
 #pragma unroll
-    for (int sp = 0; sp < kResidNormMaxSplits; ++sp) {
-      if (sp < splits) {
+    for (int sp = 0; sp < kMax; ++sp) {
+      if (NS > 0 || sp < splits) {
         const float* yr = y + (static_cast<size_t>(sp) * R + r) * H + c;
         ya[sp] = *reinterpret_cast<const float4*>(yr);
         yb[sp] = *reinterpret_cast<const float4*>(yr + 4);
@@ -162,8 +167,8 @@ __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ x, cons
     if (g != nullptr) gv = *reinterpret_cast<const u32x4*>(g + c);
     float4 sa = ya[0], sb = yb[0];
 #pragma unroll
-    for (int sp = 1; sp < kResidNormMaxSplits; ++sp) {
-      if (sp < splits) {
+    for (int sp = 1; sp < kMax; ++sp) {
+      if (NS > 0 || sp < splits) {
         sa.x += ya[sp].x; sa.y += ya[sp].y; sa.z += ya[sp].z; sa.w += ya[sp].w;
         sb.x += yb[sp].x; sb.y += yb[sp].y; sb.z += yb[sp].z; sb.w += yb[sp].w;
       }
@@ -198,7 +203,12 @@ hipError_t launch_resid_norm(float* x, const float* y, int splits, int R, int H,
                              uint16_t* hg, int Rg, hipStream_t s) {
   if (H % 8 != 0 || H > 8192 || splits < 1 || splits > kResidNormMaxSplits) return hipErrorInvalidValue;
   const int threads = (H / 8 + 63) / 64 * 64;
-  hipLaunchKernelGGL(k_resid_norm, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg);
+  switch (splits) {
+    case 2: hipLaunchKernelGGL(k_resid_norm<2>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg); break;
+    case 4: hipLaunchKernelGGL(k_resid_norm<4>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg); break;
+    case 8: hipLaunchKernelGGL(k_resid_norm<8>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg); break;
+    default: hipLaunchKernelGGL(k_resid_norm<0>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg);
+  }
   return hipGetLastError();
 }
 
