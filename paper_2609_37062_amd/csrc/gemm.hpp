@@ -15,7 +15,7 @@ struct GemmArgs {
   int R;        // valid rows
   int Rg;       // 16-row groups of the X frag buffer
   float* x;          // RESID: fp32 residual [R][N], x += y
-  double* ssq_out;   // RESID: partial sums of x^2 of the updated rows [n_groups][R]
+  double* ssq_out;   // RESID: partial sums of x^2 of the updated rows [R][n_groups]
   uint16_t* out;  // QKV: q [R][Nq]; SWIGLU: frags (out_Rg); LOGITS: logits [R][N]
   int out_Rg;
   uint16_t* pool;  // QKV: KV pool

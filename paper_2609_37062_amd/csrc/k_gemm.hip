@@ -361,7 +361,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
         for (int w2 = 1; w2 < WN; ++w2) ss += s_ss[w2][g][l];
         const int row = 16 * (g0 + g) + l;
-        if (row < a.R) a.ssq_out[static_cast<size_t>(ng) * a.R + row] = ss;
+        if (row < a.R) a.ssq_out[static_cast<size_t>(row) * gridDim.x + ng] = ss;  // [row][workgroup]
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {

@@ -11,7 +11,7 @@ namespace vsk {
 // ---------------------------------------------------------------- embedding
 // x[r][:] = float(E[ids[r]][:]) (fp32 residual), plus what the first QKV
 // projection consumes: frags of bf16(x * g) and per-16-column partial sums
-// of x^2 (ssq[c/16][r]).  Token ids outside [0, V) give a zero row.
+// of x^2 (one per row: ssq[r]).  Token ids outside [0, V) give a zero row.
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, const int32_t* __restrict__ ids,
                                                int H, int V, float* __restrict__ x, double* __restrict__ ssq) {
   __shared__ double s_ss[4];
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ 
   for (int p0 = threadIdx.x; p0 < parts; p0 += 256) {
     double v[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = p0 + 64 * q < parts ? ssq[static_cast<size_t>(p0 + 64 * q) * R + r] : 0.0;
+    for (int q = 0; q < 4; ++q) v[q] = p0 + 64 * q < parts ? ssq[static_cast<size_t>(r) * parts + p0 + 64 * q] : 0.0;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (p0 + 64 * q < parts) s += v[q];
