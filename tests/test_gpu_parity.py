@@ -130,7 +130,7 @@ def test_mid_shared_prefix():
 @pytest.mark.parametrize("shared,bps", [(1, 0), (0, 0), (1, 8)])
 def test_mid_prefix_groups(shared, bps):
     """Two shared-prefix groups (160 and 96 tokens, one of 45 members so a
-    group spans several 128-column work items) beside sequences of no group;
+    group spans several 64-column work items) beside sequences of no group;
     prefixes read once per group (shared 1) or once per sequence (0)."""
     from paper_2609_37062_amd.runner import DeviceRun
     rng = np.random.default_rng(21)
@@ -149,6 +149,40 @@ def test_mid_prefix_groups(shared, bps):
     lg2, ids2 = d.results()
     assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
     st, *_ = _check(w, lg, ids, [0, 1, 3, 20, 44, 45, 47, 49, 50, 53])
+    print(st)
+
+
+@pytest.mark.parametrize("bps", [0, 8])
+def test_mid_pair_boundaries(bps):
+    """Decode rows whose key counts fall on and around 16-token block and
+    32-key step boundaries (a wave's last step may hold one real block and a
+    masked one, a block may end the sequence exactly), every unwritten pool
+    slot holding a NaN pattern."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    kv = np.array([1, 15, 16, 17, 31, 32, 33, 48, 49, 63, 64, 65, 96, 129])
+    w = decode_workload(MID, kv - 1, seed=23, name=f"mid-pairs-{bps}")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(0, bps)
+    d.step()
+    lg, ids = d.results()
+    st, *_ = _check(w, lg, ids)
+    print(st)
+
+
+def test_mid_prefix_odd_blocks():
+    """Shared prefixes of an odd number of blocks (11 and 5): the two waves of
+    a prefix tile split an odd number of blocks, the last step unpaired."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    suf = np.random.default_rng(27).integers(0, 40, size=12 + 3 + 2)
+    w = prefix_groups_workload(MID, [(176, 12), (80, 3)], suf, seed=27, name="mid-groups-odd")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    pfx, ng = d.eng.batch_prefix_info()
+    assert ng == 2 and (pfx[:12] == 11).all() and (pfx[12:15] == 5).all() and not pfx[15:].any()
+    d.step()
+    lg, ids = d.results()
+    st, *_ = _check(w, lg, ids)
     print(st)
 
 
