@@ -116,14 +116,14 @@ inline int attn_splits(int kv_len, int bps) {
   const int nb = (kv_len + kBlock - 1) / kBlock;
   return (nb + bps - 1) / bps;
 }
-// Default split size (4-wave work items, about three per compute unit).
-// With few (row, KV head) pairs long contexts are cut into 256-token splits
-// to spread them over the compute units; once the pairs alone fill the
-// chip, 1024-token splits still cut the longest contexts of a heavy-tailed
-// batch (whose single work item would otherwise finish last) while most
-// rows need no merge (measured: batch 16 at 512-1024 tokens, batch 128 at
-// lognormal lengths).
-inline int attn_auto_bps(int n_rows, int n_kv_heads) { return n_rows * n_kv_heads >= 256 ? 64 : 16; }
+// Default split size (4-wave work items, two per compute unit).  With few
+// (row, KV head) pairs long contexts are cut into 512-token splits to spread
+// them over the compute units; once the pairs alone fill the chip,
+// 1024-token splits still cut the longest contexts of a heavy-tailed batch
+// (whose single work item would otherwise finish last) while most rows need
+// no merge (measured: batch 16 at 512-1024 tokens, batch 128 at lognormal
+// lengths).
+inline int attn_auto_bps(int n_rows, int n_kv_heads) { return n_rows * n_kv_heads >= 256 ? 64 : 32; }
 
 struct Handle {
   vsk_model_cfg cfg{};
