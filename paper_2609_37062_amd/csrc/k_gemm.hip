@@ -532,8 +532,10 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
     case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s, ev);
     case 4:
       if (p.xl) {
-        if (p.wn == 4) return launch_cfg<4, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
-        return launch_cfg<4, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        // weight rings of 4 and 2 K steps: shallower rings measured faster
+        // with X in LDS (16 steps: batch-64 pass 3.06 ms, these 2.90)
+        if (p.wn == 4) return launch_cfg<4, 1, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        return launch_cfg<4, 1, 2, 4, 2, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
       }
       if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
@@ -542,9 +544,9 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       if (p.xl) {
         // (QKV never takes it: its rotary factors would spill)
         if constexpr (EPI != EPI_QKV)
-          if (p.nt == 2) return launch_cfg<8, 2, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+          if (p.nt == 2) return launch_cfg<8, 2, 4, 2, 2, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         if (p.wn == 4) return launch_cfg<8, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
-        return launch_cfg<8, 1, 2, 4, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        return launch_cfg<8, 1, 2, 4, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
       }
       if (p.wn == 2) return launch_cfg<8, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       if (p.nt == 2) return launch_cfg<8, 2, 1, 4, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
