@@ -506,7 +506,7 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 }
 
 // Launch shapes.  mg = 16-row groups of X per tile.  For mg == 1:
-//  narrow  one 16-column N tile per wave, 8 K-split waves, 8 K steps in
+//  narrow  one 16-column N tile per wave, 8 K-split waves, 4 K steps in
 //          flight (residual projections: N = hidden);
 //  pair    two N tiles per wave, 4 K steps in flight (QKV, gate/up);
 //  wide    four N tiles per wave (lm_head).
@@ -528,7 +528,7 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
     case 1:
       if (p.nt == 4) return launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
-      return launch_cfg<1, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+      return launch_cfg<1, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
     case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s, ev);
     case 4:
       if (p.xl) {
