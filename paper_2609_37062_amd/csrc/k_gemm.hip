@@ -534,6 +534,8 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       if (p.xl) {
         // weight rings of 4 and 2 K steps: shallower rings measured faster
         // with X in LDS (16 steps: batch-64 pass 3.06 ms, these 2.90)
+        if constexpr (EPI == EPI_LOGITS)
+          if (p.nt == 2) return launch_cfg<4, 2, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         if (p.wn == 4) return launch_cfg<4, 1, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         return launch_cfg<4, 1, 2, 4, 2, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
       }
@@ -590,6 +592,10 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
       p.xl = true;
       p.wn = epi == EPI_QKV ? 2 : 4;
       wk = 8 / p.wn;
+      // lm_head (N = vocab: workgroups to spare) at 4 row groups: two N
+      // tiles per wave, half the X reads per weight byte (170 -> 152 us at
+      // batch 64)
+      if (epi == EPI_LOGITS && p.mg == 4) p.nt = 2;
     } else {
       // one column of K-split waves (N = hidden gives 192-256 workgroups)
       p.nt = shape == 1 ? 1 : shape == 2 ? 2 : (wide_n ? 2 : 1);
