@@ -229,10 +229,9 @@ void plan_prefix_items(BatchHost& b, int32_t group_size, int32_t n_kv_heads, int
   }
 }
 
-void plan_prefill_items(BatchHost& b, int32_t group_size) {
+void plan_prefill_items(BatchHost& b, int32_t group_size, int32_t block) {
   b.pre_items.clear();
   b.dec_rows.clear();
-  if (b.max_q_len <= 1) return;
   const int32_t per = std::max(1, kPreCols / group_size);
   for (int32_t i = 0; i < b.n_seqs; ++i) {
     const int32_t r0 = b.cu_q[i], r1 = b.cu_q[i + 1];
@@ -245,6 +244,9 @@ void plan_prefill_items(BatchHost& b, int32_t group_size) {
       b.pre_items.insert(b.pre_items.end(), it, it + 3);
     }
   }
+  // longest remaining walk first, ties in row order
+  auto walk = [&](int32_t r) { return (b.pos[r] + block) / block - b.pfx_blocks[r]; };
+  std::stable_sort(b.dec_rows.begin(), b.dec_rows.end(), [&](int32_t x, int32_t y) { return walk(x) > walk(y); });
 }
 
 void find_shared_prefixes(BatchHost& b, int32_t block, int32_t min_blocks) {

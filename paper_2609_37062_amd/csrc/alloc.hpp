@@ -81,16 +81,18 @@ struct BatchHost {
   int32_t n_pfx_items() const { return static_cast<int32_t>(pfx_items.size() / 5); }
   // Attention work of a pass with prefill rows (plan_prefill_items)
   std::vector<int32_t> pre_items;    // [n][3]: sequence, first row, rows -- runs of a sequence's new rows
-  std::vector<int32_t> dec_rows;     // rows of one-row sequences
+  std::vector<int32_t> dec_rows;     // rows of one-row sequences, longest walk first
   int32_t n_pre_items() const { return static_cast<int32_t>(pre_items.size() / 3); }
 };
 
-// A pass with prefill rows (a sequence with more than one new row): each
-// such sequence's rows are cut into runs of at most kPreCols / group_size
-// rows (one causal-attention work item each); the rows of one-row sequences
-// are listed for the decode attention.  A pass of one-row sequences only
-// gets no items.
-void plan_prefill_items(BatchHost& b, int32_t group_size);
+// Attention work items.  Each sequence with more than one new row has its
+// rows cut into runs of at most kPreCols / group_size rows (one
+// causal-attention work item each).  The rows of one-row sequences (every
+// row of a decode pass) are listed for the decode attention, ordered by the
+// blocks each reads after its shared prefix, most first (ties in row order):
+// the decode grid dispatches its rows in that order, so the longest walks
+// start first instead of finishing last.
+void plan_prefill_items(BatchHost& b, int32_t group_size, int32_t block);
 
 // Columns (row, query head) of one shared-prefix work item: 4 tiles of 16,
 // each walked by two waves; of one prefill work item: 8 tiles of 16.

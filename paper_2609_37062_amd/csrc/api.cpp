@@ -339,7 +339,7 @@ int vsk_batch_build(vsk_handle* h, const int64_t* seqs_host, const int32_t* q_le
   int st = build_batch(h->alloc, seqs_host, q_lens_host, n_seqs, b, h->err);
   if (st != VSK_OK) return st;
   plan_prefix_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads, h->cfg.n_kv_heads);
-  plan_prefill_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads);
+  plan_prefill_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads, kBlock);
   h->bh = std::move(b);
   h->batch_built = true;
   h->batch_uploaded = false;
@@ -880,6 +880,9 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
       aa.rows = b.dec_rows;
       if (b.n_dec_rows > 0)
         TRY(probed(4, [&](LaunchEvents ev) { return launch_attn_decode(aa, b.n_dec_rows, dec_splits, pfx_fold, s, ev); }));
+    } else if (b.n_pre_items == 0) {
+      aa.rows = b.dec_rows;  // every row, longest walk first
+      TRY(probed(4, [&](LaunchEvents ev) { return launch_attn_decode(aa, b.n_dec_rows, dec_splits, pfx_fold, s, ev); }));
     } else {
       aa.rows = nullptr;
       TRY(probed(4, [&](LaunchEvents ev) { return launch_attn_decode(aa, R, dec_splits, pfx_fold, s, ev); }));
