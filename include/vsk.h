@@ -237,8 +237,9 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  * key 3: launch shape of the per-operation projections for 33..128 rows
  *        (and longer row-tiled passes).  0 (default): with one row tile the
  *        activation chunks are staged in LDS by a ninth wave and shared by
- *        eight weight-streaming waves for QKV (two 16-column tiles per
- *        workgroup), gate/up and lm_head (four; eight, two per wave, for 65
+ *        eight weight-streaming waves for QKV (K split over workgroups in
+ *        the residual projections' staging, key 7; unsplit, two 16-column
+ *        tiles per workgroup), gate/up and lm_head (four; eight, two per wave, for 65
  *        rows or more), residual projections taking the four-tile (33..64
  *        rows) or eight-tile (65..128 rows) staging with K split over
  *        workgroups (key 5); passes of more than 128 rows
@@ -262,7 +263,12 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  * key 6: rows of a sequence with several new rows (a prefill chunk): 1 (the
  *        default) one causal work item per run of up to 128 (row, query
  *        head) pairs reading each key block once for all of them; 0 one
- *        work item per row, as for decode rows. */
+ *        work item per row, as for decode rows.
+ * key 7: the QKV projection of passes of 33..128 rows: the workgroup count
+ *        its K split aims for (1..4096); 0 (the default): 192; -1: no split
+ *        (two 16-column tiles per workgroup with the epilogue in the
+ *        projection).  Split products are added in split order by a kernel
+ *        that then applies rotary and writes q and the KV slots. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

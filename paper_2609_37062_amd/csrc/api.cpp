@@ -74,7 +74,9 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   w.ssq = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
   w.ssq_c = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
   // residual projections with K split over workgroups: one product per split
-  w.ypart = o; o = align_up(o + static_cast<size_t>(kMaxResidSplits) * std::min(max_rows, 128) * H * 4);
+  // (and the QKV projection's, N = Nq + 2 Nkv)
+  const size_t y_cols = std::max<size_t>(H, static_cast<size_t>(Nq) + 2 * static_cast<size_t>(c.n_kv_heads) * c.head_dim);
+  w.ypart = o; o = align_up(o + static_cast<size_t>(kMaxResidSplits) * std::min(max_rows, 128) * y_cols * 4);
   // lm_head argmax partials: n_groups x rows
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
@@ -547,6 +549,11 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
         return fail(h, VSK_E_ARG, "residual split target must be -1 (no split), 0 (default) or 1..4096");
       h->resid_target = value;
       return VSK_OK;
+    case 7:
+      if (value < -1 || value > 4096)
+        return fail(h, VSK_E_ARG, "QKV split target must be -1 (no split), 0 (default) or 1..4096");
+      h->qkv_target = value;
+      return VSK_OK;
     default:
       return fail(h, VSK_E_ARG, "unknown tuning key");
   }
@@ -825,6 +832,13 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
 
   const int rt = h.resid_target;  // -1 no split, 0 the layout's default, else the target
   const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape);
+  // QKV of one row tile at 4 or 8 row groups: K split over workgroups of
+  // the residual projections' layout (4 or 8 N tiles each instead of 2, so
+  // each activation chunk staged in LDS feeds two or four times the weight
+  // bytes), the products added by k_qkv_reduce, which applies the epilogue
+  GemmPlan p_qkv_split;
+  if (h.qkv_target >= 0 && p_qkv.mg >= 4 && p_qkv.m_tiles == 1)
+    p_qkv_split = plan_gemm(Nq + 2 * Nkv, H, R, EPI_RESID, h.gemm_shape, h.qkv_target > 0 ? h.qkv_target : kQkvTargetWgs);
   const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape, rt);
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape);
   const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape, rt);
@@ -868,7 +882,14 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     ga.ssq_out = nullptr;
     ga.out = q;
     ga.layer = l;
-    TRY(probed(2, [&](LaunchEvents ev) { return launch_gemm(ga, p_qkv, EPI_QKV, s, ev); }));
+    if (p_qkv_split.ksplit > 1) {
+      ga.ypart = ypart;
+      TRY(probed(2, [&](LaunchEvents ev) { return launch_gemm(ga, p_qkv_split, EPI_RESID, s, ev); }));
+      TRY(launch_qkv_reduce(ga, p_qkv_split.ksplit, s));
+      ga.ypart = nullptr;
+    } else {
+      TRY(probed(2, [&](LaunchEvents ev) { return launch_gemm(ga, p_qkv, EPI_QKV, s, ev); }));
+    }
     aa.layer = l;
     if (cascade) {
       ap.layer = l;

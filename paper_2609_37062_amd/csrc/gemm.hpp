@@ -40,6 +40,7 @@ struct GemmPlan {
 
 constexpr int kMaxResidSplits = 8;
 constexpr int kResidTargetWgs = 0;  // default split-K target of the residual projections (0: no split)
+constexpr int kQkvTargetWgs = 192;  // default split-K target of QKV at 4..8 row groups
 
 // shape: launch shape for 4 or 8 row groups (0 default; see k_gemm.hip)
 // resid_target: workgroups a residual projection's K split aims for (-1: no
@@ -47,5 +48,8 @@ constexpr int kResidTargetWgs = 0;  // default split-K target of the residual pr
 // kResidTargetWgs)
 GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0, int resid_target = 0);
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s, LaunchEvents ev = {});
+// QKV with K split: add the `splits` products in a.ypart and apply the QKV
+// epilogue (a as for the QKV projection, with N = Nq + 2 Nkv).
+hipError_t launch_qkv_reduce(const GemmArgs& a, int splits, hipStream_t s);
 
 }  // namespace vsk

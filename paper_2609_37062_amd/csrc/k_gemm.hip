@@ -36,6 +36,46 @@ namespace vsk {
 
 __device__ __forceinline__ float silu_f(float v) { return v / (1.0f + expf(-v)); }
 
+// The QKV epilogue of one row and four consecutive packed output columns
+// n0..n0+3 (n0 a multiple of 4): rotary on q and k heads with the factors of
+// packed rows n0, n0 + 2 (cs0, cs1), q to the bf16 buffer, k and v into this
+// layer's KV slot `sl` of the row.
+__device__ __forceinline__ void qkv_store(const GemmArgs& a, int row, int n0, const f32x4 v, int sl, float2 cs0,
+                                          float2 cs1) {
+  const int hd = a.hd, half = hd >> 1;
+  const int blk = sl >> 4, t = sl & 15;
+  if (n0 < a.Nq + a.Nkv) {
+    const int ph = n0 % hd;          // packed row inside the head (multiple of 4)
+    const int hb = n0 - ph;          // first packed row of the head
+    const int j0 = ph >> 1;          // dims j0, j0+half, j0+1, j0+1+half
+    const float y0 = v[0] * cs0.x - v[1] * cs0.y;
+    const float y1 = v[1] * cs0.x + v[0] * cs0.y;
+    const float y2 = v[2] * cs1.x - v[3] * cs1.y;
+    const float y3 = v[3] * cs1.x + v[2] * cs1.y;
+    if (n0 < a.Nq) {
+      uint16_t* q = a.out + static_cast<size_t>(row) * a.Nq + hb;
+      q[j0] = f2bf(y0);
+      q[j0 + half] = f2bf(y1);
+      q[j0 + 1] = f2bf(y2);
+      q[j0 + 1 + half] = f2bf(y3);
+    } else {
+      const int hk = (hb - a.Nq) / hd;
+      uint16_t* kb =
+          a.pool + ((((static_cast<size_t>(a.layer) * 2 + 0) * a.n_blocks + blk) * a.Hkv + hk) * kBlock * hd);
+      kb[kv_k_index(t, j0)] = f2bf(y0);
+      kb[kv_k_index(t, j0 + half)] = f2bf(y1);
+      kb[kv_k_index(t, j0 + 1)] = f2bf(y2);
+      kb[kv_k_index(t, j0 + 1 + half)] = f2bf(y3);
+    }
+  } else {
+    const int nv = n0 - a.Nq - a.Nkv;
+    const int hk = nv / hd, e0 = nv % hd;
+    uint16_t* vb = a.pool + ((((static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks + blk) * a.Hkv + hk) * kBlock * hd);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) vb[kv_v_index(t, e0 + r)] = f2bf(v[r]);
+  }
+}
+
 template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL>
 __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs a) {
   static_assert(!XL || (WN * WK == 8 && (WK == 2 || WK == 4)), "X in LDS: 8 compute waves");
@@ -382,7 +422,6 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
     }
   } else if constexpr (EPI == EPI_QKV) {
     if (wk == 0) {
-      const int hd = a.hd, half = hd >> 1;
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
         if (!tvalid[j]) continue;
@@ -391,42 +430,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
         for (int g = 0; g < MG; ++g) {
           const int row = 16 * (g0 + g) + rsub;
           if (row >= a.R) continue;
-          const f32x4 v = acc[j][g];
-          const int sl = q_slot[g];
-          const int blk = sl >> 4, t = sl & 15;
-          if (n0 < a.Nq + a.Nkv) {
-            const int ph = n0 % hd;          // packed row inside the head (multiple of 4)
-            const int hb = n0 - ph;          // first packed row of the head
-            const int j0 = ph >> 1;          // dims j0, j0+half, j0+1, j0+1+half
-            const float2 cs0 = q_cs[j][g][0];
-            const float2 cs1 = q_cs[j][g][1];
-            const float y0 = v[0] * cs0.x - v[1] * cs0.y;
-            const float y1 = v[1] * cs0.x + v[0] * cs0.y;
-            const float y2 = v[2] * cs1.x - v[3] * cs1.y;
-            const float y3 = v[3] * cs1.x + v[2] * cs1.y;
-            if (n0 < a.Nq) {
-              uint16_t* q = a.out + static_cast<size_t>(row) * a.Nq + hb;
-              q[j0] = f2bf(y0);
-              q[j0 + half] = f2bf(y1);
-              q[j0 + 1] = f2bf(y2);
-              q[j0 + 1 + half] = f2bf(y3);
-            } else {
-              const int hk = (hb - a.Nq) / hd;
-              uint16_t* kb = a.pool + ((((static_cast<size_t>(a.layer) * 2 + 0) * a.n_blocks + blk) * a.Hkv + hk) *
-                                       kBlock * hd);
-              kb[kv_k_index(t, j0)] = f2bf(y0);
-              kb[kv_k_index(t, j0 + half)] = f2bf(y1);
-              kb[kv_k_index(t, j0 + 1)] = f2bf(y2);
-              kb[kv_k_index(t, j0 + 1 + half)] = f2bf(y3);
-            }
-          } else {
-            const int nv = n0 - a.Nq - a.Nkv;
-            const int hk = nv / hd, e0 = nv % hd;
-            uint16_t* vb = a.pool + ((((static_cast<size_t>(a.layer) * 2 + 1) * a.n_blocks + blk) * a.Hkv + hk) *
-                                     kBlock * hd);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) vb[kv_v_index(t, e0 + r)] = f2bf(v[r]);
-          }
+          qkv_store(a, row, n0, acc[j][g], q_slot[g], q_cs[j][g][0], q_cs[j][g][1]);
         }
       }
     }
@@ -630,6 +634,51 @@ hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s, La
     case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, p, s, ev);
     default: return launch_epi<EPI_LOGITS>(a, p, s, ev);
   }
+}
+
+// ---------------------------------------------------------------- QKV, K split
+// The QKV projection with K split over workgroups: the projection kernel
+// stores each split's product (RESID layout, ypart[split][R][N]); this kernel
+// adds them in split order and applies the QKV epilogue.  One thread per row
+// and four packed columns; its loads (position, slot, every split) are all
+// issued before the first add.  NS > 0: exactly NS splits (every load
+// unconditional).
+template <int NS>
+__global__ __launch_bounds__(256) void k_qkv_reduce(GemmArgs a, int splits) {
+  if constexpr (NS > 0) splits = NS;
+  constexpr int kMax = NS > 0 ? NS : kMaxResidSplits;
+  const int row = blockIdx.y;
+  const int n0 = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
+  if (n0 >= a.N) return;
+  const int sl = a.slot[row], p = a.pos[row];
+  const float* y = a.ypart + static_cast<size_t>(row) * a.N + n0;
+  const size_t stride = static_cast<size_t>(a.R) * a.N;
+  f32x4 ys[kMax];
+#pragma unroll
+  for (int sp = 0; sp < kMax; ++sp)
+    if (NS > 0 || sp < splits) ys[sp] = *reinterpret_cast<const f32x4*>(y + sp * stride);
+  float2 cs0 = make_float2(1.f, 0.f), cs1 = make_float2(1.f, 0.f);
+  if (n0 < a.Nq + a.Nkv) {
+    const float2* rp = a.rope + static_cast<size_t>(p) * (a.hd >> 1) + ((n0 % a.hd) >> 1);
+    cs0 = rp[0];
+    cs1 = rp[1];
+  }
+  f32x4 v = ys[0];
+#pragma unroll
+  for (int sp = 1; sp < kMax; ++sp)
+    if (NS > 0 || sp < splits) v += ys[sp];
+  qkv_store(a, row, n0, v, sl, cs0, cs1);
+}
+
+hipError_t launch_qkv_reduce(const GemmArgs& a, int splits, hipStream_t s) {
+  if (splits < 2 || splits > kMaxResidSplits || a.N % 16 != 0 || a.ypart == nullptr) return hipErrorInvalidValue;
+  const dim3 grid((a.N / 4 + 255) / 256, a.R);
+  switch (splits) {
+    case 2: hipLaunchKernelGGL(k_qkv_reduce<2>, grid, dim3(256), 0, s, a, splits); break;
+    case 4: hipLaunchKernelGGL(k_qkv_reduce<4>, grid, dim3(256), 0, s, a, splits); break;
+    default: hipLaunchKernelGGL(k_qkv_reduce<0>, grid, dim3(256), 0, s, a, splits);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace vsk

@@ -61,13 +61,17 @@ def assert_bf16_close(gpu, ref, what):
     return exact
 
 
-def _check(w, subset):
+def _check(w, subset, tuning=()):
+    """Layer-local, head and end-to-end checks of one workload; `tuning`:
+    (key, value) pairs set on the device engine first."""
     from paper_2609_37062_amd.runner import DeviceRun
     t0 = time.time()
     m = w.model
     L = m.n_layers
-    print(f"[gpu] {w.name}: seqs={w.n_seqs} rows={w.n_rows} sample={subset}", flush=True)
+    print(f"[gpu] {w.name}: seqs={w.n_seqs} rows={w.n_rows} sample={subset} tuning={list(tuning)}", flush=True)
     d = DeviceRun(w, poison_pool=True)
+    for k, v in tuning:
+        d.eng.set_tuning(k, v)
     a, batch, sub, rows, kv, idx = oracle_state(w, subset)
     ks = sorted({1, L // 2, L})
     need = sorted({k for k in ks} | {k - 1 for k in ks if k > 1})

@@ -21,6 +21,9 @@ pytestmark = pytest.mark.gpu
 # and ragged row groups
 MID = ModelCfg("mid-2L", n_layers=2, hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=128, ffn=1536,
                vocab=2048, rope_theta=500000.0)
+# hidden 2048 (64 K steps): room for up to 8 K splits of the QKV projection
+WIDE = ModelCfg("wide-2L", n_layers=2, hidden=2048, n_q_heads=16, n_kv_heads=4, head_dim=128, ffn=2048,
+                vocab=4096, rope_theta=500000.0)
 
 
 def _run(w, **kw):
@@ -116,6 +119,46 @@ def test_mid_residual_k_splits(B, target):
     lg2, ids2 = d.results()
     assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
     st, *_ = _check(w, lg, ids, list(range(0, B, max(1, B // 12))))
+    print(st)
+
+
+# (model, rows, target) -> K splits of QKV: MID 40/4096 -> 2; WIDE at 3 row
+# groups (48 N groups) 0 (192) -> 4, 240 -> 5; at 7 (24 N groups) 0 -> 8,
+# 64 -> 3
+@pytest.mark.parametrize("cfg,B,target", [("mid", 40, 4096), ("mid", 100, -1), ("wide", 40, -1), ("wide", 40, 0),
+                                          ("wide", 40, 240), ("wide", 100, 0), ("wide", 100, 64)])
+def test_mid_qkv_k_splits(cfg, B, target):
+    """QKV with K split over workgroups (the splits' products added in split
+    order by the kernel that applies rotary and writes q and the KV slots):
+    no split (-1), the default (0), and 2 to 8 splits.
+
+    MID: logits end to end within the 2e-2 bar, and a replay bit-exact.
+    WIDE (hidden 2048, logits ~2x MID's): the layer-local checks of the
+    full-size tests -- each layer's new K,V within one bf16 ulp of the oracle
+    applied to the device's own input residual (the values the split
+    reduction writes), the residual after it, and the 2e-2 bar on the head.
+    End to end this batch of 100 rows has one logit 0.0202 from the oracle
+    with and without the split (z = 2.239, the device one bf16 ulp below its
+    rounding), so the bar is held where the full-size tests hold it."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    model = MID if cfg == "mid" else WIDE
+    ctx = np.random.default_rng(300 + B).integers(0, 400, size=B)
+    w = decode_workload(model, ctx, seed=19, name=f"{cfg}-qsplit-b{B}-t{target}")
+    print(f"[gpu] {w.name}", flush=True)
+    subset = list(range(0, B, max(1, B // 12)))
+    if cfg == "wide":
+        from test_gpu_fullsize import _check as layer_local_check
+        st = layer_local_check(w, subset, tuning=[(7, target)])
+        assert st["head"]["max_err"] <= 2e-2
+        return
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(7, target)
+    d.step()
+    lg, ids = d.results()
+    d.step()
+    lg2, ids2 = d.results()
+    assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
+    st, *_ = _check(w, lg, ids, subset)
     print(st)
 
 
