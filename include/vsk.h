@@ -239,8 +239,9 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        activation chunks are staged in LDS by a ninth wave and shared by
  *        eight weight-streaming waves for QKV (K split over workgroups in
  *        the residual projections' staging, key 7; unsplit, two 16-column
- *        tiles per workgroup), gate/up and lm_head (four; eight, two per wave, for 65
- *        rows or more), residual projections taking the four-tile (33..64
+ *        tiles per workgroup), gate/up (four; eight, two per wave, for 65
+ *        rows or more) and lm_head (sixteen, two per wave, no K split in
+ *        the workgroup), residual projections taking the four-tile (33..64
  *        rows) or eight-tile (65..128 rows) staging with K split over
  *        workgroups (key 5); passes of more than 128 rows
  *        take a 2 x 2 wave grid over four tiles for QKV and the eight-tile

@@ -78,7 +78,7 @@ __device__ __forceinline__ void qkv_store(const GemmArgs& a, int row, int n0, co
 
 template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL>
 __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs a) {
-  static_assert(!XL || (WN * WK == 8 && (WK == 2 || WK == 4)), "X in LDS: 8 compute waves");
+  static_assert(!XL || (WN * WK == 8 && (WK == 1 || WK == 2 || WK == 4)), "X in LDS: 8 compute waves");
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ float s_amv[WN][MG][16];
   __shared__ int s_ami[WN][MG][16];
@@ -515,10 +515,11 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 //  pair    two N tiles per wave, 4 K steps in flight (QKV, gate/up);
 //  wide    four N tiles per wave (lm_head).
 // For 4..8 row groups the default (shape 0) is, with one row tile: X staged
-// in LDS by a ninth wave for QKV (two N tiles per workgroup), gate/up and
-// lm_head (four; at 8 row groups eight, two per wave), and for the residual
-// projections the four-tile (4 row groups) or eight-tile (8) LDS layout
-// with K split over workgroups.  A row-tiled pass (more than 128 rows)
+// in LDS by a ninth wave for gate/up (four N tiles; at 8 row groups eight,
+// two per wave) and lm_head (sixteen, two per wave, the eight waves side by
+// side), for the residual projections and QKV the four-tile (4 row groups)
+// or eight-tile (8) LDS layout with K split over workgroups (unsplit QKV:
+// two N tiles per workgroup).  A row-tiled pass (more than 128 rows)
 // takes the 2 x 2 wave grid for QKV and the eight-tile LDS layout elsewhere.
 // Shape 1 takes one N tile per wave column everywhere, shape 2 two, shape 3
 // is a 2 x 2 wave grid over four N tiles, shape 4 stages X in LDS for four N
@@ -539,7 +540,7 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
         // weight rings of 4 and 2 K steps: shallower rings measured faster
         // with X in LDS (16 steps: batch-64 pass 3.06 ms, these 2.90)
         if constexpr (EPI == EPI_LOGITS)
-          if (p.nt == 2) return launch_cfg<4, 2, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+          if (p.nt == 2) return launch_cfg<4, 2, 8, 1, 8, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         if (p.wn == 4) return launch_cfg<4, 1, 4, 2, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         return launch_cfg<4, 1, 2, 4, 2, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
       }
@@ -549,6 +550,8 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
     default:
       if (p.xl) {
         // (QKV never takes it: its rotary factors would spill)
+        if constexpr (EPI == EPI_LOGITS)
+          if (p.nt == 2) return launch_cfg<8, 2, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         if constexpr (EPI != EPI_QKV)
           if (p.nt == 2) return launch_cfg<8, 2, 4, 2, 2, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         if (p.wn == 4) return launch_cfg<8, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
@@ -582,6 +585,12 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
       p.nt = 2;
       p.wn = 4;
       wk = 2;
+      // lm_head: the eight waves side by side, 16 N tiles per workgroup
+      // (half the X reads per weight byte; 242 -> 222 us at batch 128)
+      if (epi == EPI_LOGITS) {
+        p.wn = 8;
+        wk = 1;
+      }
     } else if (shape == 3 || shape == 5 || (auto_shape && !one_tile)) {
       // a row-tiled pass (more than 128 rows) re-streams the weights once per
       // row tile: there the 2 x 2 wave grid, each X chunk feeding four N
@@ -597,9 +606,14 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
       p.wn = epi == EPI_QKV ? 2 : 4;
       wk = 8 / p.wn;
       // lm_head (N = vocab: workgroups to spare) at 4 row groups: two N
-      // tiles per wave, half the X reads per weight byte (170 -> 152 us at
-      // batch 64)
-      if (epi == EPI_LOGITS && p.mg == 4) p.nt = 2;
+      // tiles per wave and the eight waves side by side (no K split inside
+      // the workgroup), a quarter of the X reads per weight byte (170 -> 152
+      // us at batch 64 with four waves side by side, 151 -> 147 with eight)
+      if (epi == EPI_LOGITS && p.mg == 4) {
+        p.nt = 2;
+        p.wn = 8;
+        wk = 1;
+      }
     } else {
       // one column of K-split waves (N = hidden gives 192-256 workgroups)
       p.nt = shape == 1 ? 1 : shape == 2 ? 2 : (wide_n ? 2 : 1);
