@@ -689,6 +689,7 @@ hipError_t launch_qkv_reduce(const GemmArgs& a, int splits, hipStream_t s) {
   const dim3 grid((a.N / 4 + 255) / 256, a.R);
   switch (splits) {
     case 2: hipLaunchKernelGGL(k_qkv_reduce<2>, grid, dim3(256), 0, s, a, splits); break;
+    case 3: hipLaunchKernelGGL(k_qkv_reduce<3>, grid, dim3(256), 0, s, a, splits); break;
     case 4: hipLaunchKernelGGL(k_qkv_reduce<4>, grid, dim3(256), 0, s, a, splits); break;
     default: hipLaunchKernelGGL(k_qkv_reduce<0>, grid, dim3(256), 0, s, a, splits);
   }
