@@ -119,11 +119,11 @@ inline int attn_splits(int kv_len, int bps) {
 // Default split size (4-wave work items, two per compute unit).  With few
 // (row, KV head) pairs long contexts are cut into 512-token splits to spread
 // them over the compute units; once the pairs alone fill the chip,
-// 1024-token splits still cut the longest contexts of a heavy-tailed batch
-// (whose single work item would otherwise finish last) while most rows need
-// no merge (measured: batch 16 at 512-1024 tokens, batch 128 at lognormal
-// lengths).
-inline int attn_auto_bps(int n_rows, int n_kv_heads) { return n_rows * n_kv_heads >= 256 ? 64 : 32; }
+// 1536-token splits still cut the longest contexts of a heavy-tailed batch
+// (dispatched first, longest walk first) while most rows need no merge
+// (measured: batch 16 at 512-1024 tokens; batch 128 at lognormal lengths,
+// 96 and 128 blocks best, 64 and 160 or more slower).
+inline int attn_auto_bps(int n_rows, int n_kv_heads) { return n_rows * n_kv_heads >= 256 ? 96 : 32; }
 
 struct Handle {
   vsk_model_cfg cfg{};
