@@ -244,8 +244,8 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        the workgroup), residual projections taking the four-tile (33..64
  *        rows) or eight-tile (65..128 rows) staging with K split over
  *        workgroups (key 5); passes of more than 128 rows
- *        take a 2 x 2 wave grid over four tiles for QKV and the eight-tile
- *        staging elsewhere.  1 one column of K-split waves, one tile, every
+ *        take the staging with the eight waves side by side (16 tiles, 8
+ *        for QKV).  1 one column of K-split waves, one tile, every
  *        projection; 2 the same with two tiles; 3 the 2 x 2 grid everywhere;
  *        4 staging with four tiles (two for QKV) everywhere, residual
  *        projections with K split over workgroups; 5 for 65 rows or more

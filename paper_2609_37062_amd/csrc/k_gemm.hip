@@ -519,8 +519,8 @@ static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStre
 // two per wave) and lm_head (sixteen, two per wave, the eight waves side by
 // side), for the residual projections and QKV the four-tile (4 row groups)
 // or eight-tile (8) LDS layout with K split over workgroups (unsplit QKV:
-// two N tiles per workgroup).  A row-tiled pass (more than 128 rows)
-// takes the 2 x 2 wave grid for QKV and the eight-tile LDS layout elsewhere.
+// two N tiles per workgroup).  A row-tiled pass (more than 128 rows) takes
+// the LDS layout with the eight waves side by side (16 N tiles; 8 for QKV).
 // Shape 1 takes one N tile per wave column everywhere, shape 2 two, shape 3
 // is a 2 x 2 wave grid over four N tiles, shape 4 stages X in LDS for four N
 // tiles (two for QKV) everywhere, shape 5 for eight (two per wave) at 8 row
@@ -550,8 +550,11 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
     default:
       if (p.xl) {
         // (QKV never takes it: its rotary factors would spill)
-        if constexpr (EPI == EPI_LOGITS)
-          if (p.nt == 2) return launch_cfg<8, 2, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        // eight waves side by side (no K split inside the workgroup)
+        if (p.wn == 8) {
+          if constexpr (EPI == EPI_QKV) return launch_cfg<8, 1, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+          else return launch_cfg<8, 2, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+        }
         if constexpr (EPI != EPI_QKV)
           if (p.nt == 2) return launch_cfg<8, 2, 4, 2, 2, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
         if (p.wn == 4) return launch_cfg<8, 1, 4, 2, 16, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
@@ -585,12 +588,20 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
       p.nt = 2;
       p.wn = 4;
       wk = 2;
-      // lm_head: the eight waves side by side, 16 N tiles per workgroup
-      // (half the X reads per weight byte; 242 -> 222 us at batch 128)
-      if (epi == EPI_LOGITS) {
+      // lm_head, and every projection of a row-tiled pass (workgroups to
+      // spare): the eight waves side by side, 16 N tiles per workgroup
+      // (half the X reads per weight byte; lm_head 242 -> 222 us at batch
+      // 128, the 2,080-row pass 21.0 -> 16.6 ms with QKV below)
+      if (epi == EPI_LOGITS || (epi != EPI_QKV && !one_tile)) {
         p.wn = 8;
         wk = 1;
       }
+    } else if (auto_shape && !one_tile && p.mg == 8 && epi == EPI_QKV) {
+      // QKV of a row-tiled pass: X in LDS, eight waves side by side with one
+      // N tile each (two would spill the rotary factors)
+      p.xl = true;
+      p.wn = 8;
+      wk = 1;
     } else if (shape == 3 || shape == 5 || (auto_shape && !one_tile)) {
       // a row-tiled pass (more than 128 rows) re-streams the weights once per
       // row tile: there the 2 x 2 wave grid, each X chunk feeding four N
