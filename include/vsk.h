@@ -258,8 +258,9 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  * key 5: residual projections (O, down) of passes of at most 128 rows: the
  *        workgroup count their K split aims for (1..4096); 0 (the default):
  *        192 workgroups in the activation-staged layout at 33..64 rows, 384
- *        at 65..128, no split in the other layouts (1..32 rows: measured no
- *        faster); -1: no split.  Split products are added to the residual in
+ *        at 65..128, 192 for the down projection at 1..16 rows (two tiles
+ *        per workgroup), no split otherwise (O at 1..32 rows, down at
+ *        17..32: measured no faster); -1: no split.  Split products are added to the residual in
  *        split order by the RMSNorm that follows.
  * key 6: rows of a sequence with several new rows (a prefill chunk): 1 (the
  *        default) one causal work item per run of up to 128 (row, query

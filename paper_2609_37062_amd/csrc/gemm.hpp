@@ -44,7 +44,8 @@ constexpr int kQkvTargetWgs = 192;  // default split-K target of QKV at 4..8 row
 
 // shape: launch shape for 4 or 8 row groups (0 default; see k_gemm.hip)
 // resid_target: workgroups a residual projection's K split aims for (-1: no
-// split; 0: the layout's default -- 192 or 384 with X in LDS, else
+// split; 0: the layout's default -- 192 or 384 with X in LDS, 192 for the
+// two-tile layout of the down projection at <= 16 rows, else
 // kResidTargetWgs)
 GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0, int resid_target = 0);
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s, LaunchEvents ev = {});

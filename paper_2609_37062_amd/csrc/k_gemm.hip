@@ -576,6 +576,11 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   int wk = 8;
   if (p.mg == 1) {
     if (epi != EPI_RESID) p.nt = epi == EPI_LOGITS ? 4 : 2;
+    // a residual projection with K > N (down): two N tiles per workgroup,
+    // half the X reads per weight byte, with K split in two (below) to keep
+    // the workgroup count (batch 16: 15.5 -> 13.3 us, the pass 2.149 ->
+    // 2.125 ms)
+    else if (K > N) p.nt = 2;
   } else if (p.mg >= 4) {
     const bool wide_n = epi == EPI_SWIGLU || epi == EPI_LOGITS;
     const bool auto_shape = shape == 0;
@@ -638,10 +643,11 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   // then adds the splits' products into the residual.  With X in LDS the
   // default target is 192 workgroups at 4 row groups (4 splits at hidden
   // 3072) and 384 at 8 (measured best of 96-384 and 128-384).
-  const int target = resid_target < 0    ? 0
-                     : resid_target > 0  ? resid_target
-                     : p.xl              ? (p.mg == 4 ? 192 : 384)
-                                         : kResidTargetWgs;
+  const int target = resid_target < 0            ? 0
+                     : resid_target > 0          ? resid_target
+                     : p.xl                      ? (p.mg == 4 ? 192 : 384)
+                     : p.mg == 1 && p.nt == 2    ? 192
+                                                 : kResidTargetWgs;
   if (epi == EPI_RESID && target > 0 && p.m_tiles == 1) {
     const int Kt = K / 32;
     int ks = std::min({(target + p.n_groups - 1) / p.n_groups, kMaxResidSplits, std::max(1, Kt / (4 * wk))});
