@@ -4,9 +4,10 @@
  * One forward pass of a Llama-style GQA decoder over the rows of a batch:
  * paged-attention decode over a block-table KV cache, bf16 weight-streaming
  * projections with a SwiGLU MLP, fused RMSNorm and rotary positions, and a
- * greedy argmax.  This is the dense-mode pass of the paper ("Design and
- * Implementation": dense mode runs every layer for every row; a row is one
- * token's hidden state, one per sequence in decode and several in prefill).
+ * greedy argmax.  It is the paper's dense mode, which takes every layer for
+ * every row (Section 3, "Design and Implementation", Vocabulary paragraph).
+ * Each row of a pass carries one token through the layers: the next token of
+ * its sequence in a decode pass, one prompt token in a prefill chunk.
  *
  * Conventions
  *  - Every function returns an int status (VSK_OK or a negative VSK_E_*).
@@ -16,10 +17,14 @@
  *    memory.  The library never allocates or frees device memory: every
  *    device buffer (weights, packed weights, KV pool, batch metadata,
  *    workspace, outputs) belongs to the caller and must outlive its use.
- *    Host arrays are copied, never retained.
+ *    Host arrays are copied, never retained.  (The library's own host
+ *    memory includes two pinned staging buffers for vsk_batch_upload.)
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *    Device work is enqueued asynchronously on it; nothing synchronises,
- *    except vsk_batch_upload, which returns once its host source can be reused.
+ *    Device work is enqueued asynchronously on it.  The calls that wait for
+ *    the device are: vsk_weights_pack_head (setup; it waits for its rotary
+ *    table copy), vsk_device_status (by definition), and vsk_batch_upload
+ *    only when the staging buffer it takes is still being read by the copy
+ *    it issued two uploads earlier.  Nothing else synchronises.
  *  - bf16 tensors are IEEE bfloat16 bit patterns (uint16), row-major unless
  *    stated otherwise.  Matrices are [out][in].
  *  - A handle is not thread-safe.  Device faults surface at the caller's
@@ -181,7 +186,16 @@ size_t vsk_workspace_bytes(const vsk_handle* h, int32_t max_rows, int32_t max_se
 int vsk_workspace_init(vsk_handle* h, void* ws_dev, size_t bytes, int32_t max_rows,
                        int32_t max_seqs, int32_t max_kv_len, void* stream);
 
-/* One decode step over the uploaded batch (every q_len must be 1):
+/* One decode step over the uploaded batch (every q_len must be 1), the
+ * dense-mode decode pass (Section 3, "Design and Implementation": dense mode
+ * runs every layer for every row; Section 3.2, Invariant 1: every layer
+ * writes its own K,V for every row; greedy decoding as in the paper's
+ * measurements, Section 2 and appendix "Natural Stopping and the Output
+ * Lengths").  Below the ridge point it is bound by streaming the weights
+ * once (appendix "The Switching Thresholds from the Roofline", decode rule).
+ * The batch metadata must have been uploaded; the workspace must be the one
+ * bound by vsk_workspace_init and large enough for the batch (else
+ * VSK_E_ARG / VSK_E_STATE before any launch).
  * ids_dev int32[n_rows] input tokens; writes every layer's K,V of every row
  * at its slot; logits_dev bf16 [n_rows][vocab]; next_ids_dev (nullable)
  * int32[n_rows] = lowest index of the maximum fp32 logit (greedy).
@@ -191,7 +205,10 @@ int vsk_decode_step(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int
                     void* ws_dev, size_t ws_bytes, void* stream);
 
 /* One ragged pass over the uploaded batch (any q_lens: chunked prefill rows
- * and decode rows together).  Prefill row at position p attends to keys
+ * and decode rows together).  The paper's prefill passes carry one row per
+ * prompt token (Section 3.1, Prefill paragraph) and are compute-bound
+ * (Section 2); the engine it builds on runs chunked prefill beside decode
+ * (appendix "The Switching Thresholds from the Roofline", prefill floor).  Prefill row at position p attends to keys
  * 0..p of its sequence; all of a layer's new K,V are written before that
  * layer's attention reads them.  Logits (bf16 [n_logit_rows][vocab]) and
  * next ids are produced only for the rows listed in logit_rows_dev
@@ -200,11 +217,66 @@ int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logi
                       int32_t n_logit_rows, void* logits_dev, int32_t* next_ids_dev,
                       void* ws_dev, size_t ws_bytes, void* stream);
 
-/* Greedy sampling over given logits (dtype 0 = bf16, 1 = fp32), row-major
- * [rows][vocab]: ids_dev[r] = lowest index of the maximum; NaN never wins;
- * an all-NaN row gives 0.  Uses no workspace beyond its arguments. */
+/* Greedy sampling (the decoding the paper measures with, Section 2 and
+ * appendix "Natural Stopping and the Output Lengths") over given logits: logits_dev
+ * row-major [rows][vocab] of dtype 0 = bf16 or 1 = fp32; ids_dev int32[rows]
+ * receives, per row, the lowest index of the maximum value.  NaN never wins;
+ * a row with no non-NaN value gives 0; a row of -inf gives 0.  rows >= 1,
+ * vocab >= 1 (any size), both pointers device memory owned by the caller.
+ * Uses no workspace beyond its arguments.  VSK_E_ARG on a null pointer, a
+ * non-positive size or an unknown dtype. */
 int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab,
                       int32_t* ids_dev, void* stream);
+
+/* ----------------------------------------------------------------- mode switch
+ * Profitability-aware mode switching (Section 3.3; appendix "The Switching
+ * Thresholds from the Roofline", decode rule and served thresholds).  Host
+ * pure functions: no handle, no device, no state beyond their arguments.
+ *
+ * Routed mode pays a fixed cost tau per step; in decode below the ridge point
+ * a Project-Only row saves only its attention read of the layer's KV, b bytes
+ * per resident token.  With a fraction s of the routed decisions projecting
+ * over L_r routed layers, routing pays when the resident tokens V exceed
+ *   V* = tau_eff * BW / (s * L_r * b),  tau_eff = tau * L_r / tau_layers
+ * (tau is measured once over tau_layers routed layers and reused as a
+ * per-routed-layer coefficient).  Thresholds: exit = V*, enter =
+ * enter_factor * V* (1.25 in the paper), each rounded to the nearest
+ * multiple of round_tokens (10000 reproduces the printed thresholds; 0
+ * rounds to the nearest token). */
+typedef struct vsk_switch_params {
+  double tau_s;                    /* fixed per-step cost of routed mode, seconds (> 0) */
+  int32_t tau_layers;              /* routed layers tau was measured over (>= 1) */
+  double bw_bytes_per_s;           /* device memory bandwidth, bytes/s (> 0) */
+  double skip;                     /* s in (0, 1]: fraction of decisions projecting */
+  int32_t routed_layers;           /* L_r (>= 1) */
+  double kv_bytes_per_token_layer; /* b (> 0): K and V bytes of one token at one layer */
+  double enter_factor;             /* >= 1 */
+  double round_tokens;             /* >= 0 */
+} vsk_switch_params;
+
+typedef struct vsk_switch_band {
+  double v_star;        /* the crossover V*, tokens (unrounded) */
+  int64_t exit_tokens;  /* routing turns off at V <= exit_tokens */
+  int64_t enter_tokens; /* routing turns on at V >= enter_tokens */
+} vsk_switch_band;
+
+/* Thresholds of the decode rule.  VSK_E_ARG on a parameter out of range. */
+int vsk_switch_thresholds(const vsk_switch_params* p, vsk_switch_band* out);
+/* One observation of the resident tokens V: the switching state (0 dense,
+ * 1 routing) moves to 1 at V >= enter, to 0 at V <= exit, and is kept in
+ * between.  *promote (nullable) = 1 exactly when the state went from 0 to 1:
+ * that crossing promotes the requests already decoding in dense mode. */
+int vsk_switch_step(const vsk_switch_band* t, int32_t routing_in, int64_t resident_tokens,
+                    int32_t* routing_out, int32_t* promote);
+/* Decode mode of one request after an observation: mode_in -1 (the request
+ * starts decoding now: it takes the current state `routing`), 0 dense (it
+ * becomes routed if `promote`), 1 routed (it stays routed: one-way). */
+int vsk_switch_decode_mode(int32_t mode_in, int32_t routing, int32_t promote, int32_t* mode_out);
+/* Prefill mode, fixed at admission: routed (1) iff the batch's prompt tokens
+ * reach floor_tokens (1536 in the paper) and the estimated Project-Only
+ * share exceeds share_min (0.35 in the paper). */
+int vsk_switch_prefill(int64_t prompt_tokens, double po_share, int64_t floor_tokens, double share_min,
+                       int32_t* routed);
 
 /* Timing probes (measurement only).  While set, the first n_pairs launches
  * of kernel class `which` in the following passes are each launched with

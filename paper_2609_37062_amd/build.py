@@ -19,7 +19,7 @@ OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libvsk.so")
 ROOT = os.path.dirname(HERE)
 
-SOURCES = ["alloc.cpp", "api.cpp", "k_misc.hip", "k_gemm.hip", "k_attn.hip", "k_step.hip"]
+SOURCES = ["alloc.cpp", "api.cpp", "mode.cpp", "k_misc.hip", "k_gemm.hip", "k_attn.hip", "k_step.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -18,6 +18,14 @@ using namespace vsk;
 
 struct vsk_handle : public Handle {};
 
+vsk::Handle::~Handle() {
+  for (Staging& st : stage) {
+    if (st.pending && st.done) (void)hipEventSynchronize(st.done);
+    if (st.done) (void)hipEventDestroy(st.done);
+    if (st.host) (void)hipHostFree(st.host);
+  }
+}
+
 namespace vsk {
 static int step_workgroups(Handle& h);
 }
@@ -425,9 +433,35 @@ int vsk_batch_upload(vsk_handle* h, void* meta_dev, size_t bytes, void* stream) 
   d.n_pfx_items = b.n_pfx_items();
   d.max_pfx_splits = b.max_pfx_splits;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = hipMemcpyAsync(meta_dev, staging.data(), staging.size(), hipMemcpyHostToDevice, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);  // staging is a local buffer
+  // copy from a pinned staging buffer: the transfer runs asynchronously and
+  // the host returns at once, unless this buffer's previous copy (issued two
+  // uploads ago) has not finished yet
+  Handle::Staging& st = h->stage[h->stage_next];
+  hipError_t e = hipSuccess;
+  if (st.pending) {
+    e = hipEventSynchronize(st.done);
+    if (e != hipSuccess) return hip_check(h, e, "metadata staging wait");
+    st.pending = false;
+  }
+  if (st.cap < staging.size()) {
+    if (st.host) (void)hipHostFree(st.host);
+    st.host = nullptr;
+    st.cap = 0;
+    const size_t cap = std::max<size_t>(align_up(staging.size(), 1 << 16), 1 << 16);
+    e = hipHostMalloc(&st.host, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_check(h, e, "metadata staging buffer");
+    st.cap = cap;
+  }
+  if (!st.done) {
+    e = hipEventCreateWithFlags(&st.done, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_check(h, e, "metadata staging event");
+  }
+  std::memcpy(st.host, staging.data(), staging.size());
+  e = hipMemcpyAsync(meta_dev, st.host, staging.size(), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipEventRecord(st.done, s);
   if (e != hipSuccess) return hip_check(h, e, "metadata upload");
+  st.pending = true;
+  h->stage_next ^= 1;
   d.n_seqs = b.n_seqs;
   d.n_rows = b.n_rows;
   d.max_blocks = b.max_blocks;

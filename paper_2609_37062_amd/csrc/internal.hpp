@@ -142,6 +142,18 @@ struct Handle {
   bool batch_built = false;
   BatchDev bd;
   bool batch_uploaded = false;
+  // metadata upload: two pinned host staging buffers used in turn, each with
+  // an event recorded after the copy that reads it, so an upload only waits
+  // when the copy issued two uploads earlier is still running
+  struct Staging {
+    void* host = nullptr;
+    size_t cap = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+  };
+  Staging stage[2];
+  int stage_next = 0;
+  ~Handle();
   // tuning
   int attn_bps = 0;  // 0: attn_auto_bps
   int layers_run = 0;  // inspection: run only the first layers_run layers (0 = all)

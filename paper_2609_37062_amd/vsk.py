@@ -35,6 +35,16 @@ class ModelCfg(C.Structure):
                 ("rope_theta", C.c_float), ("rms_eps", C.c_float)]
 
 
+class SwitchParams(C.Structure):
+    _fields_ = [("tau_s", C.c_double), ("tau_layers", C.c_int32), ("bw_bytes_per_s", C.c_double),
+                ("skip", C.c_double), ("routed_layers", C.c_int32), ("kv_bytes_per_token_layer", C.c_double),
+                ("enter_factor", C.c_double), ("round_tokens", C.c_double)]
+
+
+class SwitchThresholds(C.Structure):
+    _fields_ = [("v_star", C.c_double), ("exit_tokens", C.c_int64), ("enter_tokens", C.c_int64)]
+
+
 class LayerWeights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm",
                                           "w_gate", "w_up", "w_down")]
@@ -76,6 +86,10 @@ SIGNATURES = [
     ("vsk_argmax_sample", C.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
     ("vsk_set_tuning", C.c_int, [_VP, _I32, _I32]),
     ("vsk_residual_copy", C.c_int, [_VP, _VP, _I32, _VP]),
+    ("vsk_switch_thresholds", C.c_int, [C.POINTER(SwitchParams), C.POINTER(SwitchThresholds)]),
+    ("vsk_switch_step", C.c_int, [C.POINTER(SwitchThresholds), _I32, _I64, _PI32, _PI32]),
+    ("vsk_switch_decode_mode", C.c_int, [_I32, _I32, _I32, _PI32]),
+    ("vsk_switch_prefill", C.c_int, [_I64, C.c_double, _I64, C.c_double, _PI32]),
     ("vsk_set_probe", C.c_int, [_VP, _I32, C.POINTER(_VP), C.POINTER(_VP), _I32]),
     ("vsk_exec_counters", C.c_int, [_VP, _PI64, _I32]),
     ("vsk_set_step_trace", C.c_int, [_VP, _VP, _SZ, _PI32, _PI32]),
@@ -128,6 +142,45 @@ def argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, stream=None):
     st = lib().vsk_argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, stream)
     if st != VSK_OK:
         raise VskError(st, "argmax_sample")
+
+
+# ------------------------------------------------------------------ mode switch
+def switch_thresholds(tau_s, bw_bytes_per_s, skip, routed_layers, kv_bytes_per_token_layer, tau_layers=16,
+                      enter_factor=1.25, round_tokens=10000.0):
+    """(V*, exit tokens, enter tokens) of the decode rule (vsk_switch_thresholds)."""
+    p = SwitchParams(tau_s, tau_layers, bw_bytes_per_s, skip, routed_layers, kv_bytes_per_token_layer,
+                     enter_factor, round_tokens)
+    t = SwitchThresholds()
+    st = lib().vsk_switch_thresholds(C.byref(p), C.byref(t))
+    if st != VSK_OK:
+        raise VskError(st, "switch_thresholds")
+    return t.v_star, t.exit_tokens, t.enter_tokens
+
+
+def switch_step(exit_tokens, enter_tokens, routing, resident_tokens):
+    """One hysteresis observation: returns (routing state, promote)."""
+    t = SwitchThresholds(0.0, exit_tokens, enter_tokens)
+    r, pr = C.c_int32(), C.c_int32()
+    st = lib().vsk_switch_step(C.byref(t), routing, resident_tokens, C.byref(r), C.byref(pr))
+    if st != VSK_OK:
+        raise VskError(st, "switch_step")
+    return r.value, pr.value
+
+
+def switch_decode_mode(mode_in, routing, promote):
+    out = C.c_int32()
+    st = lib().vsk_switch_decode_mode(mode_in, routing, promote, C.byref(out))
+    if st != VSK_OK:
+        raise VskError(st, "switch_decode_mode")
+    return out.value
+
+
+def switch_prefill(prompt_tokens, po_share, floor_tokens=1536, share_min=0.35):
+    out = C.c_int32()
+    st = lib().vsk_switch_prefill(prompt_tokens, po_share, floor_tokens, share_min, C.byref(out))
+    if st != VSK_OK:
+        raise VskError(st, "switch_prefill")
+    return out.value
 
 
 class Engine:
