@@ -59,11 +59,12 @@ def from_bf16_bits(bits) -> np.ndarray:
 
 
 # ------------------------------------------------------------------ RMSNorm
-def rmsnorm(x, g, eps: float) -> np.ndarray:
-    """Row-wise x / sqrt(mean(x^2) + eps) * g over the last axis (float64)."""
-    x = np.asarray(x, dtype=np.float64)
-    ms = np.mean(x * x, axis=-1, keepdims=True)
-    return x / np.sqrt(ms + eps) * np.asarray(g, dtype=np.float64)
+def rmsnorm(x, g, eps: float, dt=np.float64) -> np.ndarray:
+    """Row-wise x / sqrt(mean(x^2) + eps) * g over the last axis, in dtype dt
+    (float64 by default; float32 for the contract-mode variant)."""
+    x = np.asarray(x, dtype=dt)
+    ms = np.mean(x * x, axis=-1, keepdims=True, dtype=dt)
+    return x / np.sqrt(ms + dt(eps)) * np.asarray(g, dtype=dt)
 
 
 # ------------------------------------------------------------------ rotary
@@ -72,40 +73,43 @@ def rope_inv_freq(head_dim: int, theta: float) -> np.ndarray:
     return theta ** (-2.0 * i / head_dim)
 
 
-def rope(x, pos, theta: float) -> np.ndarray:
+def rope(x, pos, theta: float, dt=np.float64) -> np.ndarray:
     """Rotate-half rotary embedding.
 
-    x   : [..., n_heads, head_dim] (float64)
+    x   : [..., n_heads, head_dim]
     pos : int array broadcastable to x's leading axes (one position per row)
-    Pair (j, j + d/2) turns by the angle pos * theta^(-2j/d).
+    Pair (j, j + d/2) turns by the angle pos * theta^(-2j/d).  The angles and
+    their cosines and sines are taken in float64; the rotation runs in dtype
+    dt (with float32 the factors are first rounded to float32).
     """
-    x = np.asarray(x, dtype=np.float64)
+    x = np.asarray(x, dtype=dt)
     d = x.shape[-1]
     half = d // 2
     ang = np.asarray(pos, dtype=np.float64)[..., None, None] * rope_inv_freq(d, theta)
-    c, s = np.cos(ang), np.sin(ang)
+    c, s = np.cos(ang).astype(dt), np.sin(ang).astype(dt)
     a, b = x[..., :half], x[..., half:]
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
 
 
 # ------------------------------------------------------------------ MLP
-def silu(z) -> np.ndarray:
-    z = np.asarray(z, dtype=np.float64)
-    return z / (1.0 + np.exp(-z))
+def silu(z, dt=np.float64) -> np.ndarray:
+    z = np.asarray(z, dtype=dt)
+    with np.errstate(over="ignore"):
+        return z / (dt(1.0) + np.exp(-z))
 
 
 # ------------------------------------------------------------------ attention
-def attend(q, K, V) -> np.ndarray:
+def attend(q, K, V, dt=np.float64) -> np.ndarray:
     """One query head over n keys: softmax(q.K^T / sqrt(d)) V.
 
-    q [d], K [n, d], V [n, d] -> [d]  (float64, max-subtracted softmax).
+    q [d], K [n, d], V [n, d] -> [d]  (max-subtracted softmax, in dtype dt).
     """
-    q = np.asarray(q, dtype=np.float64)
+    q = np.asarray(q, dtype=dt)
     d = q.shape[-1]
-    s = (np.asarray(K, dtype=np.float64) @ q) / np.sqrt(d)
+    s = (np.asarray(K, dtype=dt) @ q) / dt(np.sqrt(d))
     p = np.exp(s - np.max(s))
-    p /= np.sum(p)
-    return p @ np.asarray(V, dtype=np.float64)
+    p /= np.sum(p, dtype=dt)
+    return p @ np.asarray(V, dtype=dt)
 
 
 def attention_weights(q, K) -> np.ndarray:

@@ -1,13 +1,16 @@
 """Device parity at the full workload sizes, in the launch configuration the
-benchmark times, on sampled sequences.
+benchmark times.
 
 Sequences of a pass are independent, so the oracle recomputes a few sampled
-sequences of the full batch while the device runs the whole batch.
+sequences of the full batch end to end while the device runs the whole batch.
 
 Checks per workload:
-  * head (the spec bar): the oracle's final RMSNorm + lm_head applied
-    to the device's own final residual stream must give the device's bf16
-    logits within 2e-2, with the same greedy id up to near-ties;
+  * head, on every row that returns logits (the spec bar): the
+    oracle's final RMSNorm + lm_head applied to the device's own final
+    residual stream must give the device's bf16 logits within 2e-2
+    (logit_bound), and the device's greedy ids must equal the oracle's on
+    every row whose top-2 gap exceeds 0.04 (the rest: within 0.04 of the
+    maximum);
   * layer-local: at the first, middle and last layer the oracle applies that
     one layer to the device's residual stream before it; the layer's new K,V
     must agree within one bf16 ulp and the residual after it within
@@ -17,12 +20,12 @@ Checks per workload:
   * sub-path isolation (3B and 8B): with the layer's down projection zeroed
     the layer is attention + O projection only, with its O projection zeroed
     it is the MLP only; each must match within PATH_TOL;
-  * end to end: the device logits against the oracle run from the token ids
-    alone; ids must agree up to near-ties and the logits within E2E_BOUND.
-    Over 28-32 layers the bf16 rounding points amplify summation-order
-    differences: the oracle itself moves by up to 0.06 on these workloads
-    when only its matrix products switch from float64 to float32 (measured
-    on the 3B batch-16 workload), so the end-to-end bound is set at 4x that.
+  * end to end from token ids on the sampled sequences: each row is held to
+    max(2e-2, 3 x the oracle's own float32-vs-float64 spread on that row)
+    (helpers.compare_logits).  Over 28-32 layers every row's bf16 rounding
+    points flip under summation-order noise and each later normalisation
+    amplifies the flips, so the float32 contract-mode oracle itself sits
+    0.06-0.08 from the float64 one on these workloads.
 """
 import time
 
@@ -31,39 +34,33 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
+from oracle.kvcache import PagedKV  # noqa: E402
 from oracle.model import GeneratedWeights, forward  # noqa: E402
 from workloads.configs import workload  # noqa: E402
 
-from helpers import LOGIT_TOL, compare_logits, oracle_run, oracle_state  # noqa: E402
+from helpers import LOGIT_TOL, assert_bf16_close, compare_logits, e2e_compare, oracle_state  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
 LAYER_TOL = 2e-2   # max |x_dev - x_oracle| / rms(x_oracle) after one full layer
 PATH_TOL = 2e-3    # the same after one isolated sub-path (attention or MLP)
-E2E_BOUND = 0.25   # end-to-end logits bound (see module docstring)
 
 
-def assert_bf16_close(gpu, ref, what):
-    """Elementwise: equal, or one bf16 ulp apart (summation order may move a
-    rounding).  Values far below the tensor's RMS come out of cancellations
-    (a rotary pair whose terms nearly cancel), where an fp32 sum differs from
-    the float64 one by more ulps of the small result: there the floor is
-    1e-3 of the RMS."""
-    gpu = np.asarray(gpu, np.float64)
-    ref = np.asarray(ref, np.float64)
-    mag = np.maximum(np.abs(ref), 2.0 ** -126)
-    ulp = np.exp2(np.floor(np.log2(mag)) - 7)
-    floor = 1e-3 * np.sqrt(np.mean(ref ** 2))
-    bad = np.abs(gpu - ref) > np.maximum(ulp * 1.0001, floor)
-    exact = float(np.mean(gpu == ref))
-    assert not bad.any(), f"{what}: {int(bad.sum())} elements beyond 1 ulp"
-    assert exact > 0.9, f"{what}: only {exact:.3f} exact"
-    return exact
+def head_all_rows(w, W, x_final, lg, ids):
+    """The 2e-2 bar on every logit row: the oracle's final norm + lm_head on
+    the device's own final residual (x_final: all rows of the pass)."""
+    m = w.model
+    decode = all(s.q_len == 1 for s in w.seqs)
+    lrows = np.arange(w.n_rows) if decode else w.logit_rows().astype(np.int64)
+    dummy = PagedKV(m.n_layers, 1, m.n_kv_heads, m.head_dim)
+    oh = forward(m, W, dummy, {"pos": None, "slot": None, "cu_q": None, "kv_len": None, "block_table": None},
+                 np.zeros(len(lrows), np.int64), np.arange(len(lrows)), x0=x_final[lrows], layers=[])
+    return compare_logits(lg[:len(lrows)], ids[:len(lrows)], oh["z"], tol=LOGIT_TOL)
 
 
 def _check(w, subset, tuning=()):
-    """Layer-local, head and end-to-end checks of one workload; `tuning`:
-    (key, value) pairs set on the device engine first."""
+    """Layer-local, head (all rows) and end-to-end checks of one workload;
+    `tuning`: (key, value) pairs set on the device engine first."""
     from paper_2609_37062_amd.runner import DeviceRun
     t0 = time.time()
     m = w.model
@@ -76,10 +73,14 @@ def _check(w, subset, tuning=()):
     ks = sorted({1, L // 2, L})
     need = sorted({k for k in ks} | {k - 1 for k in ks if k > 1})
     xs = {}
+    x_all = None
     for k in need:
         d.set_layers(k)
         d.step()
-        xs[k] = d.residual()[rows]
+        xa = d.residual()
+        xs[k] = xa[rows]
+        if k == L:
+            x_all = xa
     d.set_layers(0)
     d.step()
     lg, ids = d.results()
@@ -100,38 +101,17 @@ def _check(w, subset, tuning=()):
         assert_bf16_close(knew[k][0], Ko, f"K layer {k - 1}")
         assert_bf16_close(knew[k][1], Vo, f"V layer {k - 1}")
         assert err <= LAYER_TOL, (k, err)
-    # ---- head on the device's final residual (the 2e-2 bar)
-    _, _, _, _, dev_rows = oracle_run_rows(w, idx)
-    lrows = logit_rows_local(w, idx, sub)
-    oh = forward(m, W, kv, sub, tok, lrows, x0=xs[L], layers=[])
-    stats["head"] = compare_logits(lg[dev_rows], ids[dev_rows], oh["z"], tol=LOGIT_TOL)
+    print(f"[gpu] {w.name}: layer-local done {time.time() - t0:.1f}s", flush=True)
+    # ---- head on the device's final residual, every logit row (the 2e-2 bar)
+    stats["head"] = head_all_rows(w, W, x_all, lg, ids)
+    print(f"[gpu] {w.name}: head {stats['head']}", flush=True)
     t2 = time.time()
-    # ---- end to end from token ids
-    out, *_ = oracle_run(w, subset)
-    st = compare_logits(lg[dev_rows], ids[dev_rows], out["z"], tol=E2E_BOUND)
-    stats["e2e"] = st
-    print(f"[gpu] {w.name}: {stats} device {t1 - t0:.1f}s oracle {time.time() - t1:.1f}s", flush=True)
+    # ---- end to end from token ids on the sampled sequences
+    stats["e2e"], *_ = e2e_compare(w, lg, ids, subset)
+    print(f"[gpu] {w.name}: {stats} device {t1 - t0:.1f}s head {t2 - t1:.1f}s e2e {time.time() - t2:.1f}s",
+          flush=True)
     d.release()
     return stats
-
-
-def logit_rows_local(w, idx, sub):
-    """Rows of the sub-batch that return logits."""
-    if all(s.q_len == 1 for s in w.seqs):
-        return np.arange(len(idx))
-    return np.asarray([int(sub["cu_q"][j + 1]) - 1 for j, i in enumerate(idx) if w.seqs[i].logits])
-
-
-def oracle_run_rows(w, idx):
-    """Device output rows of the sampled sequences (same mapping as oracle_run)."""
-    if all(s.q_len == 1 for s in w.seqs):
-        return None, None, None, None, np.asarray(idx)
-    out_pos, k = {}, 0
-    for i, s in enumerate(w.seqs):
-        if s.logits:
-            out_pos[i] = k
-            k += 1
-    return None, None, None, None, np.asarray([out_pos[i] for i in idx if w.seqs[i].logits])
 
 
 def _isolated_paths(w, subset):

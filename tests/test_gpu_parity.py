@@ -13,7 +13,7 @@ torch = pytest.importorskip("torch")
 from workloads.configs import (ModelCfg, SeqSpec, Workload, decode_workload, mixed_workload,  # noqa: E402
                                prefix_groups_workload, workload)
 
-from helpers import compare_logits, oracle_run  # noqa: E402
+from helpers import e2e_compare  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -37,8 +37,10 @@ def _run(w, **kw):
 
 
 def _check(w, lg, ids, subset=None, **kw):
-    out, kv, sub, idx, dev_rows = oracle_run(w, subset, **kw)
-    return compare_logits(lg[dev_rows], ids[dev_rows], out["z"]), out, kv, sub, idx
+    """End to end against the oracle: the 2e-2 bar, widened per row only where
+    the oracle's own float32 run drifts further (helpers.compare_logits)."""
+    st, out, kv, sub, idx, dev_rows = e2e_compare(w, lg, ids, subset, **kw)
+    return st, out, kv, sub, idx
 
 
 def test_config1_tiny_decode():
@@ -132,14 +134,16 @@ def test_mid_qkv_k_splits(cfg, B, target):
     order by the kernel that applies rotary and writes q and the KV slots):
     no split (-1), the default (0), and 2 to 8 splits.
 
-    MID: logits end to end within the 2e-2 bar, and a replay bit-exact.
-    WIDE (hidden 2048, logits ~2x MID's): the layer-local checks of the
-    full-size tests -- each layer's new K,V within one bf16 ulp of the oracle
-    applied to the device's own input residual (the values the split
-    reduction writes), the residual after it, and the 2e-2 bar on the head.
-    End to end this batch of 100 rows has one logit 0.0202 from the oracle
-    with and without the split (z = 2.239, the device one bf16 ulp below its
-    rounding), so the bar is held where the full-size tests hold it."""
+    MID: logits end to end, and a replay bit-exact.
+    WIDE (hidden 2048, logits ~2x MID's): the checks of the full-size tests --
+    each layer's new K,V within one bf16 ulp of the oracle applied to the
+    device's own input residual (the values the split reduction writes), the
+    residual after it, the 2e-2 bar on the head of every row, and end to end.
+    End to end, one rounding flip of a query element in layer 1 moves the
+    oracle's own float32 run by 0.013-0.014 on some of these rows (measured:
+    10 attention outputs, then 40 MLP inputs, 482 SwiGLU products and 566
+    final-norm outputs change by one ulp), so those rows take the
+    float32-spread bound of compare_logits."""
     from paper_2609_37062_amd.runner import DeviceRun
     model = MID if cfg == "mid" else WIDE
     ctx = np.random.default_rng(300 + B).integers(0, 400, size=B)

@@ -14,7 +14,7 @@ torch = pytest.importorskip("torch")
 
 from workloads.configs import ModelCfg, decode_workload  # noqa: E402
 
-from helpers import LOGIT_TOL, compare_logits, oracle_run, oracle_state  # noqa: E402
+from helpers import LOGIT_TOL, e2e_compare, oracle_state  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -55,8 +55,7 @@ def test_step_matches_oracle(B):
     d = _device(w, PERSISTENT)
     lg, ids = _step(d)
     assert d.eng.exec_counters()[5] == 1, "the persistent kernel did not run"
-    out, kv, sub, idx, dev_rows = oracle_run(w)
-    st = compare_logits(lg[dev_rows], ids[dev_rows], out["z"])
+    st, out, kv, sub, idx, dev_rows = e2e_compare(w, lg, ids)
     # every row's new K,V at every layer (Invariant 1)
     for l in range(MIDP.n_layers):
         K, V = d.read_kv(l, sub["slot"])
@@ -133,8 +132,7 @@ def test_step_attention_splits(bps):
     w = decode_workload(MIDP, ctx, seed=11, name="midp-splits")
     d = _device(w, PERSISTENT, bps=bps)
     lg, ids = _step(d)
-    out, kv, sub, idx, dev_rows = oracle_run(w)
-    print(compare_logits(lg[dev_rows], ids[dev_rows], out["z"]))
+    print(e2e_compare(w, lg, ids)[0])
     d.release()
 
 
@@ -142,8 +140,7 @@ def test_step_shared_prefix():
     w = _workload(14, seed=51, lo=3, hi=40, shared=256)
     d = _device(w, PERSISTENT)
     lg, ids = _step(d)
-    out, kv, sub, idx, dev_rows = oracle_run(w)
-    print(compare_logits(lg[dev_rows], ids[dev_rows], out["z"]))
+    print(e2e_compare(w, lg, ids)[0])
     d.release()
 
 

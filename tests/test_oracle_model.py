@@ -209,3 +209,61 @@ def test_layer_range_composes_to_the_whole_pass():
     np.testing.assert_array_equal(full["x"], rest["x"])
     np.testing.assert_array_equal(full["z"], rest["z"])
     np.testing.assert_array_equal(kv1.K, kv2.K)
+
+
+# ---------------------------------------------------------------- float32 contract mode
+def _int_pass(m, variant, dtype, rows=5, seed=0):
+    from intcase import fresh_workload, int_overrides
+    from helpers import oracle_state
+    w = fresh_workload(m, rows, seed=seed)
+    W = GeneratedWeights(m, w.seed, overrides=int_overrides(m, variant, seed=seed))
+    a, batch, sub, r, kv, idx = oracle_state(w)
+    out = forward(m, W, kv, sub, w.tokens[r], np.arange(rows), want_hidden=True, dtype=dtype)
+    K, V = kv.read(0, sub["slot"])
+    return out, K, V
+
+
+@pytest.mark.parametrize("variant", ["qkv", "o", "mlp"])
+def test_f32_contract_mode_equals_float64_on_exact_inputs(variant):
+    """On inputs whose every sum is an exact integer (tests/intcase.py) the
+    float32 contract mode and the float64 definition must agree bit for bit:
+    any formula the float32 path states differently shows up here."""
+    m = PIN
+    o64, K64, V64 = _int_pass(m, variant, "f64")
+    o32, K32, V32 = _int_pass(m, variant, "f32")
+    np.testing.assert_array_equal(K32, K64)
+    np.testing.assert_array_equal(V32, V64)
+    np.testing.assert_array_equal(o32["x"], o64["x"])
+    assert np.all(K64 == np.round(K64)) and np.all(V64 == np.round(V64))
+    if variant == "qkv":
+        np.testing.assert_array_equal(o32["z"], o64["z"])
+        np.testing.assert_array_equal(o32["ids"], o64["ids"])
+        assert np.all(o64["z"] == np.round(o64["z"]))
+    else:
+        assert np.all(o64["x"] == np.round(o64["x"]))
+        assert np.abs(o64["x"] - np.round(o64["x"])).max() == 0 and np.abs(o64["x"]).max() > 2
+
+
+def test_f32_contract_mode_runs_in_float32_and_stays_close():
+    """On generic inputs the float32 mode differs from the float64 one (it is
+    not silently the same computation), holds float32 values only, and stays
+    close on a 2-layer model (a bf16 rounding flip moves some logits by a few
+    hundredths; the mean moves by much less)."""
+    m = PIN
+    W = GeneratedWeights(m, seed=41, cache=True)
+    tokens = np.random.default_rng(42).integers(0, m.vocab, size=30)
+    res = {}
+    for dt in ("f64", "f32"):
+        a = BlockAllocator(16, 16)
+        a.seq_create(0)
+        a.seq_set_blocks(0, list(range(2)), 0)
+        a.reserve(0, 30)
+        b = build_batch(a, [0], [30])
+        kv = PagedKV(m.n_layers, 16, m.n_kv_heads, m.head_dim)
+        res[dt] = forward(m, W, kv, b, tokens, np.arange(30), want_hidden=True, dtype=dt)
+    x32, z32 = res["f32"]["x"], res["f32"]["z"]
+    np.testing.assert_array_equal(x32, x32.astype(np.float32).astype(np.float64))
+    np.testing.assert_array_equal(z32, z32.astype(np.float32).astype(np.float64))
+    assert not np.array_equal(res["f64"]["x"], x32)
+    d = np.abs(z32 - res["f64"]["z"])
+    assert d.max() <= 0.1 and d.mean() <= 5e-3, (d.max(), d.mean())

@@ -37,6 +37,25 @@ class ModelCfg:
     max_pos: int = 8192
     weight_sigma: float = 0.02
     kv_sigma: float = 1.0
+    # routed mode: the last `routed_layers` layers are routed (0: the last
+    # half, as the paper's skipper routes the last 16 of 32), each with a
+    # SwiGLU projector of width proj_ffn (0: ffn / 16 rounded up to 64)
+    routed_layers: int = 0
+    proj_ffn: int = 0
+
+    @property
+    def n_routed(self):
+        return self.routed_layers or self.n_layers // 2
+
+    @property
+    def first_routed(self):
+        return self.n_layers - self.n_routed
+
+    @property
+    def proj_dim(self):
+        if self.proj_ffn:
+            return self.proj_ffn
+        return max(64, (self.ffn // 16 + 63) // 64 * 64)
 
     @property
     def q_dim(self):

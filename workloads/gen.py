@@ -146,6 +146,17 @@ def _threads() -> int:
     return max(1, min(16, n))
 
 
+_POOL = None
+
+
+def _pool() -> ThreadPoolExecutor:
+    """One worker pool for the process (starting threads per call is slow)."""
+    global _POOL
+    if _POOL is None:
+        _POOL = ThreadPoolExecutor(_threads())
+    return _POOL
+
+
 def bf16_bits_np(key: int, n: int, dist=("normal", 0.02), start: int = 0) -> np.ndarray:
     """n generated bf16 bit patterns (uint16) for elements start..start+n-1."""
     table = table_for(dist)
@@ -158,8 +169,28 @@ def bf16_bits_np(key: int, n: int, dist=("normal", 0.02), start: int = 0) -> np.
 
     starts = range(0, n, _CHUNK)
     if n > 4 * _CHUNK:
-        with ThreadPoolExecutor(_threads()) as ex:
-            list(ex.map(work, starts))
+        list(_pool().map(work, starts))
+    else:
+        for c0 in starts:
+            work(c0)
+    return out
+
+
+def bf16_values_np(key: int, n: int, dist=("normal", 0.02), start: int = 0, dtype=np.float64) -> np.ndarray:
+    """The same elements as bf16_bits_np, widened exactly to float64 (or float32),
+    chunk by chunk on the thread pool."""
+    table = table_for(dist)
+    vals = (table.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(dtype)
+    out = np.empty(n, dtype)
+
+    def work(c0):
+        c1 = min(n, c0 + _CHUNK)
+        h = hash_np(key, start + c0, c1 - c0)
+        np.take(vals, (h >> np.uint32(16)), out=out[c0:c1])
+
+    starts = range(0, n, _CHUNK)
+    if n > 4 * _CHUNK:
+        list(_pool().map(work, starts))
     else:
         for c0 in starts:
             work(c0)
