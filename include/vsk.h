@@ -204,6 +204,23 @@ int vsk_workspace_init(vsk_handle* h, void* ws_dev, size_t bytes, int32_t max_ro
 int vsk_decode_step(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int32_t* next_ids_dev,
                     void* ws_dev, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * decode step as vsk_decode_step, computing the same values with the same
+ * kernels, but with its workspace taken from a fixed device array inside
+ * the library (VSK_SCRATCH_BYTES per GPU, held from library load until the
+ * process ends) instead of a caller's buffer.  It allocates and frees
+ * nothing.  The batch must fit: a batch whose workspace would exceed
+ * VSK_SCRATCH_BYTES (many rows with long contexts) is rejected with
+ * VSK_E_ARG before any launch.  The array belongs to the device current at
+ * the call (the stream must be on it) and keeps the last call's contents;
+ * every call on a GPU shares it, so calls that overlap on one GPU (several
+ * streams, threads or handles) race.  vsk_residual_copy reads the bound
+ * workspace, not this array. */
+#define VSK_SCRATCH_BYTES (64u * 1024u * 1024u)
+int vsk_decode_step_scratch(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int32_t* next_ids_dev,
+                            void* stream);
+
 /* One ragged pass over the uploaded batch (any q_lens: chunked prefill rows
  * and decode rows together).  The paper's prefill passes carry one row per
  * prompt token (Section 3.1, Prefill paragraph) and are compute-bound

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -56,7 +57,7 @@ PackedLayout packed_layout(const vsk_model_cfg& c) {
 
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len) {
+WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len, bool with_step) {
   WsLayout w;
   w.max_rows = max_rows;
   w.max_seqs = max_seqs;
@@ -89,7 +90,7 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
   // persistent decode step: every per-layer buffer is written once per launch
-  w.step = max_rows <= kStepMaxRows && step_shape_ok(c);
+  w.step = with_step && max_rows <= kStepMaxRows && step_shape_ok(c);
   if (w.step) {
     const size_t L = c.n_layers, nx = 2 * L + 1, R = max_rows;
     w.s_x = o; o = align_up(o + nx * R * H * 4);
@@ -517,6 +518,71 @@ int vsk_decode_step(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int
   if (h->exec_mode == 2 && !step_eligible(*h, a))
     return fail(h, VSK_E_UNSUPPORTED, "the persistent step kernel does not cover this pass (rows, shape or device)");
   return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "decode step");
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ scratch entry point
+// vsk_decode_step_scratch takes its workspace from this file-scope device
+// array instead of a caller's buffer.  Every GPU the library runs on holds
+// its own copy (VSK_SCRATCH_BYTES, zero at load) until the process ends.  In
+// host code `scratch` names a host-side stand-in, never the device memory:
+// the device address is looked up once per device with hipGetSymbolAddress
+// and only that pointer is handed to kernels.
+static __device__ __align__(256) uint8_t scratch[VSK_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of the current device's scratch array (looked up on the
+// first call on that device).
+hipError_t scratch_base(uint8_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = static_cast<uint8_t*>(g_scratch_ptr[dev]);
+  return hipSuccess;
+}
+}  // namespace
+
+extern "C" {
+
+int vsk_decode_step_scratch(vsk_handle* h, const int32_t* ids_dev, void* logits_dev, int32_t* next_ids_dev,
+                            void* stream) {
+  if (!h) return VSK_E_ARG;
+  if (!h->packed) return fail(h, VSK_E_STATE, "no weights bound");
+  if (!h->pool) return fail(h, VSK_E_STATE, "no KV pool bound");
+  if (!h->batch_uploaded) return fail(h, VSK_E_STATE, "no batch uploaded");
+  if (!ids_dev || !logits_dev) return fail(h, VSK_E_ARG, "null buffer");
+  const BatchDev& b = h->bd;
+  if (b.max_q_len != 1) return fail(h, VSK_E_ARG, "decode_step needs one row per sequence");
+  if (b.max_kv_len > h->cfg.max_pos) return fail(h, VSK_E_RANGE, "position beyond max_pos");
+  // the workspace of exactly this batch, without the persistent kernel's region
+  const WsLayout wl = ws_layout(h->cfg, b.n_rows, b.n_seqs, b.max_kv_len, false);
+  if (wl.total > static_cast<size_t>(VSK_SCRATCH_BYTES))
+    return fail(h, VSK_E_ARG, "the batch needs " + std::to_string(wl.total) + " bytes of scratch, more than the " +
+                                  std::to_string(static_cast<size_t>(VSK_SCRATCH_BYTES)) + " of vsk_decode_step_scratch");
+  uint8_t* base = nullptr;
+  hipError_t e = scratch_base(&base);
+  if (e != hipSuccess) return hip_check(h, e, "scratch address");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the attention arrival counters must start at zero; the layout (and so
+  // their place) follows the batch, and the array keeps the last call's bytes
+  e = launch_fill_zero(base + wl.att_cnt, static_cast<size_t>(b.n_rows) * h->cfg.n_kv_heads * 4, s);
+  if (e != hipSuccess) return hip_check(h, e, "scratch counters");
+  PassArgs a{ids_dev, nullptr, b.n_rows, static_cast<uint16_t*>(logits_dev), next_ids_dev, base, wl};
+  return hip_check(h, run_pass(*h, a, s), "decode step (scratch)");
 }
 
 int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logit_rows_dev, int32_t n_logit_rows,

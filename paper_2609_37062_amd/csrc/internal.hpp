@@ -178,7 +178,10 @@ struct Handle {
   int64_t counters[8] = {0};
 };
 
-WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len);
+// with_step: include the persistent step kernel's region when the capacity
+// and the model shape allow it
+WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len,
+                   bool with_step = true);
 
 
 // ---------------------------------------------------------------- launchers

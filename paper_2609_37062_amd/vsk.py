@@ -17,6 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libvsk.so")
 
 VSK_OK = 0
+SCRATCH_BYTES = 64 * 1024 * 1024  # VSK_SCRATCH_BYTES in vsk.h
 STATUS = {0: "OK", -1: "ARG", -2: "NOMEM", -3: "RANGE", -4: "SHARED_WRITE", -5: "STATE", -6: "HIP",
           -7: "UNSUPPORTED"}
 
@@ -82,6 +83,7 @@ SIGNATURES = [
     ("vsk_workspace_bytes", _SZ, [_VP, _I32, _I32, _I32]),
     ("vsk_workspace_init", C.c_int, [_VP, _VP, _SZ, _I32, _I32, _I32, _VP]),
     ("vsk_decode_step", C.c_int, [_VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    ("vsk_decode_step_scratch", C.c_int, [_VP, _VP, _VP, _VP, _VP]),
     ("vsk_prefill_chunk", C.c_int, [_VP, _VP, _VP, _I32, _VP, _VP, _VP, _SZ, _VP]),
     ("vsk_argmax_sample", C.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
     ("vsk_set_tuning", C.c_int, [_VP, _I32, _I32]),
@@ -313,6 +315,10 @@ class Engine:
     def decode_step(self, ids_ptr, logits_ptr, next_ids_ptr, ws_ptr, ws_bytes, stream=None):
         self._ck(lib().vsk_decode_step(self.h, ids_ptr, logits_ptr, next_ids_ptr, ws_ptr, ws_bytes, stream),
                  "decode_step")
+
+    def decode_step_scratch(self, ids_ptr, logits_ptr, next_ids_ptr, stream=None):
+        self._ck(lib().vsk_decode_step_scratch(self.h, ids_ptr, logits_ptr, next_ids_ptr, stream),
+                 "decode_step_scratch")
 
     def prefill_chunk(self, ids_ptr, logit_rows_ptr, n_logit_rows, logits_ptr, next_ids_ptr, ws_ptr, ws_bytes,
                       stream=None):
