@@ -245,6 +245,53 @@ int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logi
 int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab,
                       int32_t* ids_dev, void* stream);
 
+/* ----------------------------------------------------------------- routed mode
+ * One routed layer per Algorithm 1 (Section 3.1, "Route-Guided Cohort
+ * Execution"; appendix "Route-Guided Cohort Execution at the Kernel Level").
+ * The routed layers are first_routed..n_layers-1 (the paper's skipper routes
+ * the last 16 of 32).  Each has a projector: a SwiGLU block of width proj_ffn
+ * (p_gate, p_up [proj_ffn][hidden], p_down [hidden][proj_ffn]) that a
+ * Project-Only row runs instead of the MLP.
+ *
+ * A routed pass takes a route tape (device memory, caller-owned): run
+ * uint8 [n_routed][n_rows] (1 RUN, 0 Project-Only) and w float
+ * [n_routed][n_rows].  In a routed layer every row writes its own K,V
+ * (Invariant 1); a Project-Only row reads no KV and its attention output is
+ * zero (the attention launch keeps its shape); then, with X the layer's
+ * normalised MLP input, a RUN row adds w * MLP(X) and a Project-Only row
+ * (1 - w) * projector(X) to the residual.  The device builds the cohort maps
+ * and counts from the tape on every pass (Invariant 2); each cohort's GEMMs
+ * are launched for the whole batch and every tile at or beyond the cohort's
+ * count exits at once, so a cohort with no rows reads no weights.  A RUN row
+ * with w = 1 computes what the dense pass computes.  Layers before
+ * first_routed run dense.  The persistent step kernel (tuning key 2 = 2)
+ * has no routed mode (VSK_E_UNSUPPORTED). */
+size_t vsk_routed_weight_bytes(const vsk_model_cfg* cfg, int32_t first_routed, int32_t proj_ffn);
+/* Bind the projector weights' packed buffer (device, caller-owned, at least
+ * vsk_routed_weight_bytes; 256-byte aligned).  first_routed in
+ * [0, n_layers); proj_ffn a multiple of 64 in [64, ffn].  The workspace must
+ * then be sized (vsk_workspace_bytes) and initialised again: a routed
+ * workspace holds the Project-Only cohort's operands, both cohorts'
+ * products and the maps. */
+int vsk_routed_bind(vsk_handle* h, int32_t first_routed, int32_t proj_ffn, void* packed_dev, size_t bytes);
+/* Repack one routed layer's projector from logical [out][in] bf16. */
+int vsk_routed_pack_layer(vsk_handle* h, int32_t layer, const void* p_gate_dev, const void* p_up_dev,
+                          const void* p_down_dev, void* stream);
+/* vsk_decode_step / vsk_prefill_chunk in routed mode (arguments as there, plus
+ * the route tape run_dev, w_dev described above). */
+int vsk_decode_step_routed(vsk_handle* h, const int32_t* ids_dev, const uint8_t* run_dev, const float* w_dev,
+                           void* logits_dev, int32_t* next_ids_dev, void* ws_dev, size_t ws_bytes, void* stream);
+int vsk_prefill_chunk_routed(vsk_handle* h, const int32_t* ids_dev, const uint8_t* run_dev, const float* w_dev,
+                             const int32_t* logit_rows_dev, int32_t n_logit_rows, void* logits_dev,
+                             int32_t* next_ids_dev, void* ws_dev, size_t ws_bytes, void* stream);
+/* Inspection: copy the maps the last routed pass built (device pointers,
+ * each nullable): run_dev and proj_dev int32 [n_routed][n_rows] (the rows of
+ * each cohort in row order, first n_r / n_p entries valid), inv_dev int32
+ * [n_routed][n_rows] (each row's position in its cohort), cnt_dev int32
+ * [n_routed][2] (n_r, n_p). */
+int vsk_route_maps_read(vsk_handle* h, int32_t* run_dev, int32_t* proj_dev, int32_t* inv_dev, int32_t* cnt_dev,
+                        void* stream);
+
 /* ----------------------------------------------------------------- mode switch
  * Profitability-aware mode switching (Section 3.3; appendix "The Switching
  * Thresholds from the Roofline", decode rule and served thresholds).  Host

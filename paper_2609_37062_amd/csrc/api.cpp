@@ -57,7 +57,8 @@ PackedLayout packed_layout(const vsk_model_cfg& c) {
 
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len, bool with_step) {
+WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len, bool with_step,
+                   bool routed) {
   WsLayout w;
   w.max_rows = max_rows;
   w.max_seqs = max_seqs;
@@ -89,6 +90,21 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   // lm_head argmax partials: n_groups x rows
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
+  // routed layers: the Project-Only cohort's operands (the projector is at
+  // most ffn wide), both cohorts' down-projection products, and the maps
+  w.routed = routed;
+  if (routed) {
+    const size_t L = c.n_layers, R = max_rows;
+    const size_t yrows = std::max<size_t>(static_cast<size_t>(kMaxResidSplits) * std::min(max_rows, 128), R);
+    w.fb_po = o; o = align_up(o + Rp * H * 2);
+    w.fc_po = o; o = align_up(o + Rp * F * 2);
+    w.y_run = o; o = align_up(o + yrows * H * 4);
+    w.y_po = o; o = align_up(o + yrows * H * 4);
+    w.r_run = o; o = align_up(o + L * R * 4);
+    w.r_proj = o; o = align_up(o + L * R * 4);
+    w.r_inv = o; o = align_up(o + L * R * 4);
+    w.r_cnt = o; o = align_up(o + L * 2 * 4);
+  }
   // persistent decode step: every per-layer buffer is written once per launch
   w.step = with_step && max_rows <= kStepMaxRows && step_shape_ok(c);
   if (w.step) {
@@ -476,7 +492,7 @@ int vsk_batch_upload(vsk_handle* h, void* meta_dev, size_t bytes, void* stream) 
 // ------------------------------------------------------------------ passes
 size_t vsk_workspace_bytes(const vsk_handle* h, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len) {
   if (!h || max_rows <= 0 || max_seqs <= 0 || max_kv_len <= 0) return 0;
-  return ws_layout(h->cfg, max_rows, max_seqs, max_kv_len).total;
+  return ws_layout(h->cfg, max_rows, max_seqs, max_kv_len, true, h->routed_w != nullptr).total;
 }
 
 int vsk_workspace_init(vsk_handle* h, void* ws_dev, size_t bytes, int32_t max_rows, int32_t max_seqs,
@@ -484,7 +500,7 @@ int vsk_workspace_init(vsk_handle* h, void* ws_dev, size_t bytes, int32_t max_ro
   if (!h || !ws_dev) return VSK_E_ARG;
   if (max_rows <= 0 || max_seqs <= 0 || max_kv_len <= 0) return fail(h, VSK_E_ARG, "capacity must be positive");
   if (reinterpret_cast<uintptr_t>(ws_dev) % kAlign) return fail(h, VSK_E_ARG, "workspace not aligned");
-  const WsLayout wl = ws_layout(h->cfg, max_rows, max_seqs, max_kv_len);
+  const WsLayout wl = ws_layout(h->cfg, max_rows, max_seqs, max_kv_len, true, h->routed_w != nullptr);
   if (bytes < wl.total) return fail(h, VSK_E_ARG, "workspace smaller than vsk_workspace_bytes()");
   hipError_t e = launch_fill_zero(ws_dev, wl.total, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_check(h, e, "workspace init");
@@ -595,6 +611,118 @@ int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logi
              static_cast<uint8_t*>(ws_dev), h->wl};
   if (h->exec_mode == 2) return fail(h, VSK_E_UNSUPPORTED, "the persistent step kernel serves decode passes only");
   return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "prefill chunk");
+}
+
+// ------------------------------------------------------------------ routed mode
+static size_t routed_layer_bytes(const vsk_model_cfg& c, int32_t proj_ffn, size_t* pgu, size_t* pd) {
+  const size_t H = c.hidden, Fp = proj_ffn;
+  size_t o = 0;
+  if (pgu) *pgu = o;
+  o = align_up(o + 2 * Fp * H * 2);
+  if (pd) *pd = o;
+  o = align_up(o + H * Fp * 2);
+  return o;
+}
+
+static bool routed_cfg_ok(const vsk_model_cfg& c, int32_t first_routed, int32_t proj_ffn, std::string& why) {
+  if (first_routed < 0 || first_routed >= c.n_layers) { why = "first routed layer out of range"; return false; }
+  if (proj_ffn < 64 || proj_ffn % 64 != 0 || proj_ffn > c.ffn) {
+    why = "projector width must be a multiple of 64 in [64, ffn]";
+    return false;
+  }
+  return true;
+}
+
+size_t vsk_routed_weight_bytes(const vsk_model_cfg* cfg, int32_t first_routed, int32_t proj_ffn) {
+  std::string why;
+  if (!cfg_ok(cfg, why) || !routed_cfg_ok(*cfg, first_routed, proj_ffn, why)) return 0;
+  return routed_layer_bytes(*cfg, proj_ffn, nullptr, nullptr) * (cfg->n_layers - first_routed);
+}
+
+int vsk_routed_bind(vsk_handle* h, int32_t first_routed, int32_t proj_ffn, void* packed_dev, size_t bytes) {
+  if (!h) return VSK_E_ARG;
+  std::string why;
+  if (!routed_cfg_ok(h->cfg, first_routed, proj_ffn, why)) return fail(h, VSK_E_ARG, why);
+  const size_t need = vsk_routed_weight_bytes(&h->cfg, first_routed, proj_ffn);
+  if (!packed_dev || bytes < need) return fail(h, VSK_E_ARG, "projector weight buffer too small");
+  if (reinterpret_cast<uintptr_t>(packed_dev) % kAlign) return fail(h, VSK_E_ARG, "projector buffer not aligned");
+  h->routed_w = static_cast<uint8_t*>(packed_dev);
+  h->first_routed = first_routed;
+  h->proj_ffn = proj_ffn;
+  h->routed_layer_bytes = routed_layer_bytes(h->cfg, proj_ffn, &h->routed_pgu, &h->routed_pd);
+  h->ws = nullptr;  // the workspace layout grows: it must be sized and bound again
+  h->ws_bytes = 0;
+  return VSK_OK;
+}
+
+int vsk_routed_pack_layer(vsk_handle* h, int32_t layer, const void* p_gate_dev, const void* p_up_dev,
+                          const void* p_down_dev, void* stream) {
+  if (!h) return VSK_E_ARG;
+  if (!h->routed_w) return fail(h, VSK_E_STATE, "no projector weight buffer bound");
+  if (layer < h->first_routed || layer >= h->cfg.n_layers) return fail(h, VSK_E_RANGE, "not a routed layer");
+  if (!p_gate_dev || !p_up_dev || !p_down_dev) return fail(h, VSK_E_ARG, "null weight pointer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* base = h->routed_w + h->routed_layer_bytes * (layer - h->first_routed);
+  const int H = h->cfg.hidden, Fp = h->proj_ffn;
+  auto u16 = [](const void* p) { return static_cast<const uint16_t*>(p); };
+  hipError_t e;
+  if ((e = launch_pack(u16(p_gate_dev), u16(p_up_dev), nullptr, Fp, Fp, 2 * Fp, H, 2, h->cfg.head_dim, 0,
+                       reinterpret_cast<uint16_t*>(base + h->routed_pgu), s)) != hipSuccess)
+    return hip_check(h, e, "pack projector gate/up");
+  if ((e = launch_pack(u16(p_down_dev), nullptr, nullptr, H, 0, H, Fp, 0, h->cfg.head_dim, 0,
+                       reinterpret_cast<uint16_t*>(base + h->routed_pd), s)) != hipSuccess)
+    return hip_check(h, e, "pack projector down");
+  return VSK_OK;
+}
+
+static int routed_common(vsk_handle* h, const uint8_t* run_dev, const float* w_dev) {
+  if (!h->routed_w) return fail(h, VSK_E_STATE, "no projector weights bound (vsk_routed_bind)");
+  if (!h->wl.routed) return fail(h, VSK_E_STATE, "workspace sized before vsk_routed_bind: initialise it again");
+  if (!run_dev || !w_dev) return fail(h, VSK_E_ARG, "null route tape");
+  if (h->exec_mode == 2) return fail(h, VSK_E_UNSUPPORTED, "the persistent step kernel has no routed mode");
+  return VSK_OK;
+}
+
+int vsk_decode_step_routed(vsk_handle* h, const int32_t* ids_dev, const uint8_t* run_dev, const float* w_dev,
+                           void* logits_dev, int32_t* next_ids_dev, void* ws_dev, size_t ws_bytes, void* stream) {
+  int st = pass_common(h, ids_dev, logits_dev, ws_dev, ws_bytes);
+  if (st != VSK_OK) return st;
+  if ((st = routed_common(h, run_dev, w_dev)) != VSK_OK) return st;
+  if (h->bd.max_q_len != 1) return fail(h, VSK_E_ARG, "decode_step needs one row per sequence");
+  PassArgs a{ids_dev, nullptr, h->bd.n_rows, static_cast<uint16_t*>(logits_dev), next_ids_dev,
+             static_cast<uint8_t*>(ws_dev), h->wl, run_dev, w_dev};
+  return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "routed decode step");
+}
+
+int vsk_prefill_chunk_routed(vsk_handle* h, const int32_t* ids_dev, const uint8_t* run_dev, const float* w_dev,
+                             const int32_t* logit_rows_dev, int32_t n_logit_rows, void* logits_dev,
+                             int32_t* next_ids_dev, void* ws_dev, size_t ws_bytes, void* stream) {
+  int st = pass_common(h, ids_dev, logits_dev, ws_dev, ws_bytes);
+  if (st != VSK_OK) return st;
+  if ((st = routed_common(h, run_dev, w_dev)) != VSK_OK) return st;
+  if (!logit_rows_dev || n_logit_rows < 1 || n_logit_rows > h->bd.n_rows)
+    return fail(h, VSK_E_ARG, "logit rows must be 1..n_rows");
+  PassArgs a{ids_dev, logit_rows_dev, n_logit_rows, static_cast<uint16_t*>(logits_dev), next_ids_dev,
+             static_cast<uint8_t*>(ws_dev), h->wl, run_dev, w_dev};
+  return hip_check(h, run_pass(*h, a, static_cast<hipStream_t>(stream)), "routed prefill chunk");
+}
+
+int vsk_route_maps_read(vsk_handle* h, int32_t* run_dev, int32_t* proj_dev, int32_t* inv_dev, int32_t* cnt_dev,
+                        void* stream) {
+  if (!h) return VSK_E_ARG;
+  if (!h->ws || !h->wl.routed) return fail(h, VSK_E_STATE, "no routed workspace bound");
+  if (!h->batch_uploaded) return fail(h, VSK_E_STATE, "no batch uploaded");
+  const size_t Lr = static_cast<size_t>(h->cfg.n_layers - h->first_routed), R = h->bd.n_rows;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the maps are stored with the pass's row count as the stride of each layer
+  auto cp = [&](void* dst, size_t off, size_t n) {
+    return dst ? hipMemcpyAsync(dst, h->ws + off, n, hipMemcpyDeviceToDevice, s) : hipSuccess;
+  };
+  hipError_t e = cp(run_dev, h->wl.r_run, Lr * R * 4);
+  if (e == hipSuccess) e = cp(proj_dev, h->wl.r_proj, Lr * R * 4);
+  if (e == hipSuccess) e = cp(inv_dev, h->wl.r_inv, Lr * R * 4);
+  if (e == hipSuccess) e = cp(cnt_dev, h->wl.r_cnt, Lr * 2 * 4);
+  return hip_check(h, e, "route maps copy");
 }
 
 int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab, int32_t* ids_dev,
@@ -944,9 +1072,31 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape, rt);
   float* ypart = reinterpret_cast<float*>(ws + wl.ypart);
 
+  // routed pass (Algorithm 1): the maps of every routed layer, built on the
+  // device from the route tape before the first layer; per routed layer the
+  // MLP input is written per cohort, the RUN cohort runs the MLP and the
+  // Project-Only cohort the projector (count-bounded launches), and one
+  // kernel scatters both weighted products into the residual
+  const bool routed_pass = pa.tape_run != nullptr;
+  const int first_routed = routed_pass ? h.first_routed : c.n_layers;
+  const int Fp = h.proj_ffn;
+  uint16_t* fb_po = routed_pass ? reinterpret_cast<uint16_t*>(ws + wl.fb_po) : nullptr;
+  uint16_t* fc_po = routed_pass ? reinterpret_cast<uint16_t*>(ws + wl.fc_po) : nullptr;
+  int32_t* r_run = reinterpret_cast<int32_t*>(ws + wl.r_run);
+  int32_t* r_proj = reinterpret_cast<int32_t*>(ws + wl.r_proj);
+  int32_t* r_inv = reinterpret_cast<int32_t*>(ws + wl.r_inv);
+  int32_t* r_cnt = reinterpret_cast<int32_t*>(ws + wl.r_cnt);
+  if (routed_pass) TRY(launch_route_maps(pa.tape_run, c.n_layers - first_routed, R, r_run, r_proj, r_inv, r_cnt, s));
+  GemmPlan p_pgu, p_pd;
+  if (routed_pass) {
+    p_pgu = plan_gemm(2 * Fp, H, R, EPI_SWIGLU, h.gemm_shape);
+    p_pd = plan_gemm(H, Fp, R, EPI_RESID, h.gemm_shape, rt);
+  }
+  CohortOut cohort{};  // set for the MLP input of a routed layer
+
   // RMSNorm: one pass over x using the x^2 partials of the step that wrote it
   auto norm = [&](const uint16_t* gain, const float* xin, int rows, int rg, const double* sq, int parts) {
-    return launch_rmsnorm_frags(xin, gain, sq, parts, rows, H, c.rms_eps, fb, rg, s);
+    return launch_rmsnorm_frags(xin, gain, sq, parts, rows, H, c.rms_eps, fb, rg, s, cohort);
   };
   // a residual projection: in place (x += y, with x^2 partials), or with K
   // split over workgroups and the splits added by k_resid_norm, which also
@@ -959,7 +1109,8 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
       ga.ssq_out = nullptr;
       if ((re = probed(cls, [&](LaunchEvents ev) { return launch_gemm(ga, p, EPI_RESID, s, ev); })) != hipSuccess) return re;
       ga.ypart = nullptr;
-      if ((re = launch_resid_norm(x, ypart, p.ksplit, R, H, next_gain, c.rms_eps, fb, Rg, s)) != hipSuccess) return re;
+      if ((re = launch_resid_norm(x, ypart, p.ksplit, R, H, next_gain, c.rms_eps, fb, Rg, s, cohort)) != hipSuccess)
+        return re;
       normed = next_gain != nullptr;
     } else {
       ga.ypart = nullptr;
@@ -973,6 +1124,11 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ga.X = reinterpret_cast<const u4*>(fb);
   for (int l = 0; l < n_run; ++l) {
     const uint8_t* L = P + h.pl.layer_bytes * l;
+    const bool routed = l >= first_routed;
+    const int lr = l - first_routed;
+    const uint8_t* mask = routed ? pa.tape_run + static_cast<size_t>(lr) * R : nullptr;
+    aa.run_mask = mask;
+    pf.run_mask = mask;
     // attention block
     if (!normed) TRY(norm(norm_gain(l, false), x, R, Rg, ssq, ssq_parts));
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wqkv);
@@ -1013,9 +1169,57 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
     ga.X = reinterpret_cast<const u4*>(fa);
     ga.Kt = Nq / 32;
     ga.N = H;
+    // a routed layer's MLP input goes to its row's cohort, at its position there
+    if (routed) cohort = CohortOut{mask, r_inv + static_cast<size_t>(lr) * R, fb_po};
     TRY(resid(3, p_o, norm_gain(l, true)));
     // MLP block
     if (!normed) TRY(norm(norm_gain(l, true), x, R, Rg, ssq, ssq_parts));
+    cohort = CohortOut{};
+    if (routed) {
+      const int32_t* cnt = r_cnt + 2 * lr;
+      const uint8_t* Q = h.routed_w + h.routed_layer_bytes * lr;
+      const uint16_t* next_gain =
+          l + 1 < n_run ? norm_gain(l + 1, false) : (pa.logit_rows == nullptr ? final_gain : nullptr);
+      float* y_run = reinterpret_cast<float*>(ws + wl.y_run);
+      float* y_po = reinterpret_cast<float*>(ws + wl.y_po);
+      ga.ssq_out = nullptr;
+      ga.Kt = H / 32;
+      // RUN cohort: gate/up + SwiGLU over its n_r rows
+      ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wgu);
+      ga.X = reinterpret_cast<const u4*>(fb);
+      ga.N = 2 * F;
+      ga.out = fc;
+      ga.count = cnt;
+      TRY(probed(0, [&](LaunchEvents ev) { return launch_gemm(ga, p_gu, EPI_SWIGLU, s, ev); }));
+      // Project-Only cohort: the projector's gate/up + SwiGLU over its n_p rows
+      ga.W = reinterpret_cast<const u4*>(Q + h.routed_pgu);
+      ga.X = reinterpret_cast<const u4*>(fb_po);
+      ga.N = 2 * Fp;
+      ga.out = fc_po;
+      ga.count = cnt + 1;
+      TRY(launch_gemm(ga, p_pgu, EPI_SWIGLU, s));
+      // both down projections store their products (cohort order)
+      ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wd);
+      ga.X = reinterpret_cast<const u4*>(fc);
+      ga.Kt = F / 32;
+      ga.N = H;
+      ga.ypart = y_run;
+      ga.count = cnt;
+      TRY(probed(1, [&](LaunchEvents ev) { return launch_gemm(ga, p_d, EPI_RESID, s, ev); }));
+      ga.W = reinterpret_cast<const u4*>(Q + h.routed_pd);
+      ga.X = reinterpret_cast<const u4*>(fc_po);
+      ga.Kt = Fp / 32;
+      ga.ypart = y_po;
+      ga.count = cnt + 1;
+      TRY(launch_gemm(ga, p_pd, EPI_RESID, s));
+      ga.ypart = nullptr;
+      ga.count = nullptr;
+      // x[row] += w * y_run (RUN) or (1 - w) * y_po (Project-Only), then the next norm
+      TRY(launch_route_reduce_norm(x, y_run, p_d.ksplit, y_po, p_pd.ksplit, mask, r_inv + static_cast<size_t>(lr) * R,
+                                   pa.tape_w + static_cast<size_t>(lr) * R, R, H, next_gain, c.rms_eps, fb, Rg, s));
+      normed = next_gain != nullptr;
+      continue;
+    }
     ga.W = reinterpret_cast<const u4*>(L + h.pl.l.wgu);
     ga.X = reinterpret_cast<const u4*>(fb);
     ga.Kt = H / 32;

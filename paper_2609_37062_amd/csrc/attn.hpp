@@ -28,6 +28,9 @@ struct AttnArgs {
   const int32_t* pfx_blocks;  // [R]
   const int32_t* pfx_splits;  // [R]
   const int32_t* rows;        // nullable: the rows of the launch (grid z indexes it), else all rows
+  // routed layer (nullable): per row 1 RUN, 0 Project-Only; a Project-Only
+  // row reads no KV and its attention output is zero (Algorithm 1)
+  const uint8_t* run_mask;
 };
 
 // Causal attention of prefill rows (see k_attn_prefill).
@@ -44,6 +47,7 @@ struct AttnPrefillArgs {
   float scale_log2;
   uint16_t* out;  // o frags (K = Nq)
   int out_Rg;
+  const uint8_t* run_mask;  // routed layer (nullable): as in AttnArgs
 };
 
 // Shared-prefix attention: each work item reads a run of a group's prefix

@@ -176,6 +176,22 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   const int lane = tid & 63;
   const int w = tid >> 6;
   const int G = a.G;
+  // routed layer: a Project-Only row reads no KV and emits zero (its own K,V
+  // were written by the projection like every row's); split 0 stores it
+  if (a.run_mask != nullptr && a.run_mask[row] == 0) {
+    const int hz = lane & 15, qz = lane >> 4;
+    if (split == 0 && w == 0 && hz < G) {
+      const int col0 = (hk * G + hz) * D;
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) {
+        const size_t i0 = frag_index(row, col0 + 16 * c + 4 * qz, a.out_Rg);
+        const u32x2 zero = u32x2{0u, 0u};
+        if constexpr (WT) store_wt(a.out + i0, zero);
+        else *reinterpret_cast<u32x2*>(a.out + i0) = zero;
+      }
+    }
+    return;
+  }
   const int kv_len = a.pos[row] + 1;
   const int nb = (kv_len + kBlock - 1) / kBlock;
   // a shared prefix of P blocks is read by the prefix work items; this row's

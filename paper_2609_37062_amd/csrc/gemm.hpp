@@ -26,6 +26,7 @@ struct GemmArgs {
   float* am_val;       // LOGITS: [n_groups][R]
   int* am_idx;
   float* ypart;  // RESID with K split over workgroups: y[split][R][N] instead of x += y
+  const int* count;  // nullable: rows of this launch read on the device (<= R; a cohort's size)
 };
 
 struct GemmPlan {

@@ -103,6 +103,12 @@ struct WsLayout {
   int32_t max_rows = 0, max_seqs = 0, max_kv_len = 0, Rg = 0, max_splits = 0;
   size_t x, x_c, fa, fb, fc, q, att_o, att_ml, att_cnt, ssq, ssq_c, am_part, total;
   size_t ypart = 0;  // products of residual projections with K split over workgroups
+  // routed layers (present when `routed`): Project-Only cohort frags of the
+  // MLP input and of the SwiGLU product, both cohorts' down-projection
+  // products, and Algorithm 1's maps per layer (run, proj, inv [L][rows],
+  // counts [L][2])
+  bool routed = false;
+  size_t fb_po = 0, fc_po = 0, y_run = 0, y_po = 0, r_run = 0, r_proj = 0, r_inv = 0, r_cnt = 0;
   // persistent decode step (present when max_rows <= kStepMaxRows and the
   // model shape is covered): per-layer activations, sync flags, error word, epoch
   bool step = false;
@@ -170,6 +176,13 @@ struct Handle {
   uint8_t* ws = nullptr;
   size_t ws_bytes = 0;
   WsLayout wl;
+  // routed mode (Algorithm 1): the routed layers are first_routed..n_layers-1,
+  // each with a SwiGLU projector of width proj_ffn packed at `routed_w`
+  // (per routed layer: [gate/up interleaved 2*proj_ffn x hidden | down
+  // hidden x proj_ffn], each 256-byte aligned)
+  uint8_t* routed_w = nullptr;
+  int32_t first_routed = -1, proj_ffn = 0;
+  size_t routed_layer_bytes = 0, routed_pgu = 0, routed_pd = 0;
   // timing probes per kernel class
   static constexpr int kProbeClasses = 6;
   std::vector<hipEvent_t> probe_b[kProbeClasses], probe_e[kProbeClasses];
@@ -181,7 +194,7 @@ struct Handle {
 // with_step: include the persistent step kernel's region when the capacity
 // and the model shape allow it
 WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, int32_t max_kv_len,
-                   bool with_step = true);
+                   bool with_step = true, bool routed = false);
 
 
 // ---------------------------------------------------------------- launchers
@@ -204,6 +217,10 @@ struct PassArgs {
   int32_t* next_ids;
   uint8_t* ws;
   WsLayout wl;
+  // routed pass (nullable): route tape of the routed layers, run [L_r][rows]
+  // (1 RUN, 0 Project-Only) and weights w [L_r][rows]
+  const uint8_t* tape_run = nullptr;
+  const float* tape_w = nullptr;
 };
 hipError_t run_pass(Handle& h, const PassArgs& a, hipStream_t s);
 // True when run_pass would take the persistent step kernel for this pass.

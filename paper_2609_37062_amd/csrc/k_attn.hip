@@ -315,14 +315,18 @@ __global__ __launch_bounds__(64 * (kPreTiles + 1)) void k_attn_prefill(AttnPrefi
   if (!(w < kPreTiles && 16 * w < n_cols)) return;
 
   if (cvalid) {
+    // a Project-Only row of a routed layer emits zero
+    const bool po = a.run_mask != nullptr && a.run_mask[row] == 0;
     const float inv = 1.f / l;
     const int col0 = (hk * G + qh) * D;
 #pragma unroll
     for (int k = 0; k < VC; ++k) {
       const int e = 16 * k + 4 * quad;
-      u32x2 pk;
-      pk[0] = pack_bf2(o[k][0] * inv, o[k][1] * inv);
-      pk[1] = pack_bf2(o[k][2] * inv, o[k][3] * inv);
+      u32x2 pk = u32x2{0u, 0u};
+      if (!po) {
+        pk[0] = pack_bf2(o[k][0] * inv, o[k][1] * inv);
+        pk[1] = pack_bf2(o[k][2] * inv, o[k][3] * inv);
+      }
       *reinterpret_cast<u32x2*>(a.out + frag_index(row, col0 + e, a.out_Rg)) = pk;
     }
   }

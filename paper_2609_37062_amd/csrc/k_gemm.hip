@@ -97,6 +97,11 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
   const bool split_out = EPI == EPI_RESID && a.ypart != nullptr;
   const int nt0 = (ng * WN + wn) * NT;
   const int g0 = mt * MG;
+  // rows of this launch: the pass's rows, or a cohort's count read on the
+  // device (Algorithm 1's count-bounded GEMMs: the grid is sized for the
+  // capacity and a tile starting at or beyond the count exits at once)
+  const int Rv = a.count != nullptr ? min(a.R, *a.count) : a.R;
+  if (16 * g0 >= Rv) return;
   const int rsub = lane & 15;
   const int nq = 4 * (lane >> 4);
 
@@ -155,7 +160,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
         for (int g = 0; g < MG; ++g) {
           const int row = 16 * (g0 + g) + rsub;
-          xv[j][g] = (tvalid[j] && row < a.R) ? *reinterpret_cast<const float4*>(a.x + static_cast<size_t>(row) * a.N + n0)
+          xv[j][g] = (tvalid[j] && row < Rv) ? *reinterpret_cast<const float4*>(a.x + static_cast<size_t>(row) * a.N + n0)
                                               : make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
@@ -163,8 +168,8 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
       for (int g = 0; g < MG; ++g) {
         const int row = 16 * (g0 + g) + rsub;
-        q_slot[g] = row < a.R ? a.slot[row] : 0;
-        q_pos[g] = row < a.R ? a.pos[row] : 0;
+        q_slot[g] = row < Rv ? a.slot[row] : 0;
+        q_pos[g] = row < Rv ? a.pos[row] : 0;
       }
     }
   };
@@ -180,7 +185,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
         for (int g = 0; g < MG; ++g) {
           const int row = 16 * (g0 + g) + rsub;
-          const bool ok = rot && row < a.R;
+          const bool ok = rot && row < Rv;
           const float2* rp = a.rope + static_cast<size_t>(q_pos[g]) * half + j0;
           q_cs[j][g][0] = ok ? rp[0] : make_float2(1.f, 0.f);
           q_cs[j][g][1] = ok ? rp[1] : make_float2(1.f, 0.f);
@@ -360,7 +365,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
           for (int g = 0; g < MG; ++g) {
             const int row = 16 * (g0 + g) + rsub;
-            if (!tvalid[j] || row >= a.R) continue;
+            if (!tvalid[j] || row >= Rv) continue;
             const int n0 = 16 * (nt0 + j) + nq;
             *reinterpret_cast<f32x4*>(a.ypart + (static_cast<size_t>(ks) * a.R + row) * a.N + n0) = acc[j][g];
           }
@@ -375,7 +380,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
         double ss = 0.0;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
-          if (!tvalid[j] || row >= a.R) continue;
+          if (!tvalid[j] || row >= Rv) continue;
           const int n0 = 16 * (nt0 + j) + nq;
           float4* px = reinterpret_cast<float4*>(a.x + static_cast<size_t>(row) * a.N + n0);
           float4 v = xv[j][g];
@@ -401,7 +406,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
         for (int w2 = 1; w2 < WN; ++w2) ss += s_ss[w2][g][l];
         const int row = 16 * (g0 + g) + l;
-        if (row < a.R) a.ssq_out[static_cast<size_t>(row) * gridDim.x + ng] = ss;  // [row][workgroup]
+        if (row < Rv) a.ssq_out[static_cast<size_t>(row) * gridDim.x + ng] = ss;  // [row][workgroup]
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
@@ -413,7 +418,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
         for (int g = 0; g < MG; ++g) {
           const int row = 16 * (g0 + g) + rsub;
-          if (row >= a.R) continue;
+          if (row >= Rv) continue;
           const float a0 = silu_f(acc[j][g][0]) * acc[j][g][2];
           const float a1 = silu_f(acc[j][g][1]) * acc[j][g][3];
           *reinterpret_cast<uint32_t*>(a.out + frag_index(row, 2 * u, a.out_Rg)) = pack_bf2(a0, a1);
@@ -429,7 +434,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
         for (int g = 0; g < MG; ++g) {
           const int row = 16 * (g0 + g) + rsub;
-          if (row >= a.R) continue;
+          if (row >= Rv) continue;
           qkv_store(a, row, n0, acc[j][g], q_slot[g], q_cs[j][g][0], q_cs[j][g][1]);
         }
       }
@@ -443,7 +448,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
         int bi = INT_MAX;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
-          if (!tvalid[j] || row >= a.R) continue;
+          if (!tvalid[j] || row >= Rv) continue;
           const int n0 = 16 * (nt0 + j) + nq;
           const f32x4 v = acc[j][g];
           uint2 packed;
@@ -475,7 +480,7 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 #pragma unroll
       for (int w2 = 1; w2 < WN; ++w2) am_merge(bv, bi, s_amv[w2][g][l], s_ami[w2][g][l]);
       const int row = 16 * (g0 + g) + l;
-      if (row < a.R) {
+      if (row < Rv) {
         a.am_val[static_cast<size_t>(ng) * a.R + row] = bv;
         a.am_idx[static_cast<size_t>(ng) * a.R + row] = bi;
       }

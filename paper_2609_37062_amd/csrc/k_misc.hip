@@ -88,9 +88,12 @@ hipError_t launch_gather_rows(const float* x_in, int R_in, const int32_t* rows, 
 // of them hold the same r, and the row is normalised in one pass over x.
 // One wave per 512 elements of a row: each lane writes 8 (one 16-byte frag
 // piece); the product is taken in double and rounded once.
+// Routed layer (rc.mask non-null): the row is written at its position in
+// its cohort, into hg for a RUN row and rc.po for a Project-Only row -- the
+// cohort gather of Algorithm 1 folded into the producer of the operand.
 __global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ x, const uint16_t* __restrict__ g,
                                                       const double* __restrict__ ssq, int parts, int R, int H,
-                                                      float eps, uint16_t* __restrict__ hg, int Rg) {
+                                                      float eps, uint16_t* __restrict__ hg, int Rg, CohortOut rc) {
   const int r = blockIdx.y;
   const int c = blockIdx.x * 512 + threadIdx.x * 8;
   const bool on = c < H;
@@ -123,7 +126,13 @@ __global__ __launch_bounds__(64) void k_rmsnorm_frags(const float* __restrict__ 
   for (int k = 0; k < 4; ++k)
     o[k] = d2bf(static_cast<double>(e[2 * k]) * bf2f(gv[k] & 0xffffu) * rr) |
            (d2bf(static_cast<double>(e[2 * k + 1]) * bf2f(gv[k] >> 16) * rr) << 16);
-  *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
+  int ro = r;
+  uint16_t* dst = hg;
+  if (rc.mask != nullptr) {
+    ro = rc.inv[r];
+    if (rc.mask[r] == 0) dst = rc.po;
+  }
+  *reinterpret_cast<u32x4*>(dst + frag_index(ro, c, Rg)) = o;
 }
 
 // ---------------------------------------------------------------- residual sum + RMSNorm
@@ -141,7 +150,7 @@ constexpr int kResidNormMaxSplits = 8;
 template <int NS>
 __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ x, const float* __restrict__ y, int splits,
                                                      int R, int H, const uint16_t* __restrict__ g, float eps,
-                                                     uint16_t* __restrict__ hg, int Rg) {
+                                                     uint16_t* __restrict__ hg, int Rg, CohortOut rc) {
   if constexpr (NS > 0) splits = NS;
   constexpr int kMax = NS > 0 ? NS : kResidNormMaxSplits;
   __shared__ double s_ss[16];
@@ -196,25 +205,177 @@ __global__ __launch_bounds__(1024) void k_resid_norm(float* __restrict__ x, cons
   for (int q = 0; q < 4; ++q)
     o[q] = d2bf(static_cast<double>(e[2 * q]) * bf2f(gv[q] & 0xffffu) * rr) |
            (d2bf(static_cast<double>(e[2 * q + 1]) * bf2f(gv[q] >> 16) * rr) << 16);
-  *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
+  int ro = r;
+  uint16_t* dst = hg;
+  if (rc.mask != nullptr) {  // routed layer: the row's place in its cohort
+    ro = rc.inv[r];
+    if (rc.mask[r] == 0) dst = rc.po;
+  }
+  *reinterpret_cast<u32x4*>(dst + frag_index(ro, c, Rg)) = o;
 }
 
 hipError_t launch_resid_norm(float* x, const float* y, int splits, int R, int H, const uint16_t* g, float eps,
-                             uint16_t* hg, int Rg, hipStream_t s) {
+                             uint16_t* hg, int Rg, hipStream_t s, CohortOut rc) {
   if (H % 8 != 0 || H > 8192 || splits < 1 || splits > kResidNormMaxSplits) return hipErrorInvalidValue;
   const int threads = (H / 8 + 63) / 64 * 64;
   switch (splits) {
-    case 2: hipLaunchKernelGGL(k_resid_norm<2>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg); break;
-    case 4: hipLaunchKernelGGL(k_resid_norm<4>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg); break;
-    case 8: hipLaunchKernelGGL(k_resid_norm<8>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg); break;
-    default: hipLaunchKernelGGL(k_resid_norm<0>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg);
+    case 2: hipLaunchKernelGGL(k_resid_norm<2>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg, rc); break;
+    case 4: hipLaunchKernelGGL(k_resid_norm<4>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg, rc); break;
+    case 8: hipLaunchKernelGGL(k_resid_norm<8>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg, rc); break;
+    default: hipLaunchKernelGGL(k_resid_norm<0>, dim3(R), dim3(threads), 0, s, x, y, splits, R, H, g, eps, hg, Rg, rc);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_rmsnorm_frags(const float* x, const uint16_t* g, const double* ssq, int parts, int R, int H,
-                                float eps, uint16_t* hg, int Rg, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm_frags, dim3((H + 511) / 512, R), dim3(64), 0, s, x, g, ssq, parts, R, H, eps, hg, Rg);
+                                float eps, uint16_t* hg, int Rg, hipStream_t s, CohortOut rc) {
+  hipLaunchKernelGGL(k_rmsnorm_frags, dim3((H + 511) / 512, R), dim3(64), 0, s, x, g, ssq, parts, R, H, eps, hg, Rg,
+                     rc);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- routed layers
+// Algorithm 1's maps, rebuilt on the device from the route tape for every
+// pass (Invariant 2): for each routed layer (one workgroup each), run[] and
+// proj[] list the batch rows of the RUN and Project-Only cohorts in row
+// order, inv[r] is row r's position in its own cohort, and cnt = (n_r, n_p).
+// A block-wide exclusive scan of the RUN flags over chunks of blockDim rows.
+__global__ __launch_bounds__(1024) void k_route_maps(const uint8_t* __restrict__ tape, int R,
+                                                     int32_t* __restrict__ run, int32_t* __restrict__ proj,
+                                                     int32_t* __restrict__ inv, int32_t* __restrict__ cnt) {
+  __shared__ int s_w[16];
+  __shared__ int s_base;
+  const int l = blockIdx.x;
+  const uint8_t* t = tape + static_cast<size_t>(l) * R;
+  run += static_cast<size_t>(l) * R;
+  proj += static_cast<size_t>(l) * R;
+  inv += static_cast<size_t>(l) * R;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  if (threadIdx.x == 0) s_base = 0;
+  __syncthreads();
+  for (int r0 = 0; r0 < R; r0 += blockDim.x) {
+    const int r = r0 + threadIdx.x;
+    const bool valid = r < R;
+    const bool is_run = valid && t[r] != 0;
+    const uint64_t bal = __ballot(is_run);
+    const int below = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) s_w[w] = __popcll(bal);
+    __syncthreads();
+    int before = s_base;
+    for (int i = 0; i < w; ++i) before += s_w[i];
+    int chunk = 0;
+    for (int i = 0; i < nw; ++i) chunk += s_w[i];
+    const int n_run_before = before + below;  // RUN rows before r
+    if (valid) {
+      if (is_run) {
+        run[n_run_before] = r;
+        inv[r] = n_run_before;
+      } else {
+        const int p = r - n_run_before;  // Project-Only rows before r
+        proj[p] = r;
+        inv[r] = p;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) s_base += chunk;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    cnt[2 * l] = s_base;
+    cnt[2 * l + 1] = R - s_base;
+  }
+}
+
+hipError_t launch_route_maps(const uint8_t* tape, int n_layers, int R, int32_t* run, int32_t* proj, int32_t* inv,
+                             int32_t* cnt, hipStream_t s) {
+  if (n_layers <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_route_maps, dim3(n_layers), dim3(1024), 0, s, tape, R, run, proj, inv, cnt);
+  return hipGetLastError();
+}
+
+// The end of a routed layer's MLP: one workgroup per batch row r adds its
+// cohort's down-projection product (the splits of that cohort's launch, in
+// split order, at row inv[r] of the cohort) to the residual with weight w[r]
+// for a RUN row and 1 - w[r] for a Project-Only one -- the weighted scatter
+// of Algorithm 1 -- and (gain non-null) normalises the row into bf16 frags
+// for the next layer as k_resid_norm does.  With every row RUN and w = 1 the
+// residual is the one k_resid_norm computes from the same products.
+__global__ __launch_bounds__(1024) void k_route_reduce_norm(float* __restrict__ x, const float* __restrict__ y_run,
+                                                            int s_run, const float* __restrict__ y_po, int s_po,
+                                                            const uint8_t* __restrict__ mask,
+                                                            const int32_t* __restrict__ inv,
+                                                            const float* __restrict__ wts, int R, int H,
+                                                            const uint16_t* __restrict__ g, float eps,
+                                                            uint16_t* __restrict__ hg, int Rg) {
+  __shared__ double s_ss[16];
+  const int r = blockIdx.x;
+  const int c = threadIdx.x * 8;
+  const bool on = c < H;
+  const bool is_run = mask[r] != 0;
+  const float* y = is_run ? y_run : y_po;
+  const int splits = is_run ? s_run : s_po;
+  const int m = inv[r];
+  const float wt = is_run ? wts[r] : 1.f - wts[r];
+  float* xr = x + static_cast<size_t>(r) * H + c;
+  float e[8];
+  u32x4 gv = u32x4{0u, 0u, 0u, 0u};
+  double ss = 0.0;
+  if (on) {
+    float4 a = *reinterpret_cast<const float4*>(xr);
+    float4 b = *reinterpret_cast<const float4*>(xr + 4);
+    float4 ya[kResidNormMaxSplits], yb[kResidNormMaxSplits];
+#pragma unroll
+    for (int sp = 0; sp < kResidNormMaxSplits; ++sp) {
+      if (sp < splits) {
+        const float* yr = y + (static_cast<size_t>(sp) * R + m) * H + c;
+        ya[sp] = *reinterpret_cast<const float4*>(yr);
+        yb[sp] = *reinterpret_cast<const float4*>(yr + 4);
+      }
+    }
+    if (g != nullptr) gv = *reinterpret_cast<const u32x4*>(g + c);
+    float4 sa = ya[0], sb = yb[0];
+#pragma unroll
+    for (int sp = 1; sp < kResidNormMaxSplits; ++sp) {
+      if (sp < splits) {
+        sa.x += ya[sp].x; sa.y += ya[sp].y; sa.z += ya[sp].z; sa.w += ya[sp].w;
+        sb.x += yb[sp].x; sb.y += yb[sp].y; sb.z += yb[sp].z; sb.w += yb[sp].w;
+      }
+    }
+    a.x += wt * sa.x; a.y += wt * sa.y; a.z += wt * sa.z; a.w += wt * sa.w;
+    b.x += wt * sb.x; b.y += wt * sb.y; b.z += wt * sb.z; b.w += wt * sb.w;
+    *reinterpret_cast<float4*>(xr) = a;
+    *reinterpret_cast<float4*>(xr + 4) = b;
+    e[0] = a.x; e[1] = a.y; e[2] = a.z; e[3] = a.w;
+    e[4] = b.x; e[5] = b.y; e[6] = b.z; e[7] = b.w;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) ss += static_cast<double>(e[q]) * e[q];
+  }
+  if (g == nullptr) return;
+#pragma unroll
+  for (int mm = 32; mm >= 1; mm >>= 1) ss += __shfl_xor(ss, mm, 64);
+  if ((threadIdx.x & 63) == 0) s_ss[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  double tot = 0.0;
+  for (int w = 0; w < static_cast<int>(blockDim.x >> 6); ++w) tot += s_ss[w];
+  const double rr = 1.0 / sqrt(tot / static_cast<double>(H) + static_cast<double>(eps));
+  if (!on) return;
+  u32x4 o;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    o[q] = d2bf(static_cast<double>(e[2 * q]) * bf2f(gv[q] & 0xffffu) * rr) |
+           (d2bf(static_cast<double>(e[2 * q + 1]) * bf2f(gv[q] >> 16) * rr) << 16);
+  *reinterpret_cast<u32x4*>(hg + frag_index(r, c, Rg)) = o;
+}
+
+hipError_t launch_route_reduce_norm(float* x, const float* y_run, int s_run, const float* y_po, int s_po,
+                                    const uint8_t* mask, const int32_t* inv, const float* wts, int R, int H,
+                                    const uint16_t* g, float eps, uint16_t* hg, int Rg, hipStream_t s) {
+  if (H % 8 != 0 || H > 8192 || s_run < 1 || s_run > kResidNormMaxSplits || s_po < 1 ||
+      s_po > kResidNormMaxSplits)
+    return hipErrorInvalidValue;
+  const int threads = (H / 8 + 63) / 64 * 64;
+  hipLaunchKernelGGL(k_route_reduce_norm, dim3(R), dim3(threads), 0, s, x, y_run, s_run, y_po, s_po, mask, inv, wts,
+                     R, H, g, eps, hg, Rg);
   return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ class DeviceRun:
     """One workload resident on the device: engine, packed weights, KV pool, batch, workspace."""
 
     def __init__(self, w: Workload, device="cuda", overrides=None, weight_dist=None, max_rows=None,
-                 max_kv_len=None, pool_blocks=None, poison_pool=False):
+                 max_kv_len=None, pool_blocks=None, poison_pool=False, routed=False):
         assert torch.cuda.is_available(), "a GPU is required"
         self.w = w
         self.m = w.model
@@ -45,6 +45,9 @@ class DeviceRun:
         self.overrides = dict(overrides or {})
         self.dist = weight_dist or ("normal", self.m.weight_sigma)
         self._load_weights()
+        self.routed = routed
+        if routed:
+            self._load_projectors()
         self.n_blocks = pool_blocks or w.n_pool_blocks
         self.pool = torch.empty(self.eng.kv_pool_bytes(self.n_blocks) // 2, dtype=torch.int16, device=self.device)
         if poison_pool:
@@ -101,6 +104,46 @@ class DeviceRun:
         g = self._tensor("final_norm", -1, (m.hidden,))
         self.eng.weights_pack_head(E.data_ptr(), Wl.data_ptr(), g.data_ptr(), self.sp)
         torch.cuda.synchronize(self.device)
+
+    def _load_projectors(self):
+        """Routed mode: pack every routed layer's projector (p_gate, p_up, p_down)."""
+        m = self.m
+        Fp, H = m.proj_dim, m.hidden
+        nbytes = self.eng.routed_weight_bytes(m.first_routed, Fp)
+        self._proj_t, self.proj = _dev_buffer(nbytes, self.device)
+        self.eng.routed_bind(m.first_routed, Fp, self.proj, nbytes)
+        for l in range(m.first_routed, m.n_layers):
+            t = {n: self._tensor(n, l, shp) for n, shp in (("p_gate", (Fp, H)), ("p_up", (Fp, H)),
+                                                             ("p_down", (H, Fp)))}
+            self.eng.routed_pack_layer(l, t["p_gate"].data_ptr(), t["p_up"].data_ptr(), t["p_down"].data_ptr(),
+                                       self.sp)
+            torch.cuda.synchronize(self.device)
+            del t
+
+    def set_route(self, run, w):
+        """Device copy of a route tape: run bool [n_routed][rows], w float [n_routed][rows]."""
+        self.tape_run = torch.from_numpy(np.ascontiguousarray(run, np.uint8)).to(self.device)
+        self.tape_w = torch.from_numpy(np.ascontiguousarray(w, np.float32)).to(self.device)
+
+    def step_routed(self, stream=None):
+        """One routed pass with the tape set by set_route."""
+        sp = self.sp if stream is None else stream
+        if all(q == 1 for q in self.q_lens):
+            self.eng.decode_step_routed(self.ids.data_ptr(), self.tape_run.data_ptr(), self.tape_w.data_ptr(),
+                                        self.logits.data_ptr(), self.next_ids.data_ptr(), self.ws, self.ws_bytes, sp)
+        else:
+            self.eng.prefill_chunk_routed(self.ids.data_ptr(), self.tape_run.data_ptr(), self.tape_w.data_ptr(),
+                                          self.logit_rows.data_ptr(), len(self.logit_rows), self.logits.data_ptr(),
+                                          self.next_ids.data_ptr(), self.ws, self.ws_bytes, sp)
+
+    def route_maps(self):
+        """(run, proj, inv [n_routed][rows], cnt [n_routed][2]) of the last routed pass."""
+        L, R = self.m.n_routed, self.w.n_rows
+        bufs = [torch.empty((L, R), dtype=torch.int32, device=self.device) for _ in range(3)]
+        cnt = torch.empty((L, 2), dtype=torch.int32, device=self.device)
+        self.eng.route_maps_read(*(b.data_ptr() for b in bufs), cnt.data_ptr(), self.sp)
+        torch.cuda.synchronize(self.device)
+        return tuple(b.cpu().numpy() for b in bufs) + (cnt.cpu().numpy(),)
 
     def seq_slots(self, i, p0, n):
         ln, table = self.eng.seq_info(i)

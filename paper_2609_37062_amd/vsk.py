@@ -88,6 +88,12 @@ SIGNATURES = [
     ("vsk_argmax_sample", C.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
     ("vsk_set_tuning", C.c_int, [_VP, _I32, _I32]),
     ("vsk_residual_copy", C.c_int, [_VP, _VP, _I32, _VP]),
+    ("vsk_routed_weight_bytes", _SZ, [C.POINTER(ModelCfg), _I32, _I32]),
+    ("vsk_routed_bind", C.c_int, [_VP, _I32, _I32, _VP, _SZ]),
+    ("vsk_routed_pack_layer", C.c_int, [_VP, _I32, _VP, _VP, _VP, _VP]),
+    ("vsk_decode_step_routed", C.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
+    ("vsk_prefill_chunk_routed", C.c_int, [_VP, _VP, _VP, _VP, _VP, _I32, _VP, _VP, _VP, _SZ, _VP]),
+    ("vsk_route_maps_read", C.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     ("vsk_switch_thresholds", C.c_int, [C.POINTER(SwitchParams), C.POINTER(SwitchThresholds)]),
     ("vsk_switch_step", C.c_int, [C.POINTER(SwitchThresholds), _I32, _I64, _PI32, _PI32]),
     ("vsk_switch_decode_mode", C.c_int, [_I32, _I32, _I32, _PI32]),
@@ -324,6 +330,29 @@ class Engine:
                       stream=None):
         self._ck(lib().vsk_prefill_chunk(self.h, ids_ptr, logit_rows_ptr, n_logit_rows, logits_ptr, next_ids_ptr,
                                          ws_ptr, ws_bytes, stream), "prefill_chunk")
+
+    # -- routed mode
+    def routed_weight_bytes(self, first_routed, proj_ffn):
+        return lib().vsk_routed_weight_bytes(C.byref(self.cfg), first_routed, proj_ffn)
+
+    def routed_bind(self, first_routed, proj_ffn, ptr, nbytes):
+        self._ck(lib().vsk_routed_bind(self.h, first_routed, proj_ffn, ptr, nbytes), "routed_bind")
+
+    def routed_pack_layer(self, layer, p_gate, p_up, p_down, stream=None):
+        self._ck(lib().vsk_routed_pack_layer(self.h, layer, p_gate, p_up, p_down, stream), "routed_pack_layer")
+
+    def decode_step_routed(self, ids_ptr, run_ptr, w_ptr, logits_ptr, next_ids_ptr, ws_ptr, ws_bytes, stream=None):
+        self._ck(lib().vsk_decode_step_routed(self.h, ids_ptr, run_ptr, w_ptr, logits_ptr, next_ids_ptr, ws_ptr,
+                                              ws_bytes, stream), "decode_step_routed")
+
+    def prefill_chunk_routed(self, ids_ptr, run_ptr, w_ptr, logit_rows_ptr, n_logit_rows, logits_ptr, next_ids_ptr,
+                             ws_ptr, ws_bytes, stream=None):
+        self._ck(lib().vsk_prefill_chunk_routed(self.h, ids_ptr, run_ptr, w_ptr, logit_rows_ptr, n_logit_rows,
+                                                logits_ptr, next_ids_ptr, ws_ptr, ws_bytes, stream),
+                 "prefill_chunk_routed")
+
+    def route_maps_read(self, run_ptr, proj_ptr, inv_ptr, cnt_ptr, stream=None):
+        self._ck(lib().vsk_route_maps_read(self.h, run_ptr, proj_ptr, inv_ptr, cnt_ptr, stream), "route_maps_read")
 
     def set_tuning(self, key, value):
         self._ck(lib().vsk_set_tuning(self.h, key, value), "set_tuning")

@@ -71,11 +71,12 @@ def oracle_state(w, seq_subset=None):
     return a, batch, sub, rows, kv, idx
 
 
-def oracle_run(w, seq_subset=None, overrides=None, dist=None, dtype="f64"):
+def oracle_run(w, seq_subset=None, overrides=None, dist=None, dtype="f64", route=None):
     """Oracle pass over the listed sequences.  Returns (out, kv, sub_batch, idx, device_rows).
 
     dtype "f32" runs the oracle's contract-mode variant (float32 arithmetic,
-    same rounding points) instead of the float64 definition.
+    same rounding points) instead of the float64 definition.  route: a
+    routed pass's tape (run, w) over all rows of the workload.
 
     device_rows[j] is the row of the device's logits output that holds the
     j-th returned oracle row.
@@ -101,7 +102,8 @@ def oracle_run(w, seq_subset=None, overrides=None, dist=None, dtype="f64"):
                 lrows.append(int(sub["cu_q"][j + 1]) - 1)
                 dev_rows.append(out_pos[i])
         lrows, dev_rows = np.asarray(lrows), np.asarray(dev_rows)
-    out = forward(m, W, kv, sub, w.tokens[rows], lrows, dtype=dtype)
+    rt = None if route is None else (np.asarray(route[0])[:, rows], np.asarray(route[1])[:, rows])
+    out = forward(m, W, kv, sub, w.tokens[rows], lrows, dtype=dtype, route=rt)
     return out, kv, sub, idx, dev_rows
 
 
@@ -160,12 +162,12 @@ def compare_logits(gpu_logits, gpu_ids, z, tol=LOGIT_TOL, z32=None, k=SPREAD_K):
     return stats
 
 
-def e2e_compare(w, gpu_logits, gpu_ids, seq_subset=None, overrides=None, dist=None):
+def e2e_compare(w, gpu_logits, gpu_ids, seq_subset=None, overrides=None, dist=None, route=None):
     """End-to-end check of device logits against the oracle run from the token
     ids, with row bounds from the oracle's own float32 spread (compare_logits).
     Returns (stats, float64 oracle output, kv, sub_batch, idx, device rows)."""
-    out, kv, sub, idx, dev_rows = oracle_run(w, seq_subset, overrides=overrides, dist=dist)
+    out, kv, sub, idx, dev_rows = oracle_run(w, seq_subset, overrides=overrides, dist=dist, route=route)
     print(f"[e2e] {w.name}: float64 oracle done", flush=True)
-    out32, *_ = oracle_run(w, seq_subset, overrides=overrides, dist=dist, dtype="f32")
+    out32, *_ = oracle_run(w, seq_subset, overrides=overrides, dist=dist, dtype="f32", route=route)
     st = compare_logits(gpu_logits[dev_rows], gpu_ids[dev_rows], out["z"], z32=out32["z"])
     return st, out, kv, sub, idx, dev_rows
