@@ -1,6 +1,7 @@
 """Benchmark of the batched decode step on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
+    python bench.py --sweep          (row sweep of dense and routed steps; no JSON contract line)
 
 Workload: the 3B-class GQA decoder (28 layers, hidden 3072, 24/8 heads x 128,
 SwiGLU 8192, vocab 128256), batch 16, cached contexts U[512,1024], KV blocks of
@@ -9,12 +10,18 @@ Random-init bf16 weights and N(0,1) KV from the seeded generators; inputs are
 resident in HBM before timing starts and the step is replayed idempotently.
 
 Prints ONE JSON line.  ``value`` is decode tokens/s (rows per step / step
-time, the faster of eager launches and a captured HIP graph of the step);
-``roofline`` reports the gate/up projection (the largest kernel of a layer),
-timed live with HIP events bound to each of its launches (hipExtLaunchKernel:
-the kernel's own start and end on the pass stream) during a timed pass loop;
-``cpu_baseline`` times the float64 CPU oracle on a bounded sample of
-the same workload.  The batch-64 shared-prefix workload is reported beside it.
+time over exactly K timed steps, the faster of eager launches and a captured
+HIP graph of the step).  Beside it: per-replay statistics (median and IQR of
+at least 100 event-timed replays, and a t-based 95% interval over 5 repeats
+of the K-step loop); a 16-step decode loop that rebuilds and uploads the
+batch metadata on the host every step (allocator reserve, batch build,
+upload, step); the same workload in routed mode (half the routed decisions
+Project-Only); the batch-64 shared-prefix workload; the device's measured
+stream-read ceiling; ``roofline`` for the gate/up projection (the largest
+kernel of a layer), timed live with HIP events bound to each of its launches
+(hipExtLaunchKernel: the kernel's own start and end on the pass stream); and
+``cpu_baseline``, the float64 CPU oracle timed on a bounded sample of the
+same workload (median of 3 after a warm-up).
 """
 from __future__ import annotations
 
@@ -42,7 +49,7 @@ def parse():
     ap.add_argument("--workload", type=int, default=2, help="decode workload of the value line (2, 3 or 5)")
     ap.add_argument("--no-batch64", action="store_true", help="skip the batch-64 shared-prefix line")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-layers", type=int, default=2, help="layers in the CPU oracle sample")
+    ap.add_argument("--cpu-layers", type=int, default=1, help="layers in the CPU oracle sample")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--mode", type=int, default=0,
                     help="execution path: 0 automatic, 1 one kernel per operation, 2 persistent step kernel")
@@ -50,6 +57,12 @@ def parse():
                     help="launch-shape tuning passed to vsk_set_tuning before timing (repeatable)")
     ap.add_argument("--trace", action="store_true",
                     help="print the persistent kernel's per-phase timeline (stderr) after the timed steps")
+    ap.add_argument("--no-routed", action="store_true", help="skip the routed-mode line")
+    ap.add_argument("--no-loop", action="store_true", help="skip the host-rebuild decode loop")
+    ap.add_argument("--replays", type=int, default=100, help="event-timed replays for the per-replay statistics")
+    ap.add_argument("--sweep", action="store_true",
+                    help="row sweep (8B-class, 1k context) of dense and routed steps, eager and graph")
+    ap.add_argument("--sweep-rows", default="16,32,64,128,256,384,512,768,1024")
     ap.add_argument("--profile-pass", action="store_true",
                     help="for rocprofv3 runs: set up the workload, run one plain copy of "
                          f"{CALIB_BYTES >> 20} MiB (counter calibration), then --steps passes; no JSON")
@@ -64,6 +77,7 @@ class HipEvents:
         self.L.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
         self.L.hipEventSynchronize.argtypes = [C.c_void_p]
         self.L.hipEventDestroy.argtypes = [C.c_void_p]
+        self.L.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
 
     def create(self, n):
         out = []
@@ -147,6 +161,36 @@ def time_steps(torch, fn, steps, warmup, stream):
     return e0.elapsed_time(e1) / steps, wall
 
 
+T975_4 = 2.776  # two-sided 95% quantile of Student's t with 4 degrees of freedom
+
+
+def replay_stats(torch, fn, stream, n):
+    """A HIP event pair around each of n replays of fn on `stream`: median,
+    interquartile range and mean of the per-replay times (ms)."""
+    ev = HipEvents()
+    b, e = ev.create(n), ev.create(n)
+    sp = stream.cuda_stream
+    for i in range(n):
+        ev.L.hipEventRecord(b[i], sp)
+        fn()
+        ev.L.hipEventRecord(e[i], sp)
+    torch.cuda.synchronize()
+    d = np.array([ev.elapsed_ms(b[i], e[i]) for i in range(n)])
+    ev.destroy(b + e)
+    q1, med, q3 = np.percentile(d, [25, 50, 75])
+    return {"replays": n, "median_ms": round(float(med), 4), "iqr_ms": [round(float(q1), 4), round(float(q3), 4)],
+            "mean_ms": round(float(d.mean()), 4)}
+
+
+def repeat_ci(torch, fn, steps, stream, reps=5):
+    """reps repeats of the timed steps loop: mean and a t-based 95% interval."""
+    means = np.array([time_steps(torch, fn, steps, 0, stream)[0] for _ in range(reps)])
+    m, sd = float(means.mean()), float(means.std(ddof=1))
+    half = T975_4 * sd / np.sqrt(reps)
+    return {"repeats": reps, "steps_each": steps, "mean_ms": round(m, 4),
+            "ci95_ms": [round(m - half, 4), round(m + half, 4)]}
+
+
 PHASES = ("qkv", "attention", "o_proj", "gate_up", "down")
 
 
@@ -197,37 +241,56 @@ def apply_tuning(d, mode, tune):
         d.eng.set_tuning(int(k), int(v))
 
 
-def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False, tune=()):
+def capture(torch, step):
+    """A HIP graph of one pass (captured on a side stream after a warm-up there)."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(stream=s.cuda_stream)  # warm the capture stream
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step(stream=torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    return g
+
+
+def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False, tune=(), route=None, stats=0):
+    """Time one workload: exactly `steps` steps eager and as graph replays;
+    with stats > 0 also per-replay statistics and 5 repeats of the faster."""
     from paper_2609_37062_amd.runner import DeviceRun
-    print(f"[bench] setting up {w.name}", file=sys.stderr, flush=True)
-    d = DeviceRun(w)
+    print(f"[bench] setting up {w.name}{' (routed)' if route is not None else ''}", file=sys.stderr, flush=True)
+    d = DeviceRun(w, routed=route is not None)
     apply_tuning(d, mode, tune)
+    if route is not None:
+        d.set_route(*route)
+    step = d.step_routed if route is not None else d.step
     stream = torch.cuda.current_stream()
     res = {}
-    ms_eager, wall_eager = time_steps(torch, d.step, steps, warmup, stream)
+    ms_eager, wall_eager = time_steps(torch, step, steps, warmup, stream)
     res["ms_eager"] = ms_eager
     res["ms_eager_wall"] = wall_eager
     print(f"[bench] {w.name}: eager {ms_eager:.3f} ms/step", file=sys.stderr, flush=True)
+    best = step
+    g = None
     if use_graph:
-        g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            d.step(stream=s.cuda_stream)  # warm the capture stream
-        torch.cuda.current_stream().wait_stream(s)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            d.step(stream=torch.cuda.current_stream().cuda_stream)
-        torch.cuda.synchronize()
+        g = capture(torch, step)
         ms_graph, wall_graph = time_steps(torch, g.replay, steps, warmup, stream)
         res["ms_graph"] = ms_graph
         print(f"[bench] {w.name}: graph {ms_graph:.3f} ms/step", file=sys.stderr, flush=True)
         # graph replays must reproduce the eager result
         lg_g, ids_g = d.results()
-        d.step()
+        step()
         lg_e, ids_e = d.results()
         res["graph_matches_eager"] = bool(np.array_equal(lg_g, lg_e) and np.array_equal(ids_g, ids_e))
-        del g
+        if ms_graph < ms_eager:
+            best = g.replay
+    if stats > 0:
+        res["per_replay"] = replay_stats(torch, best, stream, stats)
+        res["repeats"] = repeat_ci(torch, best, steps, stream)
+        res["stats_of"] = "graph" if best is not step else "eager"
+    del g
     res["persistent"] = bool(d.eng.exec_counters()[5])
     if probe and res["persistent"]:
         # the whole step is one kernel: HIP events around each launch on its stream
@@ -235,9 +298,9 @@ def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False,
         b, e = ev.create(steps), ev.create(steps)
         sp = stream.cuda_stream
         for i in range(steps):
-            ev.L.hipEventRecord(C.c_void_p(b[i]), C.c_void_p(sp))
-            d.step(stream=sp)
-            ev.L.hipEventRecord(C.c_void_p(e[i]), C.c_void_p(sp))
+            ev.L.hipEventRecord(b[i], sp)
+            step(stream=sp)
+            ev.L.hipEventRecord(e[i], sp)
         torch.cuda.synchronize()
         durs = [ev.elapsed_ms(b[i], e[i]) for i in range(steps)]
         ev.destroy(b + e)
@@ -249,7 +312,7 @@ def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False,
         b, e = ev.create(n), ev.create(n)
         d.eng.set_probe(0, b, e)
         for _ in range(steps):
-            d.step()
+            step()
         torch.cuda.synchronize()
         durs = [ev.elapsed_ms(b[i], e[i]) for i in range(n)]
         d.eng.set_probe(0, [], [])
@@ -267,9 +330,84 @@ def measure(torch, w, steps, warmup, use_graph, probe=True, mode=0, trace=False,
     return res
 
 
-def cpu_baseline(w, n_layers_sample):
+def decode_loop(torch, w, n_steps=16, warm=2):
+    """A real decode loop: every step reserves one more position per sequence
+    in the host allocator, rebuilds and uploads the batch metadata, and runs
+    the step on the previous step's greedy ids (device to device, no host
+    sync).  Wall-clock per step in steady state, with the host work
+    overlapping the device's previous steps."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    print(f"[bench] decode loop on {w.name}", file=sys.stderr, flush=True)
+    kvmax = max(s.ctx + s.q_len for s in w.seqs)
+    d = DeviceRun(w, max_kv_len=kvmax + n_steps + warm + 1)
+    seqs = list(range(w.n_seqs))
+    ones = [1] * w.n_seqs
+    meta_t = torch.empty(4 * d.meta_bytes + 4096, dtype=torch.uint8, device=d.device)
+    meta = meta_t.data_ptr() + ((-meta_t.data_ptr()) % 256)
+    ids = [d.ids.clone(), torch.empty_like(d.ids)]
+    sp = d.sp
+
+    def one(i):
+        for q in seqs:
+            d.eng.reserve(q, 1)
+        d.eng.batch_build(seqs, ones)
+        d.eng.batch_upload(meta, meta_t.numel() - 256, sp)
+        d.eng.decode_step(ids[i % 2].data_ptr(), d.logits.data_ptr(), ids[(i + 1) % 2].data_ptr(), d.ws,
+                          d.ws_bytes, sp)
+
+    for i in range(warm):
+        one(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(warm, warm + n_steps):
+        one(i)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / n_steps
+    d.release()
+    del d
+    torch.cuda.empty_cache()
+    return {"steps": n_steps, "ms_per_step_wall": round(wall, 4),
+            "note": "host allocator reserve + batch build + asynchronous upload + decode step per step"}
+
+
+def stream_ceiling(torch, gib=4):
+    """Best stream-read rate of a plain read kernel over `gib` GiB (GB/s)."""
+    from paper_2609_37062_amd import vsk
+    n = gib << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(3)
+    out = torch.empty(16384, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    best = None
+    for wgs in (1024, 2048, 4096, 8192):
+        fn = lambda: vsk.stream_read(src.data_ptr(), n, out.data_ptr(), wgs, stream.cuda_stream)
+        fn()
+        r = replay_stats(torch, fn, stream, 10)
+        rate = n / (r["median_ms"] / 1e3) / 1e9
+        if best is None or rate > best[0]:
+            best = (rate, wgs, r["median_ms"])
+    del src, out
+    torch.cuda.empty_cache()
+    return {"GBps": round(best[0], 1), "workgroups": best[1], "bytes": n, "median_ms": best[2],
+            "frac_of_peak": round(best[0] * 1e9 / PEAK_HBM, 4)}
+
+
+def cpu_info():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model
+
+
+def cpu_baseline(w, n_layers_sample, reps=3):
     """Time the float64 oracle on a sample: all rows of the workload through
-    1 and 1 + n_layers_sample layers plus the lm_head, extrapolated per layer."""
+    1 and 1 + n_layers_sample layers plus the lm_head, each the median of
+    `reps` runs after a warm-up, extrapolated per layer to the full step."""
     import copy
     from dataclasses import replace
 
@@ -291,18 +429,116 @@ def cpu_baseline(w, n_layers_sample):
         W.over[("lm_head", -1)] = GeneratedWeights(ws.model, w.seed).get("lm_head", -1)
         W.get("final_norm", -1)
         lr = np.arange(w.n_rows)
-        t0 = time.perf_counter()
-        forward(ws.model, W, kv, sub, w.tokens[rows], lr)
-        times[nl] = time.perf_counter() - t0
+        runs = []
+        for i in range(reps + 1):  # the first is the warm-up
+            t0 = time.perf_counter()
+            forward(ws.model, W, kv, sub, w.tokens[rows], lr)
+            if i:
+                runs.append(time.perf_counter() - t0)
+        times[nl] = float(np.median(runs))
         del W, kv
     t_layer = (times[1 + n_layers_sample] - times[1]) / n_layers_sample
     t_step = times[1] + (w.model.n_layers - 1) * t_layer
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    info = threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] + [1])
+    blas = ", ".join(sorted({f"{i.get('internal_api')} {i.get('version')}" for i in info if i.get("user_api") == "blas"}))
     return {"value": w.n_rows / t_step, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": (f"{w.name}: all {w.n_rows} rows through 1 and {1 + n_layers_sample} of "
                        f"{w.model.n_layers} layers + lm_head (float64 NumPy, weights and KV drawn "
-                       f"before timing), per-layer time extrapolated to the full step"),
-            "s_per_step": t_step}
+                       f"before timing), each the median of {reps} runs after a warm-up; per-layer time "
+                       f"extrapolated to the full step"),
+            "cpu_model": cpu_info(), "blas": blas or "unknown", "s_per_step": t_step}
+
+
+def routed_tape(w, s=0.5, seed=7):
+    """Random skip over the routed layers: every request skips, each routed
+    decision projects with probability s."""
+    from workloads import routes
+    req = np.arange(w.n_seqs)
+    pos = np.array([q.ctx for q in w.seqs])
+    return routes.random_skip(seed, w.model.n_routed, req, pos, 1.0, s)
+
+
+def fit_line(x, y):
+    """Least-squares intercept and slope."""
+    A = np.stack([np.ones(len(x)), np.asarray(x, np.float64)], axis=1)
+    (a, b), *_ = np.linalg.lstsq(A, np.asarray(y, np.float64), rcond=None)
+    return float(a), float(b)
+
+
+def sweep(torch, rows_list, steps=10, warmup=3, ctx=1024, s_skip=0.5):
+    """Per-step latency lines of the two modes over the row count at a fixed
+    context (8B-class model, 16 of 32 layers routed, half the routed
+    decisions Project-Only), eager and captured as a graph at each row count
+    (capacity C = rows); the gate/up projection's own time per row count
+    locates the ridge.  One JSON line per row count, then the fitted lines,
+    tau (routed intercept minus dense intercept), the graph-vs-eager
+    overhead, the measured ridge and the decode rule's thresholds on this
+    device."""
+    from paper_2609_37062_amd import vsk
+    from paper_2609_37062_amd.runner import DeviceRun
+    from workloads.configs import M8B, decode_workload
+    rmax = max(rows_list)
+    w = decode_workload(M8B, np.full(rmax, ctx), seed=0, name=f"8B-sweep-ctx{ctx}")
+    print(f"[sweep] setting up {rmax} rows x {ctx} context (KV left at zero)", file=sys.stderr, flush=True)
+    d = DeviceRun(w, routed=True, fill_kv=False)
+    stream = torch.cuda.current_stream()
+    ev = HipEvents()
+    pts = []
+    for R in rows_list:
+        d.rebatch(range(R))
+        wr = decode_workload(M8B, np.full(R, ctx), seed=0)
+        d.set_route(*routed_tape(wr, s_skip))
+        rec = {"rows": R}
+        for mode, fn in (("dense", d.step), ("routed", d.step_routed)):
+            ms_e, _ = time_steps(torch, fn, steps, warmup, stream)
+            g = capture(torch, fn)
+            ms_g, _ = time_steps(torch, g.replay, steps, warmup, stream)
+            del g
+            rec[f"{mode}_eager_ms"] = round(ms_e, 4)
+            rec[f"{mode}_graph_ms"] = round(ms_g, 4)
+        # gate/up launches of a dense step (the weight-stationary GEMM of the rule)
+        n = M8B.n_layers * 3
+        b, e = ev.create(n), ev.create(n)
+        d.eng.set_probe(0, b, e)
+        for _ in range(3):
+            d.step()
+        torch.cuda.synchronize()
+        gu = float(np.median([ev.elapsed_ms(b[i], e[i]) for i in range(n)]))
+        d.eng.set_probe(0, [], [])
+        ev.destroy(b + e)
+        rec["gateup_us"] = round(gu * 1e3, 2)
+        pts.append(rec)
+        print(json.dumps({"sweep_point": rec}), flush=True)
+    d.release()
+    rows = [p["rows"] for p in pts]
+    best = lambda p, m: min(p[f"{m}_eager_ms"], p[f"{m}_graph_ms"])
+    ad, bd = fit_line(rows, [best(p, "dense") for p in pts])
+    ar, br = fit_line(rows, [best(p, "routed") for p in pts])
+    tau = (ar - ad) * 1e-3
+    # ridge: the gate/up time is flat while weight-bound, then grows with rows;
+    # M* = rows where the flat level meets the line through the largest counts
+    gu = np.array([p["gateup_us"] for p in pts])
+    flat = float(np.median(gu[: max(2, len(gu) // 3)]))
+    hi = [(r, g) for r, g in zip(rows, gu) if g > 1.5 * flat]
+    m_star = None
+    if len(hi) >= 2:
+        a, bslope = fit_line([r for r, _ in hi], [g for _, g in hi])
+        if bslope > 0:
+            m_star = round((flat - a) / bslope, 1)
+    bw = stream_ceiling(torch)["GBps"] * 1e9
+    L_r, kvb = M8B.n_routed, M8B.kv_bytes_per_token_layer
+    vstar, ex, en = vsk.switch_thresholds(max(tau, 1e-9), bw, s_skip, L_r, kvb, tau_layers=L_r)
+    graph_over = [p["dense_graph_ms"] - p["dense_eager_ms"] for p in pts]
+    summary = {"sweep": "8B-class, 1k context, random skip s=0.5 over 16 routed layers",
+               "dense_line_ms": {"intercept": round(ad, 4), "slope_per_row": round(bd, 6)},
+               "routed_line_ms": {"intercept": round(ar, 4), "slope_per_row": round(br, 6)},
+               "tau_ms": round(tau * 1e3, 4), "graph_minus_eager_ms": [round(x, 4) for x in graph_over],
+               "gateup_flat_us": round(flat, 2), "ridge_rows_measured": m_star,
+               "stream_read_GBps": round(bw / 1e9, 1),
+               "rule_on_this_device": {"v_star_tokens": round(vstar), "exit_tokens": ex, "enter_tokens": en,
+                                       "tau_layers": L_r, "skip": s_skip, "kv_bytes": kvb}}
+    print(json.dumps(summary), flush=True)
 
 
 def main():
@@ -315,6 +551,9 @@ def main():
     from workloads.configs import workload
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if a.sweep:
+        sweep(torch, [int(x) for x in a.sweep_rows.split(",")])
+        return
     w = workload(a.workload)
     if a.profile_pass:
         from paper_2609_37062_amd.runner import DeviceRun
@@ -332,7 +571,8 @@ def main():
         print(f"[bench] profile pass: {w.name}, {a.steps} steps, calibration copy {CALIB_BYTES} bytes",
               file=sys.stderr)
         return
-    r = measure(torch, w, a.steps, a.warmup, not a.no_graph, mode=a.mode, trace=a.trace, tune=a.tune)
+    r = measure(torch, w, a.steps, a.warmup, not a.no_graph, mode=a.mode, trace=a.trace, tune=a.tune,
+                stats=max(a.replays, a.steps))
     ms = min(r["ms_eager"], r.get("ms_graph", float("inf")))
     tokps = w.n_rows / (ms / 1e3)
     sb = step_bytes(w)
@@ -343,6 +583,7 @@ def main():
         kname = "gate/up projection + SwiGLU (k_gemm, EPI_SWIGLU)"
         kb = gateup_bytes(w.model, w.n_rows)
     achieved = kb / (r["kernel_ms"] / 1e3)
+    traffic = (None if r["persistent"] else gateup_traffic()) if a.workload == 2 else None
     out = {
         "metric": "decode-step latency (ms) & tokens/s at batch 16/64; achieved HBM TB/s vs peak",
         "value": round(tokps, 1),
@@ -363,18 +604,37 @@ def main():
         "ms_eager": round(r["ms_eager"], 4),
         "ms_graph": round(r["ms_graph"], 4) if "ms_graph" in r else None,
         "graph_matches_eager": r.get("graph_matches_eager"),
+        "per_replay": r.get("per_replay"),
+        "repeats": r.get("repeats"),
+        "stats_of": r.get("stats_of"),
         "step_bytes": sb,
         "step_hbm_TBps": round(sb / (ms / 1e3) / 1e12, 3),
         "step_hbm_frac": round(sb / (ms / 1e3) / PEAK_HBM, 4),
         "roofline": {"bound": "hbm", "kernel": kname,
                      "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM, 4),
-                     "traffic": (None if r["persistent"] else gateup_traffic()) if a.workload == 2 else None,
+                     "traffic": traffic,
+                     "traffic_source": ("stored rocprofv3 counters of this kernel source "
+                                        "(profiles/gateup_3b_b16_traffic.json)") if traffic is not None else None,
                      "bytes_per_launch": kb, "avg_launch_ms": round(r["kernel_ms"], 5)},
         "exec_counters": r["counters"],
     }
     if "timeline" in r:
         out["timeline"] = r["timeline"]
+    sc = stream_ceiling(torch)
+    out["stream_read_ceiling"] = sc
+    out["step_frac_of_stream_ceiling"] = round(sb / (ms / 1e3) / (sc["GBps"] * 1e9), 4)
+    if not a.no_loop and a.mode != 2:
+        out["decode_loop"] = decode_loop(torch, w)
+    if not a.no_routed and a.mode != 2:
+        rr = measure(torch, w, a.steps, a.warmup, not a.no_graph, probe=False, tune=a.tune, route=routed_tape(w))
+        msr = min(rr["ms_eager"], rr.get("ms_graph", float("inf")))
+        out["routed"] = {"workload": w.name, "policy": "random skip, half of the routed decisions Project-Only",
+                         "routed_layers": w.model.n_routed, "proj_ffn": w.model.proj_dim,
+                         "ms_per_step": round(msr, 4), "ms_eager": round(rr["ms_eager"], 4),
+                         "ms_graph": round(rr["ms_graph"], 4) if "ms_graph" in rr else None,
+                         "graph_matches_eager": rr.get("graph_matches_eager"),
+                         "tokens_per_s": round(w.n_rows / (msr / 1e3), 1)}
     if not a.no_batch64 and a.workload == 2:
         w3 = workload(3)
         r3 = measure(torch, w3, a.steps, a.warmup, not a.no_graph, probe=False, mode=a.mode if a.mode != 2 else 0,

@@ -342,6 +342,13 @@ int vsk_switch_decode_mode(int32_t mode_in, int32_t routing, int32_t promote, in
 int vsk_switch_prefill(int64_t prompt_tokens, double po_share, int64_t floor_tokens, double share_min,
                        int32_t* routed);
 
+/* Measurement: read `bytes` (a multiple of 16, 16-byte aligned device
+ * memory) once with a plain streaming kernel of `workgroups` workgroups of
+ * 256 threads, writing one uint32 per workgroup to out_dev: timed around, it
+ * gives the device's achievable stream-read bandwidth, the ceiling beside
+ * the 8 TB/s HBM peak. */
+int vsk_stream_read(const void* src_dev, size_t bytes, uint32_t* out_dev, int32_t workgroups, void* stream);
+
 /* Timing probes (measurement only).  While set, the first n_pairs launches
  * of kernel class `which` in the following passes are each launched with
  * hipExtLaunchKernel bound to (begin_events[i], end_events[i]), in launch
@@ -406,7 +413,11 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        its K split aims for (1..4096); 0 (the default): 192; -1: no split
  *        (two 16-column tiles per workgroup with the epilogue in the
  *        projection).  Split products are added in split order by a kernel
- *        that then applies rotary and writes q and the KV slots. */
+ *        that then applies rotary and writes q and the KV slots.
+ * key 8: projections of a row-tiled pass (more than 128 rows): 1 (the
+ *        default) orders the workgroups so that the row tiles of one weight
+ *        slice run together on one XCD and share its L2; 0 keeps the
+ *        dispatch order. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

@@ -732,6 +732,15 @@ int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32
   return e == hipSuccess ? VSK_OK : VSK_E_HIP;
 }
 
+int vsk_stream_read(const void* src_dev, size_t bytes, uint32_t* out_dev, int32_t workgroups, void* stream) {
+  if (!src_dev || !out_dev || bytes == 0 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(src_dev) % 16 ||
+      workgroups < 1)
+    return VSK_E_ARG;
+  return launch_stream_read(src_dev, bytes, out_dev, workgroups, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? VSK_OK
+             : VSK_E_HIP;
+}
+
 int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events, void* const* end_events, int32_t n_pairs) {
   if (!h) return VSK_E_ARG;
   if (which < 0 || which >= Handle::kProbeClasses) return fail(h, VSK_E_RANGE, "unknown probe class");
@@ -776,6 +785,10 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       if (value < -1 || value > 4096)
         return fail(h, VSK_E_ARG, "residual split target must be -1 (no split), 0 (default) or 1..4096");
       h->resid_target = value;
+      return VSK_OK;
+    case 8:
+      if (value < 0 || value > 1) return fail(h, VSK_E_ARG, "XCD remap switch must be 0 or 1");
+      h->xcd_remap = value;
       return VSK_OK;
     case 7:
       if (value < -1 || value > 4096)
@@ -979,6 +992,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   ga.rope = reinterpret_cast<const float2*>(P + h.pl.rope);
   ga.x = x;
   ga.out_Rg = Rg;
+  ga.xcd_remap = h.xcd_remap;
 
   AttnArgs aa{};
   aa.q = q;

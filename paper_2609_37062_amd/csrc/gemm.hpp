@@ -27,6 +27,7 @@ struct GemmArgs {
   int* am_idx;
   float* ypart;  // RESID with K split over workgroups: y[split][R][N] instead of x += y
   const int* count;  // nullable: rows of this launch read on the device (<= R; a cohort's size)
+  int xcd_remap;     // row-tiled passes: row tiles of one N group on one XCD at the same time
 };
 
 struct GemmPlan {

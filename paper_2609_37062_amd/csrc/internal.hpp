@@ -169,6 +169,7 @@ struct Handle {
   int resid_target = 0;   // residual projections: split-K workgroup target (0 default, -1 no split)
   int qkv_target = 0;     // QKV at 4..8 row groups: split-K workgroup target (0 default, -1 no split)
   int prefill_attn = 1;   // prefill rows through the causal multi-row kernel (0: one row per work item)
+  int xcd_remap = 1;      // row-tiled projections: XCD-aware workgroup order (0: dispatch order)
   int step_wgs = -1;   // workgroups of a persistent launch on this device (0: not runnable; -1: not queried)
   uint64_t* step_trace = nullptr;  // measurement: timestamp buffer of the persistent kernel
   size_t step_trace_cap = 0;       // its capacity in uint64

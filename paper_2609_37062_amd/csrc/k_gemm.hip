@@ -90,7 +90,24 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
   // K-split role: it holds no sums and runs no epilogue)
   const bool loader = XL && w == WN * WK;
   const int wn = w % WN, wk = loader ? -1 : w / WN;
-  const int ng = blockIdx.x, ks = blockIdx.y, mt = blockIdx.z;
+  // Workgroup -> (N group, K split, row tile).  Workgroups are dispatched to
+  // the 8 XCDs in turn (linear id modulo 8), each XCD with its own L2.  In a
+  // row-tiled pass every row tile re-reads the same weights, so with
+  // a.xcd_remap the linear ids an XCD receives are renumbered consecutively
+  // and the row tile varies fastest: the row tiles of one N group run at the
+  // same time on one XCD and read that weight slice from HBM once, the rest
+  // from its L2.
+  int ng = blockIdx.x, ks = blockIdx.y, mt = blockIdx.z;
+  if (a.xcd_remap) {
+    const int nwg = gridDim.x * gridDim.y * gridDim.z;
+    const int bid = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int xcd = bid & 7, slot = bid >> 3;
+    const int lid = xcd * (nwg >> 3) + min(xcd, nwg & 7) + slot;  // a bijection of [0, nwg)
+    mt = lid % gridDim.z;
+    const int rest = lid / gridDim.z;
+    ks = rest % gridDim.y;
+    ng = rest / gridDim.y;
+  }
   const int n_tiles = a.N >> 4;
   // RESID with K split over workgroups (gridDim.y splits): this workgroup
   // takes K steps [k_lo, k_hi) and stores its product, unreduced
@@ -490,7 +507,9 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
 
 // ---------------------------------------------------------------- launcher
 template <int MG, int NT, int WN, int WK, int PF, int EPI, bool XL = false>
-static hipError_t launch_cfg(const GemmArgs& a, int m_tiles, int ksplit, hipStream_t s, const LaunchEvents& ev) {
+static hipError_t launch_cfg(const GemmArgs& a_in, int m_tiles, int ksplit, hipStream_t s, const LaunchEvents& ev) {
+  GemmArgs a = a_in;
+  a.xcd_remap = a_in.xcd_remap && m_tiles > 1 ? 1 : 0;
   const int n_groups = (a.N / 16 + NT * WN - 1) / (NT * WN);
   dim3 grid(n_groups, ksplit, m_tiles);
   // cross-wave reduction; with X in LDS the same space first holds the X chunks

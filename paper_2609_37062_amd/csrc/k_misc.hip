@@ -534,6 +534,35 @@ hipError_t launch_fill_zero(void* dst, size_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- stream read (measurement)
+// Reads `n16` 16-byte words once, four per thread per round in a grid-stride
+// loop, and leaves one word per workgroup (an xor of what it read, so no load
+// is dead): the achievable HBM read rate of a plain streaming kernel.
+__global__ __launch_bounds__(256) void k_stream_read(const u32x4* __restrict__ src, size_t n16,
+                                                     uint32_t* __restrict__ out) {
+  __shared__ uint32_t s_x[4];
+  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+  size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  u32x4 acc = u32x4{0u, 0u, 0u, 0u};
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const u32x4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+    acc ^= a ^ b ^ c ^ d;
+  }
+  for (; i < n16; i += stride) acc ^= src[i];
+  uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x ^= __shfl_xor(x, m, 64);
+  if ((threadIdx.x & 63) == 0) s_x[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) out[blockIdx.x] = s_x[0] ^ s_x[1] ^ s_x[2] ^ s_x[3];
+}
+
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* out, int wgs, hipStream_t s) {
+  if (bytes % 16 != 0 || wgs < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_stream_read, dim3(wgs), dim3(256), 0, s, static_cast<const u32x4*>(src), bytes / 16, out);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- KV scatter / gather
 // One thread per (token, kv head, dim); logical layout [n][Hkv][hd].
 template <bool WRITE>

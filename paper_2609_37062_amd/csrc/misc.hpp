@@ -33,6 +33,7 @@ hipError_t launch_argmax_partials(const float* pv, const int* pi, int n_groups, 
                                   hipStream_t s);
 hipError_t launch_pack(const uint16_t* s0, const uint16_t* s1, const uint16_t* s2, int n0, int n1, int N, int K,
                        int perm_kind, int head_dim, int n_rope_rows, uint16_t* dst, hipStream_t s);
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* out, int wgs, hipStream_t s);
 hipError_t launch_kv_move(bool write, uint16_t* pool, int layer, int n_blocks, int Hkv, int hd,
                           const int32_t* slots, int n, uint16_t* k, uint16_t* v, hipStream_t s);
 

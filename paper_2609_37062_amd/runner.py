@@ -34,7 +34,7 @@ class DeviceRun:
     """One workload resident on the device: engine, packed weights, KV pool, batch, workspace."""
 
     def __init__(self, w: Workload, device="cuda", overrides=None, weight_dist=None, max_rows=None,
-                 max_kv_len=None, pool_blocks=None, poison_pool=False, routed=False):
+                 max_kv_len=None, pool_blocks=None, poison_pool=False, routed=False, fill_kv=True):
         assert torch.cuda.is_available(), "a GPU is required"
         self.w = w
         self.m = w.model
@@ -52,9 +52,12 @@ class DeviceRun:
         self.pool = torch.empty(self.eng.kv_pool_bytes(self.n_blocks) // 2, dtype=torch.int16, device=self.device)
         if poison_pool:
             self.pool.fill_(-1)  # every unwritten slot holds a bf16 NaN pattern
+        elif not fill_kv:
+            self.pool.zero_()  # timing runs that skip drawing the cached KV
         self.eng.kv_init(self.pool.data_ptr(), self.n_blocks)
         self.slots = apply_recipe(self.eng, w)
-        self._fill_kv()
+        if fill_kv:
+            self._fill_kv()
         seqs = list(range(w.n_seqs))
         self.q_lens = [s.q_len for s in w.seqs]
         self.eng.batch_build(seqs, self.q_lens)
@@ -68,6 +71,7 @@ class DeviceRun:
         self._ws_t, self.ws = _dev_buffer(self.ws_bytes, self.device)
         self.eng.workspace_init(self.ws, self.ws_bytes, *self.cap, self.sp)
         self.ids = torch.from_numpy(np.ascontiguousarray(w.tokens, np.int32)).to(self.device)
+        self._ids_all = self.ids
         lr = w.logit_rows()
         self.logit_rows = torch.from_numpy(lr).to(self.device)
         self.n_out = len(lr) if any(s.q_len > 1 for s in w.seqs) else R
@@ -163,6 +167,18 @@ class DeviceRun:
             V = torch.cat([kv_values_torch(self.w, l, 1, p0, n, cid, self.device) for (i, p0, n, cid) in ranges])
             self.eng.kv_write(l, slots_d.data_ptr(), n_tot, K.data_ptr(), V.data_ptr(), self.sp)
         torch.cuda.synchronize(self.device)
+
+    def rebatch(self, seqs):
+        """Make the first decode rows a new batch of the listed sequences (one row
+        each; rows, ids and logits buffers keep their capacity)."""
+        self.q_lens = [1] * len(seqs)
+        self.eng.batch_build(list(seqs), self.q_lens)
+        need = self.eng.batch_device_bytes()
+        if need > self.meta_bytes:
+            self._meta_t, self.meta = _dev_buffer(need, self.device)
+            self.meta_bytes = need
+        self.eng.batch_upload(self.meta, self.meta_bytes, self.sp)
+        self.ids = self._ids_all[:len(seqs)]
 
     # ---------------------------------------------------------- passes
     def step(self, stream=None):

@@ -98,6 +98,7 @@ SIGNATURES = [
     ("vsk_switch_step", C.c_int, [C.POINTER(SwitchThresholds), _I32, _I64, _PI32, _PI32]),
     ("vsk_switch_decode_mode", C.c_int, [_I32, _I32, _I32, _PI32]),
     ("vsk_switch_prefill", C.c_int, [_I64, C.c_double, _I64, C.c_double, _PI32]),
+    ("vsk_stream_read", C.c_int, [_VP, _SZ, _VP, _I32, _VP]),
     ("vsk_set_probe", C.c_int, [_VP, _I32, C.POINTER(_VP), C.POINTER(_VP), _I32]),
     ("vsk_exec_counters", C.c_int, [_VP, _PI64, _I32]),
     ("vsk_set_step_trace", C.c_int, [_VP, _VP, _SZ, _PI32, _PI32]),
@@ -150,6 +151,12 @@ def argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, stream=None):
     st = lib().vsk_argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, stream)
     if st != VSK_OK:
         raise VskError(st, "argmax_sample")
+
+
+def stream_read(src_ptr, nbytes, out_ptr, workgroups, stream=None):
+    st = lib().vsk_stream_read(src_ptr, nbytes, out_ptr, workgroups, stream)
+    if st != VSK_OK:
+        raise VskError(st, "stream_read")
 
 
 # ------------------------------------------------------------------ mode switch
