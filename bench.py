@@ -64,7 +64,7 @@ def parse():
                     help="row sweep (8B-class, 1k context) of dense and routed steps, eager and graph")
     ap.add_argument("--sweep-rows", default="16,32,64,128,256,384,512,768,1024")
     ap.add_argument("--profile-pass", action="store_true",
-                    help="for rocprofv3 runs: set up the workload, run one plain copy of "
+                    help="for rocprofv3 runs: set up the workload, run one plain copy and one plain read of "
                          f"{CALIB_BYTES >> 20} MiB (counter calibration), then --steps passes; no JSON")
     return ap.parse_args()
 
@@ -379,7 +379,7 @@ def stream_ceiling(torch, gib=4):
     out = torch.empty(16384, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
     best = None
-    for wgs in (1024, 2048, 4096, 8192):
+    for wgs in (256, 512, 1024, 2048, 4096):
         fn = lambda: vsk.stream_read(src.data_ptr(), n, out.data_ptr(), wgs, stream.cuda_stream)
         fn()
         r = replay_stats(torch, fn, stream, 10)
@@ -565,10 +565,15 @@ def main():
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
+        # a plain read of known size (k_stream_read) for the byte counters
+        from paper_2609_37062_amd import vsk
+        out = torch.empty(4096, dtype=torch.int32, device="cuda")
+        vsk.stream_read(src.data_ptr(), CALIB_BYTES, out.data_ptr(), 512, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
         for _ in range(a.steps):
             d.step()
         torch.cuda.synchronize()
-        print(f"[bench] profile pass: {w.name}, {a.steps} steps, calibration copy {CALIB_BYTES} bytes",
+        print(f"[bench] profile pass: {w.name}, {a.steps} steps, calibration copy and read of {CALIB_BYTES} bytes",
               file=sys.stderr)
         return
     r = measure(torch, w, a.steps, a.warmup, not a.no_graph, mode=a.mode, trace=a.trace, tune=a.tune,
