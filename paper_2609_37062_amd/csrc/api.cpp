@@ -871,6 +871,7 @@ static hipError_t run_step(Handle& h, const PassArgs& pa, int n_wgs, hipStream_t
   const int d = c.head_dim;
   StepArgs a{};
   a.n_run = h.layers_run > 0 ? h.layers_run : c.n_layers;
+  a.n_layers = c.n_layers;
   a.H = c.hidden;
   a.Nq = c.n_q_heads * d;
   a.Nkv = c.n_kv_heads * d;

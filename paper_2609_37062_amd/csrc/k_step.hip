@@ -658,6 +658,17 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
       return;
   }
 
+  // a pass that runs fewer layers still counts its arrival at the points of
+  // the layers it skips: every counter then holds the pass's epoch times its
+  // arrivals, which the next pass's waits rely on (no workgroup waits at
+  // these points)
+  if (threadIdx.x == 0)
+    for (int pt = point; pt < 5 * a.n_layers; ++pt)
+      __hip_atomic_fetch_add(a.flags + (static_cast<size_t>(pt) * kSyncCounters + (blockIdx.x % kSyncCounters)) *
+                                           kFlagWords,
+                             1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  point = 5 * a.n_layers;
+
   // ---- final norm + lm_head + argmax partials
   const int nb = 2 * a.n_run;
   e.N = a.V;

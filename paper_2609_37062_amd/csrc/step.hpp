@@ -17,7 +17,8 @@ inline int step_syncs(int n_layers) { return 5 * n_layers + 2; }
 
 struct StepArgs {
   // model
-  int n_run;  // layers to run
+  int n_run;     // layers to run
+  int n_layers;  // layers of the model (synchronisation points are numbered for all of them)
   int H, Nq, Nkv, F, V, hd, G, Hkv;
   float eps;
   // packed weights

@@ -71,6 +71,33 @@ def oracle_state(w, seq_subset=None):
     return a, batch, sub, rows, kv, idx
 
 
+def assert_kv_layer_local(d, w, seq_subset=None, step=None):
+    """Every layer's new K,V for the subset's rows (Invariant 1: each row writes
+    its own slot at every layer) within one bf16 ulp of the oracle applied to
+    that layer alone, from the device's own input residual of the layer (end to
+    end, an earlier layer's bf16 rounding flips would move later layers' K,V by
+    more than an ulp).  `step` runs the device pass (default d.step); the
+    engine is left with the full pass run last."""
+    m = w.model
+    step = step or d.step
+    a, batch, sub, rows, kv, idx = oracle_state(w, seq_subset)
+    xs = {}
+    for l in range(1, m.n_layers):
+        d.set_layers(l)
+        step()
+        xs[l] = d.residual()[rows]
+    d.set_layers(0)
+    step()
+    W = GeneratedWeights(m, w.seed)
+    tok = w.tokens[rows]
+    for l in range(m.n_layers):
+        forward(m, W, kv, sub, tok, None, x0=xs.get(l), layers=[l])
+        K, V = d.read_kv(l, sub["slot"])
+        Ko, Vo = kv.read(l, sub["slot"])
+        assert_bf16_close(K, Ko, f"K layer {l}")
+        assert_bf16_close(V, Vo, f"V layer {l}")
+
+
 def oracle_run(w, seq_subset=None, overrides=None, dist=None, dtype="f64", route=None):
     """Oracle pass over the listed sequences.  Returns (out, kv, sub_batch, idx, device_rows).
 
