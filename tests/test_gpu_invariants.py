@@ -94,6 +94,35 @@ def test_integer_inputs_bit_exact(variant, model, rows):
     d.release()
 
 
+@pytest.mark.parametrize("rows", [200, 520])
+@pytest.mark.parametrize("variant", ["qkv", "o", "mlp"])
+def test_integer_inputs_bit_exact_row_tiled(variant, rows):
+    """Passes of more than 128 rows (several 128-row tiles, the last one
+    ragged) through every epilogue (QKV, RESID, SWIGLU, LOGITS), bit for bit
+    against the oracle."""
+    m = MID
+    w = fresh_workload(m, rows, seed=rows, name=f"int-rowtiled-{variant}-r{rows}")
+    over = int_overrides(m, variant, seed=rows)
+    d = _device(w, overrides=over)
+    d.step()
+    lg, ids = d.results()
+    x_dev = d.residual()
+    a, batch, sub, r, kv, idx = oracle_state(w)
+    W = GeneratedWeights(m, w.seed, overrides=over)
+    out = forward(m, W, kv, sub, w.tokens[r], np.arange(rows), want_hidden=True)
+    for l in range(m.n_layers if variant == "qkv" else 1):
+        K, V = d.read_kv(l, sub["slot"])
+        Ko, Vo = kv.read(l, sub["slot"])
+        np.testing.assert_array_equal(K, Ko)
+        np.testing.assert_array_equal(V, Vo)
+    if variant == "qkv":
+        np.testing.assert_array_equal(lg, out["logits"])
+        np.testing.assert_array_equal(ids, out["ids"])
+    else:
+        np.testing.assert_array_equal(x_dev, out["x"])
+    d.release()
+
+
 # ---------------------------------------------------------------- attention invariants
 def _probe_overrides(m, v_row):
     """Embedding rows of ones (the normed input is exactly 1), Wv making every
