@@ -77,19 +77,28 @@ __device__ __forceinline__ int pair_k_index(int lane, int grp) {
 __device__ __forceinline__ int pair_v_block(int lane) { return lane >> 5; }
 __device__ __forceinline__ int pair_v_index(int lane) { return (lane & 15) + 32 * ((lane >> 4) & 1); }
 
+// The probabilities of a step as the B operand of P V, split into kPTerms
+// bf16 terms whose sum is the float32 probability to about 8 kPTerms
+// significant bits (each term is the bf16 rounding of what the previous
+// ones left over); the products of the terms are accumulated in float32.
+constexpr int kPTerms = 3;
+struct PTerms {
+  u32x4 t[kPTerms];
+};
+
 // One step over the keys at positions t0 .. t0 + 31, in two phases so that a
 // caller streaming K and V through registers can reload K as soon as the
 // scores are taken and V as soon as P V is issued.
 // pair_scores: S = K q from kg[G][c] (the K operands of group G), the online
-// softmax update of (m, l), and P = P_hi + P_lo (both bf16, about 16
-// significant bits, so the probabilities are not cut to bf16 precision before
-// P V) as the B operands ph, pl; alpha rescales O.  Keys at t >= t_end do not
+// softmax update of (m, l), and P as the bf16 terms pp (so the probabilities
+// are not cut to bf16 precision before P V); alpha rescales O.  Keys at
+// t >= t_end do not
 // count; with MASK a key also needs t <= lim.  Base 2 (sc = log2(e) /
 // sqrt(D)).  A column with no valid key yet keeps m = -inf and contributes
 // nothing.
 template <int D, bool MASK>
 __device__ __forceinline__ void pair_scores(const u32x4 (&qf)[D / 32], const u32x4 (&kg)[2][D / 32], int t0,
-                                            int t_end, int lim, float sc, float& m, float& l, u32x4& ph, u32x4& pl,
+                                            int t_end, int lim, float sc, float& m, float& l, PTerms& pp,
                                             float& alpha) {
   constexpr int KC = D / 32;
   const int tv = t0 + 8 * ((threadIdx.x & 63) >> 4);  // this lane's first key (of 8)
@@ -131,8 +140,13 @@ __device__ __forceinline__ void pair_scores(const u32x4 (&qf)[D / 32], const u32
   m = m_new;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    ph[j] = pack_bf2(p[2 * j], p[2 * j + 1]);
-    pl[j] = pack_bf2(p[2 * j] - bf2f(ph[j] & 0xffffu), p[2 * j + 1] - bf2f(ph[j] >> 16));
+    float r0 = p[2 * j], r1 = p[2 * j + 1];
+#pragma unroll
+    for (int t = 0; t < kPTerms; ++t) {
+      pp.t[t][j] = pack_bf2(r0, r1);
+      r0 -= bf2f(pp.t[t][j] & 0xffffu);
+      r1 -= bf2f(pp.t[t][j] >> 16);
+    }
   }
 }
 
@@ -140,8 +154,8 @@ __device__ __forceinline__ void pair_scores(const u32x4 (&qf)[D / 32], const u32
 // keys at t >= t_end are zeroed first: a slot past the end of a sequence may
 // hold a NaN pattern, and a zero probability times NaN is NaN.
 template <int D>
-__device__ __forceinline__ void pair_pv(u32x4 (&vt)[D / 16], int t0, int t_end, const u32x4& ph, const u32x4& pl,
-                                        float alpha, f32x4 (&o)[D / 16]) {
+__device__ __forceinline__ void pair_pv(u32x4 (&vt)[D / 16], int t0, int t_end, const PTerms& pp, float alpha,
+                                        f32x4 (&o)[D / 16]) {
   constexpr int VC = D / 16;
   const int tv = t0 + 8 * ((threadIdx.x & 63) >> 4);
   if (tv + 7 >= t_end) {
@@ -157,8 +171,9 @@ __device__ __forceinline__ void pair_pv(u32x4 (&vt)[D / 16], int t0, int t_end, 
 #pragma unroll
   for (int c = 0; c < VC; ++c) {
     o[c] *= alpha;
-    o[c] = mfma_16x16x32(vt[c], ph, o[c]);  // lane holds O[column lane % 16][dim 16c + 4 (lane / 16) + r]
-    o[c] = mfma_16x16x32(vt[c], pl, o[c]);
+    // lane holds O[column lane % 16][dim 16c + 4 (lane / 16) + r]
+#pragma unroll
+    for (int t = 0; t < kPTerms; ++t) o[c] = mfma_16x16x32(vt[c], pp.t[t], o[c]);
   }
 }
 
@@ -310,19 +325,19 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   // (the last pair is peeled so that the loop's loads are unconditional)
   for (int p = 0; p + 1 < n_pairs; ++p) {
     const int t0 = t_first + 2 * kBlock * p;
-    u32x4 ph, pl;
+    PTerms pp;
     float alpha;
-    pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, ph, pl, alpha);
+    pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, pp, alpha);
     load_k(kg, p + 1, cnt, w_lo);
-    pair_pv<D>(vt, t0, t_end, ph, pl, alpha, o);
+    pair_pv<D>(vt, t0, t_end, pp, alpha, o);
     load_v(vt, p + 1, cnt, w_lo);
   }
   if (n_pairs > 0) {
     const int t0 = t_first + 2 * kBlock * (n_pairs - 1);
-    u32x4 ph, pl;
+    PTerms pp;
     float alpha;
-    pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, ph, pl, alpha);
-    pair_pv<D>(vt, t0, t_end, ph, pl, alpha, o);
+    pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, pp, alpha);
+    pair_pv<D>(vt, t0, t_end, pp, alpha, o);
   }
 
   // ---- merge the waves of this workgroup

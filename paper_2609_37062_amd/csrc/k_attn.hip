@@ -150,10 +150,10 @@ __device__ __forceinline__ bool mq_walk(const u32x4 (&qf)[D / 32], const uint16_
             vt[c] = u32x4{lo[0], lo[1], hi[0], hi[1]};
           }
           const int t0 = kBlock * (b0 + 2 * p);
-          u32x4 ph, pl;
+          PTerms pp;
           float alpha;
-          pair_scores<D, MASK>(qf, kg, t0, t_end, lim, sc, m, l, ph, pl, alpha);
-          pair_pv<D>(vt, t0, t_end, ph, pl, alpha, o);
+          pair_scores<D, MASK>(qf, kg, t0, t_end, lim, sc, m, l, pp, alpha);
+          pair_pv<D>(vt, t0, t_end, pp, alpha, o);
         }
       }
     }

@@ -11,13 +11,14 @@ largest float32-vs-float64 logit spread)); a row whose top-2 gap exceeds
 twice that bound is decided and must agree exactly, and every other
 disagreement must be within twice the bound of the maximum.  The raw exact
 agreement is reported beside the float32 oracle's own raw agreement with the
-float64 one.  On the 2-layer model one bf16 rounding flip moves logits by
-~0.01, so raw agreement there is set by the near-tie rate and by how often
-the implementation flips a rounding: the device's attention carries its
-softmax probabilities as two bf16 terms (about 16 significant bits), so its
-attention outputs flip a bf16 rounding more often than a float32 run's do
-(measured: device 10206/10240 = 99.67% raw, the float32 oracle 99.92%, the
-1-layer model 99.92%, every decided row exact).  The full-size workloads add
+float64 one and must reach 99.9%.  On the 2-layer model one bf16 rounding
+flip moves logits by ~0.01, so raw agreement there is set by the near-tie
+rate and by how often the implementation flips a rounding.  The device's
+attention carries its softmax probabilities into P V as three bf16 terms
+(about 24 significant bits, as a float32 run has); with two terms (about 16
+bits) its attention outputs flipped more roundings and raw agreement was
+10206/10240 = 99.67% against the float32 oracle's 99.92%; with three it is
+10233/10240 = 99.93% (every decided row exact).  The full-size workloads add
 their head rows in test_gpu_fullsize.py.
 """
 import numpy as np
@@ -79,6 +80,5 @@ def test_greedy_agreement_over_10k_rows():
           f"float32 oracle {f32}/{n} = {f32 / n:.5f}, decided rows {dec}/{n} all exact", flush=True)
     assert n >= 10_000
     assert dec == tiny["decided_agree"] + mid["decided_agree"]
-    # the 1-layer model: near-ties below the bf16 flip level are rare
-    assert tiny["gpu"] / tiny["rows"] >= 0.998
-    assert gpu / n >= 0.995
+    assert tiny["gpu"] / tiny["rows"] >= 0.999
+    assert gpu / n >= 0.999
