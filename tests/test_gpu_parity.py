@@ -173,8 +173,9 @@ def test_mid_shared_prefix():
 @pytest.mark.parametrize("shared,bps", [(1, 0), (0, 0), (1, 8)])
 def test_mid_prefix_groups(shared, bps):
     """Two shared-prefix groups (160 and 96 tokens, one of 45 members so a
-    group spans several 64-column work items) beside sequences of no group;
-    prefixes read once per group (shared 1) or once per sequence (0)."""
+    group spans several 64-column work items, a row's query heads split
+    between two of them) beside sequences of no group; prefixes read once per
+    group (shared 1) or once per sequence (0)."""
     from paper_2609_37062_amd.runner import DeviceRun
     rng = np.random.default_rng(21)
     suf = rng.integers(1, 90, size=45 + 5 + 4)
@@ -191,8 +192,45 @@ def test_mid_prefix_groups(shared, bps):
     d.step()
     lg2, ids2 = d.results()
     assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
-    st, *_ = _check(w, lg, ids, [0, 1, 3, 20, 44, 45, 47, 49, 50, 53])
+    st, *_ = _check(w, lg, ids, [0, 1, 3, 20, 21, 44, 45, 47, 49, 50, 53])
     print(st)
+
+
+def test_shared_prefix_graph_replay():
+    """A decode pass with shared-prefix groups captured in a graph: every
+    replay, with eager passes between, reproduces the eager pass bit for bit
+    (the split-merge arrival counters are back at zero after every pass)."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    suf = np.random.default_rng(33).integers(1, 60, size=30)
+    w = prefix_groups_workload(MID, [(192, 24), (64, 4)], suf, seed=33, name="mid-groups-graph")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(0, 8)
+    d.step()
+    lg1, ids1 = d.results()
+    st, *_ = _check(w, lg1, ids1, [0, 5, 23, 24, 27, 28, 29])
+    print(st)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        d.step(stream=s.cuda_stream)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        d.step(stream=torch.cuda.current_stream().cuda_stream)
+    for _ in range(3):
+        d.logits.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        lg, ids = d.results()
+        np.testing.assert_array_equal(lg, lg1)
+        np.testing.assert_array_equal(ids, ids1)
+        d.step()
+        lg, ids = d.results()
+        np.testing.assert_array_equal(lg, lg1)
+    del g
+    d.release()
 
 
 @pytest.mark.parametrize("bps", [0, 8])

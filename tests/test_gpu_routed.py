@@ -22,7 +22,7 @@ torch = pytest.importorskip("torch")
 
 from oracle.model import GeneratedWeights, forward, route_maps  # noqa: E402
 from workloads import routes  # noqa: E402
-from workloads.configs import ModelCfg, decode_workload, mixed_workload, workload  # noqa: E402
+from workloads.configs import ModelCfg, decode_workload, mixed_workload, prefix_groups_workload, workload  # noqa: E402
 
 from helpers import assert_bf16_close, e2e_compare, oracle_state  # noqa: E402
 
@@ -128,6 +128,30 @@ def test_routed_decode_matches_oracle(policy, rows):
     print(f"[gpu] routed {policy} rows={rows}: {st} cohorts {cnt.tolist()}", flush=True)
     _first_routed_kv(d, w, tape, subset)
     # a replay is bit-identical
+    d.step_routed()
+    lg2, ids2 = d.results()
+    np.testing.assert_array_equal(lg, lg2)
+    np.testing.assert_array_equal(ids, ids2)
+    d.release()
+
+
+def test_routed_decode_with_shared_prefixes():
+    """Shared-prefix groups in a routed pass (Project-Only members read no KV
+    of their own and emit zero; the prefix partials of RUN members are folded
+    in): end to end against the oracle, and a second pass bit-identical."""
+    m = MIDR
+    suf = np.random.default_rng(61).integers(1, 50, size=26)
+    w = prefix_groups_workload(m, [(160, 20), (64, 3)], suf, seed=61, name="routed-groups")
+    req = np.arange(w.n_seqs)
+    pos = np.array([s.ctx for s in w.seqs])
+    tape = routes.random_skip(5, m.n_routed, req, pos, 1.0, 0.5)
+    d = _device(w)
+    d.eng.set_tuning(0, 8)
+    d.set_route(*tape)
+    d.step_routed()
+    lg, ids = d.results()
+    st, *_ = e2e_compare(w, lg, ids, [0, 3, 19, 20, 22, 23, 25], route=tape)
+    print(f"[gpu] routed groups: {st}", flush=True)
     d.step_routed()
     lg2, ids2 = d.results()
     np.testing.assert_array_equal(lg, lg2)
