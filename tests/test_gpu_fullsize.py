@@ -142,6 +142,13 @@ def test_config2_3b_decode_b16():
     _check(workload(2), [0, 15])
 
 
+def test_config2_persistent_step():
+    """The persistent decode-step kernel (one launch per pass, tuning key 2 =
+    2; the pass fails rather than fall back when it is not eligible) at the
+    3B batch-16 workload: the same layer-local, head and end-to-end checks."""
+    _check(workload(2), [0, 15], tuning=((2, 2),))
+
+
 def test_config2_isolated_paths():
     _isolated_paths(workload(2), [0, 5])
 
