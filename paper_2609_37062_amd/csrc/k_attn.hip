@@ -107,7 +107,11 @@ __device__ __forceinline__ bool mq_walk(const u32x4 (&qf)[D / 32], const uint16_
 #pragma unroll
           for (int hb = 0; hb < 2; ++hb) {
             const size_t blk = static_cast<size_t>(tbl[min(2 * (st * NH + hp) + hb, cnt - 1)]);
-            const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + lane;
+            // block B's K pieces land swizzled (piece j at slot j ^ 4): a
+            // compute wave's 16 lanes of one LDS read phase then take 16
+            // distinct 16-byte bank groups (8 from each block) instead of
+            // the same 8 twice
+            const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + blk * kv_stride) + (lane ^ (hb ? 4 : 0));
             const u32x4* vp = reinterpret_cast<const u32x4*>(vbase + blk * kv_stride) + lane;
 #pragma unroll
             for (int g = 0; g < NCH; ++g)
@@ -130,6 +134,7 @@ __device__ __forceinline__ bool mq_walk(const u32x4 (&qf)[D / 32], const uint16_
     } else {
       const int my_pairs = (my_cnt + 1) / 2;
       const int kb = pair_k_block(lane), k0 = pair_k_index(lane, 0), k1 = pair_k_index(lane, 1);
+      const int ksw = kb ? 4 : 0;  // block B's K pieces are stored swizzled (see the loader)
       const int vb = pair_v_block(lane), vi = pair_v_index(lane);
       for (int st = 0; st < n_steps; ++st) {
         barrier_after_lds_reads();
@@ -141,8 +146,8 @@ __device__ __forceinline__ bool mq_walk(const u32x4 (&qf)[D / 32], const uint16_
           u32x4 vt[VC];
 #pragma unroll
           for (int c = 0; c < KC; ++c) {
-            kg[0][c] = kp[c * 64 + k0];
-            kg[1][c] = kp[c * 64 + k1];
+            kg[0][c] = kp[c * 64 + (k0 ^ ksw)];
+            kg[1][c] = kp[c * 64 + (k1 ^ ksw)];
           }
 #pragma unroll
           for (int c = 0; c < VC; ++c) {
