@@ -417,7 +417,10 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  * key 8: projections of a row-tiled pass (more than 128 rows): 1 (the
  *        default) orders the workgroups so that the row tiles of one weight
  *        slice run together on one XCD and share its L2; 0 keeps the
- *        dispatch order. */
+ *        dispatch order.
+ * key 9: the workgroup count the shared-prefix work items of a decode pass
+ *        aim for when a group's prefix is split (1..4096, default 192); it
+ *        applies to batches built after the call (vsk_batch_build). */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

@@ -365,7 +365,7 @@ int vsk_batch_build(vsk_handle* h, const int64_t* seqs_host, const int32_t* q_le
   BatchHost b;
   int st = build_batch(h->alloc, seqs_host, q_lens_host, n_seqs, b, h->err);
   if (st != VSK_OK) return st;
-  plan_prefix_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads, h->cfg.n_kv_heads);
+  plan_prefix_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads, h->cfg.n_kv_heads, h->pfx_target);
   plan_prefill_items(b, h->cfg.n_q_heads / h->cfg.n_kv_heads, kBlock);
   h->bh = std::move(b);
   h->batch_built = true;
@@ -785,6 +785,10 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       if (value < -1 || value > 4096)
         return fail(h, VSK_E_ARG, "residual split target must be -1 (no split), 0 (default) or 1..4096");
       h->resid_target = value;
+      return VSK_OK;
+    case 9:
+      if (value < 1 || value > 4096) return fail(h, VSK_E_ARG, "shared-prefix work item target must be 1..4096");
+      h->pfx_target = value;
       return VSK_OK;
     case 8:
       if (value < 0 || value > 1) return fail(h, VSK_E_ARG, "XCD remap switch must be 0 or 1");

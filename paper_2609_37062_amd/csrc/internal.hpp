@@ -166,6 +166,7 @@ struct Handle {
   int exec_mode = 0;   // 0 automatic, 1 one kernel per operation, 2 persistent step kernel
   int gemm_shape = 0;  // projection launch shape for 4 or 8 row groups (0 default)
   int shared_prefix = 1;  // read shared prefixes once per group (decode passes)
+  int pfx_target = 192;   // workgroups the shared-prefix work items of a pass aim for
   int resid_target = 0;   // residual projections: split-K workgroup target (0 default, -1 no split)
   int qkv_target = 0;     // QKV at 4..8 row groups: split-K workgroup target (0 default, -1 no split)
   int prefill_attn = 1;   // prefill rows through the causal multi-row kernel (0: one row per work item)
