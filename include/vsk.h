@@ -238,12 +238,14 @@ int vsk_prefill_chunk(vsk_handle* h, const int32_t* ids_dev, const int32_t* logi
  * appendix "Natural Stopping and the Output Lengths") over given logits: logits_dev
  * row-major [rows][vocab] of dtype 0 = bf16 or 1 = fp32; ids_dev int32[rows]
  * receives, per row, the lowest index of the maximum value.  NaN never wins;
- * a row with no non-NaN value gives 0; a row of -inf gives 0.  rows >= 1,
- * vocab >= 1 (any size), both pointers device memory owned by the caller.
- * Uses no workspace beyond its arguments.  VSK_E_ARG on a null pointer, a
- * non-positive size or an unknown dtype. */
+ * a row with no non-NaN value gives 0 and is flagged in no_value_dev
+ * (nullable int32[rows]: 1 for such a row, else 0); a row of -inf gives 0
+ * (unflagged: -inf is a value).  rows >= 1, vocab >= 1 (any size), every
+ * pointer device memory owned by the caller.  Uses no workspace beyond its
+ * arguments.  VSK_E_ARG on a null logits or ids pointer, a non-positive
+ * size or an unknown dtype. */
 int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab,
-                      int32_t* ids_dev, void* stream);
+                      int32_t* ids_dev, int32_t* no_value_dev, void* stream);
 
 /* ----------------------------------------------------------------- routed mode
  * One routed layer per Algorithm 1 (Section 3.1, "Route-Guided Cohort

@@ -726,9 +726,10 @@ int vsk_route_maps_read(vsk_handle* h, int32_t* run_dev, int32_t* proj_dev, int3
 }
 
 int vsk_argmax_sample(const void* logits_dev, int32_t dtype, int32_t rows, int32_t vocab, int32_t* ids_dev,
-                      void* stream) {
+                      int32_t* no_value_dev, void* stream) {
   if (!logits_dev || !ids_dev || rows < 1 || vocab < 1 || (dtype != 0 && dtype != 1)) return VSK_E_ARG;
-  hipError_t e = launch_argmax_logits(logits_dev, dtype, rows, vocab, ids_dev, static_cast<hipStream_t>(stream));
+  hipError_t e =
+      launch_argmax_logits(logits_dev, dtype, rows, vocab, ids_dev, no_value_dev, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? VSK_OK : VSK_E_HIP;
 }
 

@@ -209,7 +209,8 @@ hipError_t launch_kv_write(const Handle& h, int layer, const int32_t* slots, int
                            const uint16_t* v, hipStream_t s);
 hipError_t launch_kv_read(const Handle& h, int layer, const int32_t* slots, int n, uint16_t* k, uint16_t* v,
                           hipStream_t s);
-hipError_t launch_argmax_logits(const void* logits, int dtype, int rows, int vocab, int32_t* ids, hipStream_t s);
+hipError_t launch_argmax_logits(const void* logits, int dtype, int rows, int vocab, int32_t* ids, int32_t* no_value,
+                                hipStream_t s);
 
 struct PassArgs {
   const int32_t* ids;

@@ -433,7 +433,7 @@ hipError_t launch_argmax_partials(const float* pv, const int* pi, int n_groups, 
 
 template <int DT>
 __global__ __launch_bounds__(1024) void k_argmax_logits(const void* __restrict__ logits, int vocab,
-                                                        int32_t* __restrict__ ids) {
+                                                        int32_t* __restrict__ ids, int32_t* __restrict__ no_value) {
   const int r = blockIdx.x;
   float bv = -INFINITY;
   int bi = INT_MAX;
@@ -446,14 +446,18 @@ __global__ __launch_bounds__(1024) void k_argmax_logits(const void* __restrict__
     if (!(v != v)) am_merge(bv, bi, v, j);
   }
   block_am_reduce(bv, bi);
-  if (threadIdx.x == 0) ids[r] = (bi == INT_MAX) ? 0 : bi;
+  if (threadIdx.x == 0) {
+    ids[r] = (bi == INT_MAX) ? 0 : bi;
+    if (no_value != nullptr) no_value[r] = bi == INT_MAX ? 1 : 0;  // every value NaN
+  }
 }
 
-hipError_t launch_argmax_logits(const void* logits, int dtype, int rows, int vocab, int32_t* ids, hipStream_t s) {
+hipError_t launch_argmax_logits(const void* logits, int dtype, int rows, int vocab, int32_t* ids, int32_t* no_value,
+                                hipStream_t s) {
   if (dtype == 0)
-    hipLaunchKernelGGL(k_argmax_logits<0>, dim3(rows), dim3(1024), 0, s, logits, vocab, ids);
+    hipLaunchKernelGGL(k_argmax_logits<0>, dim3(rows), dim3(1024), 0, s, logits, vocab, ids, no_value);
   else
-    hipLaunchKernelGGL(k_argmax_logits<1>, dim3(rows), dim3(1024), 0, s, logits, vocab, ids);
+    hipLaunchKernelGGL(k_argmax_logits<1>, dim3(rows), dim3(1024), 0, s, logits, vocab, ids, no_value);
   return hipGetLastError();
 }
 

@@ -85,7 +85,7 @@ SIGNATURES = [
     ("vsk_decode_step", C.c_int, [_VP, _VP, _VP, _VP, _VP, _SZ, _VP]),
     ("vsk_decode_step_scratch", C.c_int, [_VP, _VP, _VP, _VP, _VP]),
     ("vsk_prefill_chunk", C.c_int, [_VP, _VP, _VP, _I32, _VP, _VP, _VP, _SZ, _VP]),
-    ("vsk_argmax_sample", C.c_int, [_VP, _I32, _I32, _I32, _VP, _VP]),
+    ("vsk_argmax_sample", C.c_int, [_VP, _I32, _I32, _I32, _VP, _VP, _VP]),
     ("vsk_set_tuning", C.c_int, [_VP, _I32, _I32]),
     ("vsk_residual_copy", C.c_int, [_VP, _VP, _I32, _VP]),
     ("vsk_routed_weight_bytes", _SZ, [C.POINTER(ModelCfg), _I32, _I32]),
@@ -147,8 +147,8 @@ def kv_pool_bytes(m, n_blocks) -> int:
     return lib().vsk_kv_pool_bytes(C.byref(c), n_blocks)
 
 
-def argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, stream=None):
-    st = lib().vsk_argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, stream)
+def argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, stream=None, no_value_ptr=None):
+    st = lib().vsk_argmax_sample(logits_ptr, dtype, rows, vocab, ids_ptr, no_value_ptr, stream)
     if st != VSK_OK:
         raise VskError(st, "argmax_sample")
 

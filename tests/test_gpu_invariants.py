@@ -15,7 +15,8 @@ pass, all through the C ABI.
     token of those blocks (Invariant 1 writes exactly the rows' own slots);
   * vsk_argmax_sample: bit-exact against the oracle's lowest-index argmax on
     bf16 and fp32 logits with planted ties, NaN, all-NaN and all -inf rows,
-    +inf, signed zeros, at vocabulary 128256 and odd sizes.
+    +inf, signed zeros, at vocabulary 128256 and odd sizes; its flag marks
+    exactly the all-NaN rows.
 """
 import numpy as np
 import pytest
@@ -294,13 +295,22 @@ def test_argmax_sample_is_bit_exact(dtype, vocab):
         t = torch.from_numpy(z.astype(np.float32)).cuda()
         zin = z.astype(np.float32).astype(np.float64)
     ids = torch.full((len(z),), -7, dtype=torch.int32, device="cuda")
+    flags = torch.full((len(z),), -7, dtype=torch.int32, device="cuda")
     print(f"[gpu] argmax_sample dtype={dtype} vocab={vocab} rows={len(z)}", flush=True)
-    vsk.argmax_sample(t.data_ptr(), dtype, len(z), vocab, ids.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    vsk.argmax_sample(t.data_ptr(), dtype, len(z), vocab, ids.data_ptr(), torch.cuda.current_stream().cuda_stream,
+                      flags.data_ptr())
     torch.cuda.synchronize()
     got = ids.cpu().numpy()
     want = nm.argmax_lowest(zin)
     np.testing.assert_array_equal(got, want)
     assert got[3] == 0 and got[4] == 0
+    # the flag marks exactly the rows with no value that is not NaN
+    np.testing.assert_array_equal(flags.cpu().numpy(), np.isnan(zin).all(axis=1).astype(np.int32))
+    # without the flag buffer the ids are the same
+    ids2 = torch.full((len(z),), -7, dtype=torch.int32, device="cuda")
+    vsk.argmax_sample(t.data_ptr(), dtype, len(z), vocab, ids2.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ids2.cpu().numpy(), got)
 
 
 def test_argmax_sample_rejects_bad_arguments():
