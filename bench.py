@@ -45,7 +45,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=2, help="decode workload of the value line (2, 3 or 5)")
     ap.add_argument("--no-batch64", action="store_true", help="skip the batch-64 shared-prefix line")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")

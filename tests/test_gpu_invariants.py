@@ -10,6 +10,7 @@ pass, all through the C ABI.
     output is exactly bf16 1.0 (seen through Wo = I as a residual of 2.0);
   * V = one-hot(position): the attention output is the softmax row P itself;
   * a first token (no cached context) attends only to itself: o = v exactly;
+  * Wq = 0: uniform attention, each output the mean of its head's values;
   * no stray KV writes: after a pass every pool block other than those
     holding the pass's new slots is byte-identical, and so is every other
     token of those blocks (Invariant 1 writes exactly the rows' own slots);
@@ -187,6 +188,33 @@ def test_one_hot_v_exposes_the_softmax_row():
     assert np.all(diff[big] <= ulp[big]), diff.max()  # one bf16 ulp at most
     assert np.all(diff[~big] <= 2.0 ** -16)
     assert np.mean(diff == 0) > 0.9, np.mean(diff == 0)
+    d.release()
+
+
+def test_zero_queries_average_v():
+    """Wq = 0: every score is 0, the softmax is uniform, and each head's
+    output is the mean of its KV head's values over keys 0..p (cached ones
+    and the row's own new v); with Wo = I and unit embeddings the residual is
+    1 + o.  Against the oracle within one bf16 ulp (the mean's float32 sum
+    may round either way), with one split per row and with merged splits."""
+    m = TINY
+    ctx = np.random.default_rng(4).integers(1, 300, size=10)
+    w = decode_workload(m, ctx, seed=4, name="q-zero")
+    over = {("embed", -1): np.ones((m.vocab, m.hidden)), ("wq", 0): np.zeros((m.q_dim, m.hidden)),
+            ("wo", 0): np.eye(m.hidden), ("w_down", 0): np.zeros((m.hidden, m.ffn))}
+    d = _device(w, overrides=over)
+    a, batch, sub, r, kv, idx = oracle_state(w)
+    W = GeneratedWeights(m, w.seed, overrides=over)
+    o_or = forward(m, W, kv, sub, w.tokens[r], None)["x"] - 1.0
+    mag = np.maximum(np.abs(o_or), 2.0 ** -126)
+    ulp = np.exp2(np.floor(np.log2(mag)) - 7)
+    for bps in (0, 8):
+        d.eng.set_tuning(0, bps)
+        d.step()
+        o_dev = d.residual() - 1.0
+        diff = np.abs(o_dev - o_or)
+        assert np.all(diff <= np.maximum(ulp * 1.0001, 2.0 ** -16)), (bps, diff.max())
+        assert np.mean(diff == 0) > 0.9, np.mean(diff == 0)
     d.release()
 
 
