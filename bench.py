@@ -544,7 +544,7 @@ def sweep(torch, rows_list, steps=10, warmup=3, ctx=1024, s_skip=0.5):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1", "n_gpus": a.gpus}))
+        print(json.dumps({"error": "the library runs on one GPU; --gpus must be 1", "n_gpus": a.gpus}))
         sys.exit(2)
     import torch
 

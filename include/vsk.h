@@ -48,7 +48,7 @@ enum {
   VSK_E_SHARED_WRITE = -4, /* a new position falls in a block shared by several sequences */
   VSK_E_STATE = -5,        /* call out of order (unknown/duplicate sequence, nothing bound) */
   VSK_E_HIP = -6,          /* the HIP runtime reported an error */
-  VSK_E_UNSUPPORTED = -7   /* shape this build has no kernel for */
+  VSK_E_UNSUPPORTED = -7   /* shape the library has no kernel for */
 };
 
 /* Model shape.  block_size must be 16; head_dim 64 or 128; n_q_heads a

@@ -8,7 +8,7 @@ from oracle.kvcache import BlockAllocator, PagedKV, build_batch, select_seqs
 from oracle.model import GeneratedWeights, forward
 from workloads.setup import apply_recipe, kv_fill_ranges, kv_values_np
 
-# logits tolerance against the oracle's float64 z (the spec bar); the
+# logits tolerance against the oracle's float64 z (the logits tolerance of the decode step); the
 # magnitude from which a bf16 output cannot meet it (half-ulp 1/32); the
 # factor on the oracle's own float32-vs-float64 spread that bounds a row end
 # to end where that spread exceeds the bar (see compare_logits)
@@ -137,7 +137,7 @@ def oracle_run(w, seq_subset=None, overrides=None, dist=None, dtype="f64", route
 def compare_logits(gpu_logits, gpu_ids, z, tol=LOGIT_TOL, z32=None, k=SPREAD_K):
     """Check bf16 device logits and greedy ids against the oracle's float64 z.
 
-    The bound is `tol` (the spec bar), or, given the oracle's float32
+    The bound is `tol` (the logits tolerance of the decode step), or, given the oracle's float32
     contract-mode z32 of the same rows, max(tol, k * spread) with spread =
     max |z32 - z| over the rows compared: a correct float32 implementation
     drifts from the float64 definition by about that much, and no less.  One

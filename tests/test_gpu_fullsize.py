@@ -5,7 +5,7 @@ Sequences of a pass are independent, so the oracle recomputes a few sampled
 sequences of the full batch end to end while the device runs the whole batch.
 
 Checks per workload:
-  * head, on every row that returns logits (the spec bar): the
+  * head, on every row that returns logits (the logits tolerance of the decode step): the
     oracle's final RMSNorm + lm_head applied to the device's own final
     residual stream must give the device's bf16 logits within 2e-2
     (logit_bound), and the device's greedy ids must equal the oracle's on
