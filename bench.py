@@ -191,7 +191,7 @@ def repeat_ci(torch, fn, steps, stream, reps=5):
             "ci95_ms": [round(m - half, 4), round(m + half, 4)]}
 
 
-PHASES = ("qkv", "attention", "o_proj", "gate_up", "down")
+PHASES = ("norm_attn", "qkv", "attention", "o_proj", "norm_mlp", "gate_up", "down")
 
 
 def step_timeline(torch, d, reps=3):
@@ -212,10 +212,11 @@ def step_timeline(torch, d, reps=3):
         t = buf.cpu().numpy().reshape(n_pts, n_wgs, 2).astype(np.float64) * 0.01  # 100 MHz -> us
         runs.append(t)
     d.eng.set_step_trace(0, 0)
-    L = (n_pts - 2) // 5
+    P = len(PHASES)
+    L = (n_pts - 3) // P
     out = {}
-    for name, pts in [("embed", [0])] + [(PHASES[k], [1 + 5 * l + k for l in range(L)]) for k in range(5)] + \
-            [("lm_head", [5 * L + 1])]:
+    for name, pts in [("embed", [0])] + [(PHASES[k], [1 + P * l + k for l in range(L)]) for k in range(P)] + \
+            [("norm_final", [P * L + 1]), ("lm_head", [P * L + 2])]:
         span, busy, sync = [], [], []
         for t in runs:
             for p in pts:

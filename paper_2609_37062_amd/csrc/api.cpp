@@ -114,6 +114,7 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
     w.s_q = o; o = align_up(o + L * R * Nq * 2);
     w.s_o = o; o = align_up(o + L * kStepMaxRows * Nq * 2);
     w.s_a = o; o = align_up(o + L * kStepMaxRows * F * 2);
+    w.s_n = o; o = align_up(o + nx * kStepMaxRows * H * 2);
     w.s_am = o; o = align_up(o + static_cast<size_t>(c.vocab / 16) * R * 8);
     w.s_flags = o; o = align_up(o + static_cast<size_t>(step_syncs(c.n_layers)) * kSyncCounters * kFlagWords * 4);
     w.s_err = o; o = align_up(o + 4);
@@ -913,6 +914,7 @@ static hipError_t run_step(Handle& h, const PassArgs& pa, int n_wgs, hipStream_t
   a.qs = reinterpret_cast<uint16_t*>(ws + wl.s_q);
   a.os = reinterpret_cast<uint16_t*>(ws + wl.s_o);
   a.as = reinterpret_cast<uint16_t*>(ws + wl.s_a);
+  a.ns = reinterpret_cast<uint16_t*>(ws + wl.s_n);
   a.am_val = reinterpret_cast<float*>(ws + wl.s_am);
   a.am_idx = reinterpret_cast<int*>(ws + wl.s_am + static_cast<size_t>(c.vocab / 16) * wl.max_rows * 4);
   a.flags = reinterpret_cast<unsigned*>(ws + wl.s_flags);

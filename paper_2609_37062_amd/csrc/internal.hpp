@@ -112,7 +112,7 @@ struct WsLayout {
   // persistent decode step (present when max_rows <= kStepMaxRows and the
   // model shape is covered): per-layer activations, sync flags, error word, epoch
   bool step = false;
-  size_t s_x, s_ssq, s_q, s_o, s_a, s_am, s_flags, s_err, s_epoch;
+  size_t s_x, s_ssq, s_q, s_o, s_a, s_n, s_am, s_flags, s_err, s_epoch;
 };
 
 // attention split: 16-token blocks per split-K work item (tunable, >= kAttnMinBps)

@@ -34,10 +34,13 @@
 // waves of a workgroup split K (wave w takes K steps w, w+8, ...), keep kPF
 // weight tiles in flight in a register ring that runs on across unit
 // boundaries, and are reduced in LDS in wave order, as the per-op projection
-// kernel does.  The RMSNorm of a projection's input is done while staging
-// that input: each wave normalises its K steps of the 16 rows into LDS,
-// h = bf16(x * g / sqrt(mean(x^2) + eps)), from the per-tile sums of x^2 the
-// producing residual projection wrote.
+// kernel does.  The RMSNorm of a projection's input is a phase of its own:
+// after the residual is complete every workgroup normalises a share of the
+// 16 rows, h = bf16(x * g / sqrt(mean(x^2) + eps)) from the per-tile sums of
+// x^2 the producing residual projection wrote, into the input frags of the
+// projection; one more synchronisation point, and the projection streams
+// them like any other input (the weight stream is already running across
+// both points).
 #include <climits>
 #include <cmath>
 
@@ -146,15 +149,35 @@ struct NormIn {
   int parts;
 };
 
-// Stage the normalised input of a projection in LDS: wave w holds its K
-// steps w, w+8, ... of the 16 rows as B-operand frags, h = bf16(x g r) with
-// r = 1/sqrt(sum x^2 / H + eps) summed from `parts` per-tile partials in a
-// fixed order (the same order and arithmetic as the per-op norm kernel).
-__device__ __forceinline__ void stage_norm(const float* __restrict__ x, const uint16_t* __restrict__ gain,
-                           const double* __restrict__ ssq, int parts, int R, int H, float eps, unsigned char* lds) {
+// The normalised input of a projection, h = bf16(x g r) with
+// r = 1/sqrt(sum x^2 / H + eps), written as B-operand frags of the 16 rows
+// ([K / 32][64 lanes] of 8 bf16) to memory, each workgroup its share of the
+// frags' lanes.  r is summed from `parts` per-tile partials in a fixed order
+// (the same order and arithmetic as the per-op norm kernel): every
+// workgroup takes the sums of all 16 rows, wave w those of rows 2w and 2w+1.
+// The first element loads are issued before the partials are summed, so
+// the phase costs about one memory round trip.
+__device__ __forceinline__ void norm_slice(const NormIn& ni, int R, int H, float eps, uint16_t* __restrict__ xf,
+                                           unsigned char* lds) {
   const int tid = opaque_tid();
   const int lane = tid & 63, w = tid >> 6;
-  double* s_r = reinterpret_cast<double*>(lds + static_cast<size_t>(H / 256) * kWaves * 1024 + kLdsRed);
+  double* s_r = reinterpret_cast<double*>(lds + kLdsRed);
+  const int n_tasks = (H / 32) * 64;  // one per lane of every frag
+  const int lo = static_cast<int>(static_cast<int64_t>(n_tasks) * blockIdx.x / gridDim.x);
+  const int hi = static_cast<int>(static_cast<int64_t>(n_tasks) * (blockIdx.x + 1) / gridDim.x);
+  float4 va, vb;
+  u32x4 gv;
+  int t = lo + tid;
+  auto load = [&]() {
+    const int fl = t & 63, kt = t >> 6;
+    const int row = fl & 15, c = 32 * kt + 8 * (fl >> 4);
+    const bool ok = t < hi && row < R;
+    const float* xp = ni.x + static_cast<size_t>(ok ? row : 0) * H + (ok ? c : 0);
+    va = __builtin_bit_cast(float4, ldg4(xp));
+    vb = __builtin_bit_cast(float4, ldg4(xp + 4));
+    gv = ldg4(ni.gain + (t < hi ? c : 0));
+  };
+  load();
   // this wave's two rows: every partial this lane adds is loaded before the
   // first sum (at most kParts / 64 per row), then added in partial order
   constexpr int kPl = kMaxParts / 64;
@@ -165,7 +188,7 @@ __device__ __forceinline__ void stage_norm(const float* __restrict__ x, const ui
 #pragma unroll
     for (int q = 0; q < kPl; ++q) {
       const int p = lane + 64 * q;
-      pv[k][q] = (row < R && p < parts) ? as_global(ssq)[static_cast<size_t>(p) * R + row] : 0.0;
+      pv[k][q] = (row < R && p < ni.parts) ? as_global(ni.ssq)[static_cast<size_t>(p) * R + row] : 0.0;
     }
   }
 #pragma unroll
@@ -174,45 +197,26 @@ __device__ __forceinline__ void stage_norm(const float* __restrict__ x, const ui
     double s = 0.0;
 #pragma unroll
     for (int q = 0; q < kPl; ++q)
-      if (lane + 64 * q < parts) s += pv[k][q];
+      if (lane + 64 * q < ni.parts) s += pv[k][q];
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
     if (lane == 0 && row < R) s_r[row] = 1.0 / sqrt(s / static_cast<double>(H) + static_cast<double>(eps));
   }
   __syncthreads();
-  const int row = lane & 15, c8 = 8 * (lane >> 4);
-  const int S = H / 256;
-  const double rr = row < R ? s_r[row] : 0.0;
-  u32x4* dst = reinterpret_cast<u32x4*>(lds) + static_cast<size_t>(w) * S * 64 + lane;
-  // four K steps per round: their loads are all issued before the first
-  // product (one memory round trip per round instead of one per K step),
-  // and the products are taken in double
-  constexpr int kR = 4;
-  for (int i0 = 0; i0 < S; i0 += kR) {
-    float4 va[kR], vb[kR];
-    u32x4 gv[kR];
+  while (t < hi) {
+    const int row = t & 15;
+    u32x4 o = u32x4{0u, 0u, 0u, 0u};
+    if (row < R) {
+      const double rr = s_r[row];
+      const float e[8] = {va.x, va.y, va.z, va.w, vb.x, vb.y, vb.z, vb.w};
 #pragma unroll
-    for (int k = 0; k < kR; ++k) {
-      const int c = 32 * (w + kWaves * (i0 + k)) + c8;
-      const bool ok = row < R && i0 + k < S;
-      const float* xp = x + static_cast<size_t>(ok ? row : 0) * H + (ok ? c : 0);
-      va[k] = __builtin_bit_cast(float4, ldg4(xp));
-      vb[k] = __builtin_bit_cast(float4, ldg4(xp + 4));
-      gv[k] = ldg4(gain + (ok ? c : 0));
+      for (int q = 0; q < 4; ++q)
+        o[q] = d2bf(static_cast<double>(e[2 * q]) * bf2f(gv[q] & 0xffffu) * rr) |
+               (d2bf(static_cast<double>(e[2 * q + 1]) * bf2f(gv[q] >> 16) * rr) << 16);
     }
-#pragma unroll
-    for (int k = 0; k < kR; ++k) {
-      if (i0 + k >= S) break;
-      u32x4 o = u32x4{0u, 0u, 0u, 0u};
-      if (row < R) {
-        const float e[8] = {va[k].x, va[k].y, va[k].z, va[k].w, vb[k].x, vb[k].y, vb[k].z, vb[k].w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          o[q] = d2bf(static_cast<double>(e[2 * q]) * bf2f(gv[k][q] & 0xffffu) * rr) |
-                 (d2bf(static_cast<double>(e[2 * q + 1]) * bf2f(gv[k][q] >> 16) * rr) << 16);
-      }
-      dst[static_cast<size_t>(i0 + k) * 64] = o;
-    }
+    store_wt(xf + static_cast<size_t>(t) * 8, o);
+    t += blockDim.x;
+    if (t < hi) load();
   }
 }
 
@@ -355,10 +359,11 @@ __device__ __forceinline__ void epilogue(const Epi& e, int unit, const f32x4 v, 
 
 // One projection phase of this workgroup, entered right after the previous
 // phase's work: arrive at `point`, start the weight stream (the first kPF
-// tiles of each wave do not depend on the input), wait for every workgroup,
-// stage the input (XN: normalised from x into LDS; else its frags stream from
-// g.Xf beside the weights), then run the units.  Returns false when a wait
-// of this pass failed.
+// tiles of each wave do not depend on the input), wait for every workgroup;
+// XN: write this workgroup's share of the normalised input frags to g.Xf,
+// arrive at `point + 1` and wait again; then run the units, the input frags
+// streaming from g.Xf beside the weights.  Returns false when a wait of
+// this pass failed.
 template <int EPI, bool XN>
 __device__ __forceinline__ bool gemm_phase(const GemmPh& g, const Epi& e, const NormIn& ni, float eps, unsigned char* lds,
                            const Sync& sy, int point) {
@@ -395,19 +400,18 @@ __device__ __forceinline__ bool gemm_phase(const GemmPh& g, const Epi& e, const 
     for (int s = 0; s < kPF; ++s) VSK_RING_LOAD(s, false);
   }
   if (!await(sy, point)) return false;
-  if (!has) return true;
   if constexpr (XN) {
-    stage_norm(ni.x, ni.gain, ni.ssq, ni.parts, e.R, g.Kt * 32, eps, lds);
-    __syncthreads();
-  } else {
-#pragma unroll
-    for (int s = 0; s < kPF; ++s) {
-      xr[s] = Xg[static_cast<size_t>(kWaves * xi) * 64];
-      if (++xi == S) xi = 0;
-    }
+    norm_slice(ni, e.R, g.Kt * 32, eps, reinterpret_cast<uint16_t*>(const_cast<u32x4*>(g.Xf)), lds);
+    arrive(sy, point + 1);
+    if (!await(sy, point + 1)) return false;
   }
-  const u32x4* xl = reinterpret_cast<const u32x4*>(lds) + static_cast<size_t>(w) * S * 64 + lane;
-  f32x4* red = reinterpret_cast<f32x4*>(lds + (XN ? static_cast<size_t>(S) * kWaves * 1024 : 0));
+  if (!has) return true;
+#pragma unroll
+  for (int s = 0; s < kPF; ++s) {
+    xr[s] = Xg[static_cast<size_t>(kWaves * xi) * 64];
+    if (++xi == S) xi = 0;
+  }
+  f32x4* red = reinterpret_cast<f32x4*>(lds);
   const int J = (g.u_hi - g.u_lo) * S;  // positions of this wave
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f}, done = acc;
   int cu = g.u_lo, ci = 0, pend = -1;
@@ -416,13 +420,7 @@ __device__ __forceinline__ bool gemm_phase(const GemmPh& g, const Epi& e, const 
 
   // consume the position in slot s: one MFMA; at the end of a unit the
   // wave's sum goes to LDS (wave 0 keeps its own)
-#define VSK_CONSUME(s)                                                        \
-  do {                                                                        \
-    u32x4 xv_;                                                                \
-    if constexpr (XN) xv_ = xl[static_cast<size_t>(ci) * 64];                 \
-    else xv_ = xr[s];                                                         \
-    acc = mfma_16x16x32(wr[s], xv_, acc);                                     \
-  } while (0)
+#define VSK_CONSUME(s) acc = mfma_16x16x32(wr[s], xr[s], acc)
 #define VSK_UNIT_END()                                                        \
   do {                                                                        \
     if (++ci == S) {                                                          \
@@ -452,7 +450,7 @@ __device__ __forceinline__ bool gemm_phase(const GemmPh& g, const Epi& e, const 
 #pragma unroll
     for (int s = 0; s < kPF; ++s) {
       VSK_CONSUME(s);
-      VSK_RING_LOAD(s, !XN);
+      VSK_RING_LOAD(s, true);
       VSK_UNIT_END();
       // keep each refill next to its use
       __builtin_amdgcn_sched_barrier(0);
@@ -563,6 +561,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
   const int parts = H / 16;
   auto xbuf = [&](int b) { return a.xs + static_cast<size_t>(b) * R * H; };
   auto sbuf = [&](int b) { return a.ssq + static_cast<size_t>(b) * parts * R; };
+  auto nbuf = [&](int b) { return a.ns + static_cast<size_t>(b) * kStepMaxRows * H; };
   auto layer = [&](int l) { return a.P + a.layer_bytes * l; };
   auto gemm = [&](const uint8_t* W, int Kt, int N, const uint16_t* Xf) {
     GemmPh g{reinterpret_cast<const u32x4*>(W), Kt, 0, 0, reinterpret_cast<const u32x4*>(Xf)};
@@ -591,11 +590,12 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
     e.N = a.Nq + 2 * a.Nkv;
     e.q = a.qs + static_cast<size_t>(l) * R * a.Nq;
     e.layer = l;
-    if (!gemm_phase<EPI_QKV, true>(gemm(Lw + a.lo.wqkv, H / 32, e.N, nullptr), e,
+    if (!gemm_phase<EPI_QKV, true>(gemm(Lw + a.lo.wqkv, H / 32, e.N, nbuf(2 * l)), e,
                                    NormIn{xbuf(2 * l), reinterpret_cast<const uint16_t*>(Lw + a.lo.attn_norm),
                                           sbuf(2 * l), l == 0 ? 1 : parts},
-                                   a.eps, lds, sy, point++))
+                                   a.eps, lds, sy, point))
       return;
+    point += 2;
     // ---- attention
     arrive(sy, point);
     if (!await(sy, point++)) return;
@@ -643,11 +643,12 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
     // ---- gate/up + SwiGLU
     e.N = 2 * a.F;
     e.a_out = a.as + static_cast<size_t>(l) * 16 * a.F;
-    if (!gemm_phase<EPI_SWIGLU, true>(gemm(Lw + a.lo.wgu, H / 32, 2 * a.F, nullptr), e,
+    if (!gemm_phase<EPI_SWIGLU, true>(gemm(Lw + a.lo.wgu, H / 32, 2 * a.F, nbuf(2 * l + 1)), e,
                                       NormIn{xbuf(2 * l + 1), reinterpret_cast<const uint16_t*>(Lw + a.lo.mlp_norm),
                                              sbuf(2 * l + 1), parts},
-                                      a.eps, lds, sy, point++))
+                                      a.eps, lds, sy, point))
       return;
+    point += 2;
     // ---- down + residual
     e.N = H;
     e.x_in = xbuf(2 * l + 1);
@@ -663,11 +664,11 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
   // arrivals, which the next pass's waits rely on (no workgroup waits at
   // these points)
   if (threadIdx.x == 0)
-    for (int pt = point; pt < 5 * a.n_layers; ++pt)
+    for (int pt = point; pt < kLayerSyncs * a.n_layers; ++pt)
       __hip_atomic_fetch_add(a.flags + (static_cast<size_t>(pt) * kSyncCounters + (blockIdx.x % kSyncCounters)) *
                                            kFlagWords,
                              1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  point = 5 * a.n_layers;
+  point = kLayerSyncs * a.n_layers;
 
   // ---- final norm + lm_head + argmax partials
   const int nb = 2 * a.n_run;
@@ -675,10 +676,11 @@ __global__ __launch_bounds__(64 * kWaves) void k_step(StepArgs a) {
   e.logits = a.logits;
   e.am_val = a.am_val;
   e.am_idx = a.am_idx;
-  if (!gemm_phase<EPI_LOGITS, true>(gemm(reinterpret_cast<const uint8_t*>(a.lm_head), H / 32, a.V, nullptr), e,
+  if (!gemm_phase<EPI_LOGITS, true>(gemm(reinterpret_cast<const uint8_t*>(a.lm_head), H / 32, a.V, nbuf(nb)), e,
                                     NormIn{xbuf(nb), a.final_gain, sbuf(nb), a.n_run == 0 ? 1 : parts}, a.eps, lds,
-                                    sy, point++))
+                                    sy, point))
     return;
+  point += 2;
   arrive(sy, point);
   if (!await(sy, point++)) return;
   argmax_phase(a, xbuf(nb), lds);
@@ -695,7 +697,7 @@ bool step_shape_ok(const vsk_model_cfg& c) {
 }
 
 size_t step_lds_bytes(const vsk_model_cfg& c) {
-  const size_t gemm = static_cast<size_t>(c.hidden / 256) * kWaves * 1024 + kLdsRed + kStepMaxRows * 8;
+  const size_t gemm = kLdsRed + kStepMaxRows * 8;
   const size_t attn = c.head_dim == 128 ? sizeof(AttnLds<128, kWaves>) : sizeof(AttnLds<64, kWaves>);
   return std::max<size_t>(std::max(gemm, attn), 256);
 }

@@ -11,9 +11,11 @@ constexpr int kSyncCounters = 8;   // arrival counters per synchronisation point
 constexpr int kFlagWords = 16;     // 64 bytes between two counters
 
 // Synchronisation points of a persistent pass over n layers: after the
-// embedding, after each of a layer's five phases (QKV, attention, O,
-// gate/up, down) and after the lm_head.
-inline int step_syncs(int n_layers) { return 5 * n_layers + 2; }
+// embedding, after each of a layer's seven phases (attention norm, QKV,
+// attention, O, MLP norm, gate/up, down), after the final norm and after
+// the lm_head.
+constexpr int kLayerSyncs = 7;
+inline int step_syncs(int n_layers) { return kLayerSyncs * n_layers + 3; }
 
 struct StepArgs {
   // model
@@ -51,6 +53,7 @@ struct StepArgs {
   uint16_t* qs;    // [L][R][Nq] rotated q
   uint16_t* os;    // [L] attention output frags (16 rows, Nq wide)
   uint16_t* as;    // [L] SwiGLU output frags (16 rows, F wide)
+  uint16_t* ns;    // [2L+1] normalised projection-input frags (16 rows, H wide), one per residual buffer
   float* am_val;   // [V/16][R] lm_head argmax partials
   int* am_idx;
   unsigned* flags;      // [syncs][kSyncCounters][kFlagWords] arrival counters
@@ -64,8 +67,8 @@ struct StepArgs {
 };
 
 // Shapes the persistent kernel covers: every projection's K a multiple of
-// 256 with at least 8 K steps per wave, hidden at most 4096 (the normalised
-// input of a projection is staged in LDS), head_dim 64 or 128.
+// 256 with at least 8 K steps per wave, hidden at most 4096 (at most 256
+// sum-of-squares partials per row), head_dim 64 or 128.
 bool step_shape_ok(const vsk_model_cfg& c);
 // LDS bytes of one persistent workgroup for this model.
 size_t step_lds_bytes(const vsk_model_cfg& c);
