@@ -142,6 +142,12 @@ def test_errors_leave_state_unchanged():
     with pytest.raises(vsk.VskError) as ex:
         e.batch_build([7], [1])
     assert ex.value.code == "STATE"
+    # an empty pass, and rows outside 1..resident length of the sequence
+    for seqs, q in (([], []), ([1], [0]), ([1], [21])):
+        with pytest.raises(vsk.VskError) as ex:
+            e.batch_build(seqs, q)
+        assert ex.value.code == "ARG", (seqs, q)
+    assert (e.seq_info(1), e.free_blocks()) == before
     e.close()
 
 
