@@ -360,10 +360,10 @@ __device__ __forceinline__ void epilogue(const Epi& e, int unit, const f32x4 v, 
 // One projection phase of this workgroup, entered right after the previous
 // phase's work: arrive at `point`, start the weight stream (the first kPF
 // tiles of each wave do not depend on the input), wait for every workgroup;
-// XN: write this workgroup's share of the normalised input frags to g.Xf,
-// arrive at `point + 1` and wait again; then run the units, the input frags
-// streaming from g.Xf beside the weights.  Returns false when a wait of
-// this pass failed.
+// XN: arrive at `point` and wait, write this workgroup's share of the
+// normalised input frags to g.Xf, arrive at `point + 1`, start the weight
+// stream and wait again; then run the units, the input frags streaming from
+// g.Xf beside the weights.  Returns false when a wait of this pass failed.
 template <int EPI, bool XN>
 __device__ __forceinline__ bool gemm_phase(const GemmPh& g, const Epi& e, const NormIn& ni, float eps, unsigned char* lds,
                            const Sync& sy, int point) {
@@ -394,15 +394,22 @@ __device__ __forceinline__ bool gemm_phase(const GemmPh& g, const Epi& e, const 
     }                                                                         \
   } while (0)
 
-  arrive(sy, point);
-  if (has) {
+  // the first weight tiles go out before the wait that precedes the input
+  // (with XN after the norm's stores: an arrival drains every outstanding
+  // load, and the ring would hold up the norm phase's arrival)
+  auto prefetch = [&]() {
+    if (has) {
 #pragma unroll
-    for (int s = 0; s < kPF; ++s) VSK_RING_LOAD(s, false);
-  }
+      for (int s = 0; s < kPF; ++s) VSK_RING_LOAD(s, false);
+    }
+  };
+  arrive(sy, point);
+  if constexpr (!XN) prefetch();
   if (!await(sy, point)) return false;
   if constexpr (XN) {
     norm_slice(ni, e.R, g.Kt * 32, eps, reinterpret_cast<uint16_t*>(const_cast<u32x4*>(g.Xf)), lds);
     arrive(sy, point + 1);
+    prefetch();
     if (!await(sy, point + 1)) return false;
   }
   if (!has) return true;
