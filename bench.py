@@ -22,6 +22,13 @@ kernel of a layer), timed live with HIP events bound to each of its launches
 (hipExtLaunchKernel: the kernel's own start and end on the pass stream); and
 ``cpu_baseline``, the float64 CPU oracle timed on a bounded sample of the
 same workload (median of 3 after a warm-up).
+
+``--workload 4`` times the 2,080-row mixed pass (four 512-row prompts
+prefilled beside 32 decoding sequences, logits for 36 rows) instead: the
+value is rows/s, and ``roofline`` is the gate/up projection's flops over its
+launch time against the dense bf16 matrix-core peak (the pass is bound by the
+matrix cores, not HBM); ``step_TFLOPs`` is the whole pass's algorithmic flops
+over the step time.
 """
 from __future__ import annotations
 
@@ -38,6 +45,7 @@ sys.path.insert(0, ROOT)
 import numpy as np  # noqa: E402
 
 PEAK_HBM = 8.0e12  # MI355X HBM3E, bytes/s
+PEAK_MFMA_BF16 = 2.5e15  # MI355X dense bf16 matrix-core rate, flop/s
 CALIB_BYTES = 512 << 20  # plain device-to-device copy used to calibrate byte counters
 
 
@@ -46,7 +54,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", type=int, default=2, help="decode workload of the value line (2, 3 or 5)")
+    ap.add_argument("--workload", type=int, default=2,
+                    help="workload of the value line: 2, 3 or 5 (decode tokens/s), 4 (mixed prefill + decode "
+                         "pass, rows/s, matrix-core roofline)")
     ap.add_argument("--no-batch64", action="store_true", help="skip the batch-64 shared-prefix line")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-layers", type=int, default=1, help="layers in the CPU oracle sample")
@@ -107,7 +117,7 @@ def step_bytes(w):
     wbytes = m.weight_bytes_streamed()
     kv_read = w.unique_resident_tokens() * m.n_layers * m.kv_bytes_per_token_layer
     kv_write = B * m.n_layers * m.kv_bytes_per_token_layer
-    logits = B * m.vocab * 2
+    logits = len(w.logit_rows()) * m.vocab * 2
     emb = B * m.hidden * 2
     return wbytes + kv_read + kv_write + logits + emb
 
@@ -115,6 +125,23 @@ def step_bytes(w):
 def gateup_bytes(m, R):
     """Algorithmic bytes of one gate/up launch: its weights, its input rows, its output."""
     return 2 * m.ffn * m.hidden * 2 + R * m.hidden * 2 + R * m.ffn * 2
+
+
+def gateup_flops(m, R):
+    """Algorithmic flops of one gate/up launch over R rows (padding rows excluded)."""
+    return 2 * R * m.hidden * 2 * m.ffn
+
+
+def step_flops(w):
+    """Algorithmic flops of one pass: every projection over every row, the
+    lm_head over the logit rows, and attention (QK and PV) over every
+    attended key (a prefill row attends its own position and those before)."""
+    m = w.model
+    Nq, Nkv = m.n_q_heads * m.head_dim, m.n_kv_heads * m.head_dim
+    per_row = 2 * m.hidden * (Nq + 2 * Nkv) + 2 * Nq * m.hidden + 2 * m.hidden * 2 * m.ffn + 2 * m.ffn * m.hidden
+    keys = sum(sum(s.ctx + j + 1 for j in range(s.q_len)) for s in w.seqs)
+    attn = 4 * Nq * keys
+    return m.n_layers * (w.n_rows * per_row + attn) + 2 * len(w.logit_rows()) * m.hidden * m.vocab
 
 
 def gemm_kernel_hash():
@@ -408,7 +435,8 @@ def cpu_info():
 def cpu_baseline(w, n_layers_sample, reps=3):
     """Time the float64 oracle on a sample: all rows of the workload through
     1 and 1 + n_layers_sample layers plus the lm_head, each the median of
-    `reps` runs after a warm-up, extrapolated per layer to the full step."""
+    `reps` runs after a warm-up, extrapolated per layer to the full step
+    (rows per second of the whole step)."""
     import copy
     from dataclasses import replace
 
@@ -446,7 +474,7 @@ def cpu_baseline(w, n_layers_sample, reps=3):
     return {"value": w.n_rows / t_step, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": (f"{w.name}: all {w.n_rows} rows through 1 and {1 + n_layers_sample} of "
                        f"{w.model.n_layers} layers + lm_head (float64 NumPy, weights and KV drawn "
-                       f"before timing), each the median of {reps} runs after a warm-up; per-layer time "
+                       f"before timing), each the median of {reps} run(s) after a warm-up; per-layer time "
                        f"extrapolated to the full step"),
             "cpu_model": cpu_info(), "blas": blas or "unknown", "s_per_step": t_step}
 
@@ -582,6 +610,7 @@ def main():
     ms = min(r["ms_eager"], r.get("ms_graph", float("inf")))
     tokps = w.n_rows / (ms / 1e3)
     sb = step_bytes(w)
+    mixed = a.workload == 4
     if r["persistent"]:
         kname = "persistent decode step (k_step: every layer's projections, attention, lm_head, argmax)"
         kb = sb
@@ -590,10 +619,25 @@ def main():
         kb = gateup_bytes(w.model, w.n_rows)
     achieved = kb / (r["kernel_ms"] / 1e3)
     traffic = (None if r["persistent"] else gateup_traffic()) if a.workload == 2 else None
+    roofline = {"bound": "hbm", "kernel": kname,
+                "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM, 4),
+                "traffic": traffic,
+                "traffic_source": ("stored rocprofv3 counters of this kernel source "
+                                   "(profiles/gateup_3b_b16_traffic.json)") if traffic is not None else None,
+                "bytes_per_launch": kb, "avg_launch_ms": round(r["kernel_ms"], 5)}
+    if mixed:
+        # the 2,080-row pass is bound by the matrix cores: gate/up's flops over its launch time
+        fl = gateup_flops(w.model, w.n_rows)
+        tf = fl / (r["kernel_ms"] / 1e3) / 1e12
+        roofline = {"bound": "mfma", "kernel": kname, "achieved": round(tf, 1), "peak": PEAK_MFMA_BF16 / 1e12,
+                    "unit": "TFLOP/s", "frac": round(tf * 1e12 / PEAK_MFMA_BF16, 4), "traffic": None,
+                    "flops_per_launch": fl, "avg_launch_ms": round(r["kernel_ms"], 5)}
     out = {
-        "metric": "decode-step latency (ms) & tokens/s at batch 16/64; achieved HBM TB/s vs peak",
+        "metric": ("mixed prefill + decode pass: rows/s; achieved matrix-core TFLOP/s vs peak" if mixed else
+                   "decode-step latency (ms) & tokens/s at batch 16/64; achieved HBM TB/s vs peak"),
         "value": round(tokps, 1),
-        "unit": "tokens/s",
+        "unit": "rows/s" if mixed else "tokens/s",
         "n_gpus": 1,
         "steps": a.steps,
         "warmup": a.warmup,
@@ -616,23 +660,22 @@ def main():
         "step_bytes": sb,
         "step_hbm_TBps": round(sb / (ms / 1e3) / 1e12, 3),
         "step_hbm_frac": round(sb / (ms / 1e3) / PEAK_HBM, 4),
-        "roofline": {"bound": "hbm", "kernel": kname,
-                     "achieved": round(achieved / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM, 4),
-                     "traffic": traffic,
-                     "traffic_source": ("stored rocprofv3 counters of this kernel source "
-                                        "(profiles/gateup_3b_b16_traffic.json)") if traffic is not None else None,
-                     "bytes_per_launch": kb, "avg_launch_ms": round(r["kernel_ms"], 5)},
+        "roofline": roofline,
         "exec_counters": r["counters"],
     }
+    if mixed:
+        sf = step_flops(w)
+        out["step_flops"] = sf
+        out["step_TFLOPs"] = round(sf / (ms / 1e3) / 1e12, 1)
+        out["step_mfma_frac"] = round(sf / (ms / 1e3) / PEAK_MFMA_BF16, 4)
     if "timeline" in r:
         out["timeline"] = r["timeline"]
     sc = stream_ceiling(torch)
     out["stream_read_ceiling"] = sc
     out["step_frac_of_stream_ceiling"] = round(sb / (ms / 1e3) / (sc["GBps"] * 1e9), 4)
-    if not a.no_loop and a.mode != 2:
+    if not a.no_loop and a.mode != 2 and not mixed:
         out["decode_loop"] = decode_loop(torch, w)
-    if not a.no_routed and a.mode != 2:
+    if not a.no_routed and a.mode != 2 and not mixed:
         rr = measure(torch, w, a.steps, a.warmup, not a.no_graph, probe=False, tune=a.tune, route=routed_tape(w))
         msr = min(rr["ms_eager"], rr.get("ms_graph", float("inf")))
         out["routed"] = {"workload": w.name, "policy": "random skip, half of the routed decisions Project-Only",
@@ -654,7 +697,10 @@ def main():
             "step_hbm_frac": round(sb3 / (ms3 / 1e3) / PEAK_HBM, 4)}
     if not a.no_cpu:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        cb = cpu_baseline(w, a.cpu_layers)
+        # the 2,080-row pass costs the oracle minutes per layer: one timed run each
+        cb = cpu_baseline(w, a.cpu_layers, reps=1 if mixed else 3)
+        if mixed:
+            cb["unit"] = "rows/s"
         cb.pop("s_per_step")
         cb["value"] = round(cb["value"], 4)
         out["cpu_baseline"] = cb
