@@ -110,3 +110,57 @@ def test_odd_shape_routed(shape, rows):
     st, *_ = e2e_compare(w, lg, ids, sub, route=tape)
     d.release()
     print(st)
+
+
+# positions up to the largest the library takes (max_pos 16384)
+LONG = ModelCfg("long-2L", n_layers=2, hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn=512, vocab=512,
+                rope_theta=500000.0, max_pos=16384)
+
+
+@pytest.mark.parametrize("bps", [0, 8, 512])
+def test_long_contexts(bps):
+    """Decode rows at positions up to 16,383 (the last rotary position),
+    with the default split, 8-block splits (up to 128 split partials per
+    row and KV head, merged in order) and 512-block splits."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    ctx = np.array([16383, 12000, 9001, 5000, 1, 8192])
+    w = decode_workload(LONG, ctx, seed=41, name=f"long-bps{bps}")
+    print(f"[gpu] {w.name} bps={bps}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(0, bps)
+    d.step()
+    lg, ids = d.results()
+    st, *_ = e2e_compare(w, lg, ids)
+    assert_kv_layer_local(d, w)
+    d.release()
+    print(st)
+
+
+@pytest.mark.parametrize("prefill_kernel", [1, 0])
+def test_long_context_prefill_chunk(prefill_kernel):
+    """Prefill chunks continuing long cached sequences: 40 rows after 9,000
+    tokens (past the 8,192 positions a causal prefill work item stages, so
+    the pass takes one decode work item per row) and 30 rows after 3,000,
+    beside two decode rows."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    from workloads.configs import SeqSpec, Workload
+    rng = np.random.default_rng(43)
+    specs = [(9000, 40), (3000, 30), (12000, 1), (700, 1)]
+    n_pool = sum((c + q + 15) // 16 for c, q in specs) + 8
+    perm = [int(b) for b in rng.permutation(n_pool)]
+    seqs, pos = [], 0
+    for i, (ctx, q) in enumerate(specs):
+        nb = (ctx + 15) // 16
+        seqs.append(SeqSpec(ctx, q, perm[pos:pos + nb], [(0, ctx, i)]))
+        pos += nb
+    tokens = rng.integers(0, LONG.vocab, size=sum(q for _, q in specs)).astype(np.int32)
+    w = Workload(0, f"long-chunk-{prefill_kernel}", LONG, seqs, n_pool, tokens, 7)
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(6, prefill_kernel)
+    d.step()
+    lg, ids = d.results()
+    st, *_ = e2e_compare(w, lg, ids)
+    assert_kv_layer_local(d, w)
+    d.release()
+    print(st)
