@@ -113,3 +113,57 @@ def test_greedy_generation_matches_oracle(model):
             assert d.eng.exec_counters()[5] == 1, "the persistent kernel did not run"
     assert new_blocks >= B - 1, new_blocks  # all sequences but one took a new block
     d.release()
+
+
+def test_prefill_then_generate():
+    """Three fresh prompts of 37 tokens prefilled in one chunk (the causal
+    multi-row kernel; logits of each prompt's last row), then 12 decode
+    passes generating from the prefill's greedy ids, against the oracle
+    following the same path."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    from workloads.configs import mixed_workload
+    m = MODELS["gqa4-d128"]
+    T, plen = 12, 37
+    w = mixed_workload(m, n_pre=3, plen=plen, ctx=np.zeros(0, np.int64), seed=23, name="gen-prefill")
+    B = w.n_seqs
+    print(f"[gpu] {w.name} rows={w.n_rows} then {T} decode passes", flush=True)
+    d = DeviceRun(w, max_kv_len=plen + T + 1, poison_pool=True)
+    sp = d.sp
+    seqs, ones = list(range(B)), [1] * B
+    meta_t = torch.empty(4 * d.meta_bytes + 4096, dtype=torch.uint8, device=d.device)
+    meta = meta_t.data_ptr() + ((-meta_t.data_ptr()) % 256)
+    a, kv = _oracle_store(w)
+    kv32 = _oracle_store(w)[1]
+    W = GeneratedWeights(m, w.seed)
+    # the prefill pass
+    d.step()
+    lg, nxt = d.results()
+    batch = build_batch(a, seqs, [s.q_len for s in w.seqs])
+    sub, rows = select_seqs(batch, seqs)
+    last = np.asarray(sub["cu_q"][1:]) - 1
+    out = forward(m, W, kv, sub, w.tokens[rows], last)
+    out32 = forward(m, W, kv32, sub, w.tokens[rows], last, dtype="f32")
+    st = compare_logits(lg, nxt, out["z"], z32=out32["z"])
+    print(f"[gen] prefill: {st}", flush=True)
+    ids = [torch.from_numpy(nxt.astype(np.int32)).to(d.device), torch.empty(B, dtype=torch.int32, device=d.device)]
+    logits = torch.empty((B, m.vocab), dtype=torch.int16, device=d.device)
+    for t in range(T):
+        for q in seqs:
+            d.eng.reserve(q, 1)
+            a.reserve(q, 1)
+        d.eng.batch_build(seqs, ones)
+        d.eng.batch_upload(meta, meta_t.numel() - 256, sp)
+        d.eng.decode_step(ids[t % 2].data_ptr(), logits.data_ptr(), ids[(t + 1) % 2].data_ptr(), d.ws, d.ws_bytes,
+                          sp)
+        torch.cuda.synchronize()
+        lg = logits.view(torch.bfloat16).float().cpu().numpy().astype(np.float64)
+        tok_in = ids[t % 2].cpu().numpy()
+        nxt = ids[(t + 1) % 2].cpu().numpy()
+        batch = build_batch(a, seqs, ones)
+        np.testing.assert_array_equal(d.eng.batch_host()["slot"], batch["slot"])
+        sub, rows = select_seqs(batch, seqs)
+        out = forward(m, W, kv, sub, tok_in[rows], np.arange(B))
+        out32 = forward(m, W, kv32, sub, tok_in[rows], np.arange(B), dtype="f32")
+        st = compare_logits(lg, nxt, out["z"], z32=out32["z"])
+        print(f"[gen] pass {t}: {st}", flush=True)
+    d.release()
