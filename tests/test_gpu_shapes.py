@@ -164,3 +164,19 @@ def test_long_context_prefill_chunk(prefill_kernel):
     assert_kv_layer_local(d, w)
     d.release()
     print(st)
+
+
+def test_large_prefill_chunk():
+    """A 4,100-row pass: four 1,024-token prompts prefilled in one chunk
+    (33 row tiles of 128, causal items of 128 / G rows) beside four decode
+    rows; logits of the 8 last rows against the oracle, K,V of a subset of
+    the sequences layer-local."""
+    m = SHAPES["h256-g5-d128"]
+    ctx = np.array([5, 300, 1000, 77])
+    w = mixed_workload(m, n_pre=4, plen=1024, ctx=ctx, seed=31, name="large-prefill")
+    assert w.n_rows == 4100
+    d, lg, ids = _run(w)
+    st, *_ = e2e_compare(w, lg, ids)
+    assert_kv_layer_local(d, w, seq_subset=[0, 3, 5])
+    d.release()
+    print(st)
