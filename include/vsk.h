@@ -406,7 +406,10 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        at 65..128, 192 for the down projection at 1..16 rows (two tiles
  *        per workgroup), no split otherwise (O at 1..32 rows, down at
  *        17..32: measured no faster); -1: no split.  Split products are added to the residual in
- *        split order by the RMSNorm that follows.
+ *        split order by the RMSNorm that follows.  Passes of more than 128
+ *        rows whose residual projections have at most 128 workgroups (N
+ *        groups x row tiles) split K into as many splits as keep them within
+ *        256, unless the key is -1.
  * key 6: rows of a sequence with several new rows (a prefill chunk): 1 (the
  *        default) one causal work item per run of up to 128 (row, query
  *        head) pairs reading each key block once for all of them; 0 one
@@ -415,7 +418,10 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        its K split aims for (1..4096); 0 (the default): 192; -1: no split
  *        (two 16-column tiles per workgroup with the epilogue in the
  *        projection).  Split products are added in split order by a kernel
- *        that then applies rotary and writes q and the KV slots.
+ *        that then applies rotary and writes q and the KV slots.  Passes of
+ *        more than 128 rows split QKV the same way when the residual
+ *        layout would give it at most 128 workgroups (within 256 after the
+ *        split), unless the key is -1.
  * key 8: projections of a row-tiled pass (more than 128 rows): 1 (the
  *        default) orders the workgroups so that the row tiles of one weight
  *        slice run together on one XCD and share its L2; 0 keeps the

@@ -84,9 +84,10 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   w.ssq = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
   w.ssq_c = o; o = align_up(o + (H / 16) * static_cast<size_t>(max_rows) * 8);
   // residual projections with K split over workgroups: one product per split
-  // (and the QKV projection's, N = Nq + 2 Nkv)
+  // and row (and the QKV projection's, N = Nq + 2 Nkv); row-tiled passes with
+  // few workgroups split too
   const size_t y_cols = std::max<size_t>(H, static_cast<size_t>(Nq) + 2 * static_cast<size_t>(c.n_kv_heads) * c.head_dim);
-  w.ypart = o; o = align_up(o + static_cast<size_t>(kMaxResidSplits) * std::min(max_rows, 128) * y_cols * 4);
+  w.ypart = o; o = align_up(o + static_cast<size_t>(kMaxResidSplits) * max_rows * y_cols * 4);
   // lm_head argmax partials: n_groups x rows
   const size_t lm_groups = static_cast<size_t>(ceil_div(c.vocab, 16));  // upper bound over plans
   w.am_part = o; o = align_up(o + lm_groups * max_rows * 8);
@@ -95,7 +96,7 @@ WsLayout ws_layout(const vsk_model_cfg& c, int32_t max_rows, int32_t max_seqs, i
   w.routed = routed;
   if (routed) {
     const size_t L = c.n_layers, R = max_rows;
-    const size_t yrows = std::max<size_t>(static_cast<size_t>(kMaxResidSplits) * std::min(max_rows, 128), R);
+    const size_t yrows = static_cast<size_t>(kMaxResidSplits) * R;  // a product per K split of every row
     w.fb_po = o; o = align_up(o + Rp * H * 2);
     w.fc_po = o; o = align_up(o + Rp * F * 2);
     w.y_run = o; o = align_up(o + yrows * H * 4);
@@ -1087,7 +1088,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   // each activation chunk staged in LDS feeds two or four times the weight
   // bytes), the products added by k_qkv_reduce, which applies the epilogue
   GemmPlan p_qkv_split;
-  if (h.qkv_target >= 0 && p_qkv.mg >= 4 && p_qkv.m_tiles == 1)
+  if (h.qkv_target >= 0 && p_qkv.mg >= 4)
     p_qkv_split = plan_gemm(Nq + 2 * Nkv, H, R, EPI_RESID, h.gemm_shape, h.qkv_target > 0 ? h.qkv_target : kQkvTargetWgs);
   const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape, rt);
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape);

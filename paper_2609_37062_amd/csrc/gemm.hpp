@@ -43,6 +43,8 @@ struct GemmPlan {
 constexpr int kMaxResidSplits = 8;
 constexpr int kResidTargetWgs = 0;  // default split-K target of the residual projections (0: no split)
 constexpr int kQkvTargetWgs = 192;  // default split-K target of QKV at 4..8 row groups
+constexpr int kRowTiledSplitBelow = 128;  // row-tiled residual projections split K at or below these workgroups
+constexpr int kRowTiledTarget = 256;      // into as many splits as stay within this many workgroups
 
 // shape: launch shape for 4 or 8 row groups (0 default; see k_gemm.hip)
 // resid_target: workgroups a residual projection's K split aims for (-1: no

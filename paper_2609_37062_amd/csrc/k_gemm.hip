@@ -673,9 +673,17 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
                      : p.xl                      ? (p.mg == 4 ? 192 : 384)
                      : p.mg == 1 && p.nt == 2    ? 192
                                                  : kResidTargetWgs;
-  if (epi == EPI_RESID && target > 0 && p.m_tiles == 1) {
+  // A row-tiled pass with few workgroups (n_groups x m_tiles at most
+  // kRowTiledSplitBelow: 129 to about a thousand rows at hidden 4096, where
+  // 16 N groups per row tile left 32-128 workgroups streaming the weights)
+  // splits K too, into as many splits as keep the workgroups within
+  // kRowTiledTarget (one per compute unit: a launch of one round).
+  const int tiles = p.n_groups * p.m_tiles;
+  const bool row_tiled_split = p.m_tiles > 1 && tiles <= kRowTiledSplitBelow;
+  if (epi == EPI_RESID && target > 0 && (p.m_tiles == 1 || row_tiled_split)) {
     const int Kt = K / 32;
-    int ks = std::min({(target + p.n_groups - 1) / p.n_groups, kMaxResidSplits, std::max(1, Kt / (4 * wk))});
+    const int want = p.m_tiles == 1 ? (target + tiles - 1) / tiles : kRowTiledTarget / tiles;
+    int ks = std::min({want, kMaxResidSplits, std::max(1, Kt / (4 * wk))});
     ks = std::max(ks, 1);
     const int kc = (Kt + ks - 1) / ks;  // equal splits
     p.ksplit = (Kt + kc - 1) / kc;
