@@ -379,14 +379,14 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        16 rows) whose every projection K is a multiple of 256 and at least
  *        2048, with hidden at most 4096, and returns VSK_E_UNSUPPORTED for
  *        other passes.  Both paths compute the same values.
- * key 3: launch shape of the per-operation projections for 33..128 rows
+ * key 3: launch shape of the per-operation projections for 17..128 rows
  *        (and longer row-tiled passes).  0 (default): with one row tile the
  *        activation chunks are staged in LDS by a ninth wave and shared by
  *        eight weight-streaming waves for QKV (K split over workgroups in
  *        the residual projections' staging, key 7; unsplit, two 16-column
  *        tiles per workgroup), gate/up (four; eight, two per wave, for 65
  *        rows or more) and lm_head (sixteen, two per wave, no K split in
- *        the workgroup), residual projections taking the four-tile (33..64
+ *        the workgroup), residual projections taking the four-tile (17..64
  *        rows) or eight-tile (65..128 rows) staging with K split over
  *        workgroups (key 5); passes of more than 128 rows
  *        take the staging with the eight waves side by side (16 tiles, 8
@@ -402,10 +402,10 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        them once per sequence.
  * key 5: residual projections (O, down) of passes of at most 128 rows: the
  *        workgroup count their K split aims for (1..4096); 0 (the default):
- *        192 workgroups in the activation-staged layout at 33..64 rows, 384
+ *        192 workgroups in the activation-staged layout at 17..64 rows, 384
  *        at 65..128, 192 for the down projection at 1..16 rows (two tiles
- *        per workgroup), no split otherwise (O at 1..32 rows, down at
- *        17..32: measured no faster); -1: no split.  Split products are added to the residual in
+ *        per workgroup), no split for O at 1..16 rows (measured no faster);
+ *        -1: no split.  Split products are added to the residual in
  *        split order by the RMSNorm that follows.  Passes of more than 128
  *        rows whose residual projections have at most 128 workgroups (N
  *        groups x row tiles) split K into as many splits as keep them within
@@ -414,7 +414,7 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        default) one causal work item per run of up to 128 (row, query
  *        head) pairs reading each key block once for all of them; 0 one
  *        work item per row, as for decode rows.
- * key 7: the QKV projection of passes of 33..128 rows: the workgroup count
+ * key 7: the QKV projection of passes of 17..128 rows: the workgroup count
  *        its K split aims for (1..4096); 0 (the default): 192; -1: no split
  *        (two 16-column tiles per workgroup with the epilogue in the
  *        projection).  Split products are added in split order by a kernel

@@ -538,7 +538,8 @@ static hipError_t launch_cfg(const GemmArgs& a_in, int m_tiles, int ksplit, hipS
 //          flight (residual projections: N = hidden);
 //  pair    two N tiles per wave, 4 K steps in flight (QKV, gate/up);
 //  wide    four N tiles per wave (lm_head).
-// For 4..8 row groups the default (shape 0) is, with one row tile: X staged
+// For 2..8 row groups (2 takes the 4-row-group layouts) the default
+// (shape 0) is, with one row tile: X staged
 // in LDS by a ninth wave for gate/up (four N tiles; at 8 row groups eight,
 // two per wave) and lm_head (sixteen, two per wave, the eight waves side by
 // side), for the residual projections and QKV the four-tile (4 row groups)
@@ -558,7 +559,6 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       if (p.nt == 4) return launch_cfg<1, 4, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       if (p.nt == 2) return launch_cfg<1, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       return launch_cfg<1, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
-    case 2: return launch_cfg<2, 1, 1, 8, 8, EPI>(a, p.m_tiles, p.ksplit, s, ev);
     case 4:
       if (p.xl) {
         // weight rings of 4 and 2 K steps: shallower rings measured faster
@@ -593,7 +593,10 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
 GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   GemmPlan p;
   const int Rg = (R + 15) / 16;
-  p.mg = Rg <= 1 ? 1 : Rg <= 2 ? 2 : Rg <= 4 ? 4 : 8;
+  // 17..32 rows take the 4-row-group layouts (the padding groups re-read the
+  // last one): against one column of K-split waves over 2 row groups the 8B
+  // step at 24 and 32 rows went from 5.15 / 5.24 to 4.58 / 4.67 ms
+  p.mg = Rg <= 1 ? 1 : Rg <= 4 ? 4 : 8;
   p.m_tiles = (Rg + p.mg - 1) / p.mg;
   p.nt = 1;
   p.wn = 1;
