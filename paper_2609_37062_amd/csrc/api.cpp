@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <mutex>
@@ -1016,34 +1017,44 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   aa.row_seq = b.row_seq;
   aa.pos = b.pos;
   aa.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(d)));
+  // shared prefixes of a decode pass: read once per group by k_attn_prefix
+  const bool cascade = h.shared_prefix != 0 && b.n_pfx_items > 0 && pa.logit_rows == nullptr;
+  // the blocks each row of the decode kernel walks (after its shared prefix)
+  int blk_min = INT_MAX, blk_max = 0, n_dec = 0;
+  {
+    const BatchHost& bh = h.bh;
+    auto row_blocks = [&](int r) {
+      const int nb = (bh.pos[r] + 1 + kBlock - 1) / kBlock - (cascade ? bh.pfx_blocks[r] : 0);
+      blk_min = std::min(blk_min, nb);
+      blk_max = std::max(blk_max, nb);
+      ++n_dec;
+    };
+    if (h.prefill_attn != 0 && b.n_pre_items > 0 && b.max_kv_len <= kMaxPrefillBlocks * kBlock) {
+      for (int32_t r : bh.dec_rows) row_blocks(r);
+    } else {
+      for (int r = 0; r < R; ++r) row_blocks(r);
+    }
+  }
   aa.bps = h.attn_bps > 0 ? h.attn_bps : attn_auto_bps(R, c.n_kv_heads);
+  // 128..255 (row, KV head) pairs whose walks are within 20% of each other:
+  // one split per pair (no merge, and the items are balanced already); a
+  // wider spread keeps the split, the longest walk setting the time, and
+  // fewer pairs keep it for the parallelism
+  const int pairs = n_dec * c.n_kv_heads;
+  if (h.attn_bps == 0 && pairs >= 128 && pairs < 256 && 5 * blk_min >= 4 * blk_max)
+    aa.bps = std::clamp((blk_max + 7) / 8 * 8, kAttnMinBps, kAttnMaxBps);
   aa.max_splits = attn_splits(b.max_kv_len, aa.bps);
   aa.part_o = reinterpret_cast<float*>(ws + wl.att_o);
   aa.part_ml = reinterpret_cast<float2*>(ws + wl.att_ml);
   aa.counter = reinterpret_cast<int*>(ws + wl.att_cnt);
   aa.out = fa;
   aa.out_Rg = Rg;
-  // shared prefixes of a decode pass: read once per group by k_attn_prefix
-  const bool cascade = h.shared_prefix != 0 && b.n_pfx_items > 0 && pa.logit_rows == nullptr;
   aa.split_stride = aa.max_splits + (cascade ? b.max_pfx_splits : 0);
   aa.pfx_blocks = cascade ? b.pfx_blocks : nullptr;
   aa.pfx_splits = cascade ? b.pfx_splits : nullptr;
   // decode work items launched per (row, KV head): the most splits any
   // decode row has after its shared prefix (the rest would exit at once)
-  int dec_splits = 1;
-  {
-    const BatchHost& bh = h.bh;
-    auto row_splits = [&](int r) {
-      const int nb = (bh.pos[r] + 1 + kBlock - 1) / kBlock;
-      const int P = cascade ? bh.pfx_blocks[r] : 0;
-      dec_splits = std::max(dec_splits, (nb - P + aa.bps - 1) / aa.bps);
-    };
-    if (h.prefill_attn != 0 && b.n_pre_items > 0 && b.max_kv_len <= kMaxPrefillBlocks * kBlock) {
-      for (int32_t r : bh.dec_rows) row_splits(r);
-    } else {
-      for (int r = 0; r < R; ++r) row_splits(r);
-    }
-  }
+  const int dec_splits = std::max(1, (blk_max + aa.bps - 1) / aa.bps);
   const int pfx_fold = cascade ? b.max_pfx_splits : 0;
   AttnPrefixArgs ap{};
   ap.q = q;
