@@ -428,7 +428,11 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  *        dispatch order.
  * key 9: the workgroup count the shared-prefix work items of a decode pass
  *        aim for when a group's prefix is split (1..4096, default 192); it
- *        applies to batches built after the call (vsk_batch_build). */
+ *        applies to batches built after the call (vsk_batch_build).
+ * key 10: 16-row groups per tile of the gate/up and QKV projections of a
+ *        row-tiled pass.  0 (the default): 11 where the launch then runs in
+ *        fewer rounds x tile height (one workgroup per compute unit, 256 per
+ *        round), else 8; 8 or 11 force that height. */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

@@ -798,6 +798,10 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       if (value < 0 || value > 1) return fail(h, VSK_E_ARG, "XCD remap switch must be 0 or 1");
       h->xcd_remap = value;
       return VSK_OK;
+    case 10:
+      if (value != 0 && value != 8 && value != 11) return fail(h, VSK_E_ARG, "row tile must be 0 (auto), 8 or 11");
+      h->row_tile = value;
+      return VSK_OK;
     case 7:
       if (value < -1 || value > 4096)
         return fail(h, VSK_E_ARG, "QKV split target must be -1 (no split), 0 (default) or 1..4096");
@@ -1093,7 +1097,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   pf.out_Rg = Rg;
 
   const int rt = h.resid_target;  // -1 no split, 0 the layout's default, else the target
-  const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape);
+  const GemmPlan p_qkv = plan_gemm(Nq + 2 * Nkv, H, R, EPI_QKV, h.gemm_shape, 0, h.row_tile);
   // QKV of one row tile at 4 or 8 row groups: K split over workgroups of
   // the residual projections' layout (4 or 8 N tiles each instead of 2, so
   // each activation chunk staged in LDS feeds two or four times the weight
@@ -1102,7 +1106,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   if (h.qkv_target >= 0 && p_qkv.mg >= 4)
     p_qkv_split = plan_gemm(Nq + 2 * Nkv, H, R, EPI_RESID, h.gemm_shape, h.qkv_target > 0 ? h.qkv_target : kQkvTargetWgs);
   const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape, rt);
-  const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape);
+  const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape, 0, h.row_tile);
   const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape, rt);
   float* ypart = reinterpret_cast<float*>(ws + wl.ypart);
 
@@ -1123,7 +1127,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   if (routed_pass) TRY(launch_route_maps(pa.tape_run, c.n_layers - first_routed, R, r_run, r_proj, r_inv, r_cnt, s));
   GemmPlan p_pgu, p_pd;
   if (routed_pass) {
-    p_pgu = plan_gemm(2 * Fp, H, R, EPI_SWIGLU, h.gemm_shape);
+    p_pgu = plan_gemm(2 * Fp, H, R, EPI_SWIGLU, h.gemm_shape, 0, h.row_tile);
     p_pd = plan_gemm(H, Fp, R, EPI_RESID, h.gemm_shape, rt);
   }
   CohortOut cohort{};  // set for the MLP input of a routed layer

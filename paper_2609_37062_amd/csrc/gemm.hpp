@@ -45,13 +45,16 @@ constexpr int kResidTargetWgs = 0;  // default split-K target of the residual pr
 constexpr int kQkvTargetWgs = 192;  // default split-K target of QKV at 4..8 row groups
 constexpr int kRowTiledSplitBelow = 128;  // row-tiled residual projections split K at or below these workgroups
 constexpr int kRowTiledTarget = 256;      // into as many splits as stay within this many workgroups
+constexpr int kComputeUnits = 256;        // MI355X: 8 XCDs x 32 compute units
 
 // shape: launch shape for 4 or 8 row groups (0 default; see k_gemm.hip)
 // resid_target: workgroups a residual projection's K split aims for (-1: no
 // split; 0: the layout's default -- 192 or 384 with X in LDS, 192 for the
 // two-tile layout of the down projection at <= 16 rows, else
 // kResidTargetWgs)
-GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0, int resid_target = 0);
+// row_tile: 16-row groups per tile of a row-tiled gate/up or QKV (0: chosen
+// from the launch rounds, 8 or 11: that height)
+GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0, int resid_target = 0, int row_tile = 0);
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s, LaunchEvents ev = {});
 // QKV with K split: add the `splits` products in a.ypart and apply the QKV
 // epilogue (a as for the QKV projection, with N = Nq + 2 Nkv).

@@ -316,15 +316,23 @@ __global__ __launch_bounds__(64 * (WN * WK + (XL ? 1 : 0))) void k_gemm(GemmArgs
           const int it = c * SPW + i;
           if (FULL || it < n_it) {
             const u32x4* xb = xs + (static_cast<size_t>((c % kBuf) * kCK + wk + i * WK) * MG) * 64 + lane;
-            // all MG reads of the step before its MFMAs: one LDS wait per
-            // step instead of one per row group
-            u32x4 xv[MG];
+            // all reads of a batch before its MFMAs: one LDS wait per batch
+            // instead of one per row group.  Up to 8 row groups the step is
+            // one batch; taller tiles read theirs four at a time (at 11 row
+            // groups with two N tiles per wave, two batches spill)
+            constexpr int XB = MG > 8 ? 4 : MG;
 #pragma unroll
-            for (int g = 0; g < MG; ++g) xv[g] = xb[g * 64];
+            for (int gb = 0; gb < MG; gb += XB) {
+              u32x4 xv[XB];
 #pragma unroll
-            for (int j = 0; j < NT; ++j)
+              for (int g = 0; g < XB; ++g)
+                if (gb + g < MG) xv[g] = xb[(gb + g) * 64];
 #pragma unroll
-              for (int g = 0; g < MG; ++g) acc[j][g] = mfma_16x16x32(fa[st0 + i][j], xv[g], acc[j][g]);
+              for (int j = 0; j < NT; ++j)
+#pragma unroll
+                for (int g = 0; g < XB; ++g)
+                  if (gb + g < MG) acc[j][gb + g] = mfma_16x16x32(fa[st0 + i][j], xv[g], acc[j][gb + g]);
+            }
             wload(fa[st0 + i], it + PF);
           }
           __builtin_amdgcn_sched_barrier(0);
@@ -571,6 +579,14 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
+    case 11:
+      // 11 row groups per tile: row-tiled gate/up and QKV whose launch
+      // rounds that height fills better (see plan_gemm); staged X, the
+      // eight waves side by side (QKV with two N tiles per wave spills
+      // 147 registers in its rotary epilogue at this height)
+      if constexpr (EPI == EPI_QKV) return launch_cfg<11, 1, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+      else if constexpr (EPI == EPI_SWIGLU) return launch_cfg<11, 2, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+      else return hipErrorInvalidValue;
     default:
       if (p.xl) {
         // (QKV takes one N tile per wave: see plan_gemm)
@@ -590,7 +606,7 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
   }
 }
 
-GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
+GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target, int row_tile) {
   GemmPlan p;
   const int Rg = (R + 15) / 16;
   // 17..32 rows take the 4-row-group layouts (the padding groups re-read the
@@ -666,6 +682,22 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target) {
   }
   const int cols_per_group = 16 * p.nt * p.wn;
   p.n_groups = (N / 16 * 16 + cols_per_group - 1) / cols_per_group;
+  // Tile height of a row-tiled gate/up or QKV.  One staged workgroup fills
+  // a compute unit (LDS), so a launch runs in rounds of kComputeUnits
+  // workgroups and a partly filled last round costs a whole one; a tile of
+  // mg row groups costs about mg.  11 row groups replace 8 where rounds x mg
+  // comes out lower: at 2,080 rows (130 groups) 12 tiles instead of 17, the
+  // gate/up launch 3 rounds instead of 5 (33 against 40), QKV 2 instead of 3.
+  if (p.xl && p.wn == 8 && p.m_tiles > 1 && (epi == EPI_SWIGLU || epi == EPI_QKV) && row_tile != 8) {
+    auto cost = [&](int mg) {
+      const int t = (Rg + mg - 1) / mg;
+      return (t * p.n_groups + kComputeUnits - 1) / kComputeUnits * mg;
+    };
+    if (row_tile == 11 || cost(11) < cost(8)) {
+      p.mg = 11;
+      p.m_tiles = (Rg + 10) / 11;
+    }
+  }
   // a residual projection of one row tile splits K until the workgroups
   // reach resid_target, keeping at least 4 K steps per wave; k_resid_norm
   // then adds the splits' products into the residual.  With X in LDS the

@@ -162,6 +162,38 @@ def test_mid_qkv_k_splits(cfg, B, target):
     print(st)
 
 
+@pytest.mark.parametrize("cfg,B,row_tile", [("mid", 130, 11), ("mid", 200, 11), ("mid", 300, 11), ("mid", 300, 8),
+                                            ("wide", 200, 11)])
+def test_row_tile_heights(cfg, B, row_tile):
+    """Gate/up and QKV of a row-tiled pass with 11 row groups per tile
+    (tuning key 10): one padded tile (130 rows: 9 groups), a tile of 2
+    groups after a full one (200 rows), 11 + 8 groups (300 rows), and the
+    8-group tiles at 300 rows for comparison.  MID: logits end to end and a
+    replay bit-exact; WIDE: the layer-local checks of the full-size tests
+    (each layer's new K,V within one bf16 ulp, the residual, the 2e-2 head
+    bar)."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    model = MID if cfg == "mid" else WIDE
+    ctx = np.random.default_rng(400 + B).integers(0, 400, size=B)
+    w = decode_workload(model, ctx, seed=23, name=f"{cfg}-rowtile-b{B}-m{row_tile}")
+    print(f"[gpu] {w.name}", flush=True)
+    subset = list(range(0, B, max(1, B // 12)))
+    if cfg == "wide":
+        from test_gpu_fullsize import _check as layer_local_check
+        st = layer_local_check(w, subset, tuning=[(10, row_tile)])
+        assert st["head"]["max_err"] <= 2e-2
+        return
+    d = DeviceRun(w, poison_pool=True)
+    d.eng.set_tuning(10, row_tile)
+    d.step()
+    lg, ids = d.results()
+    d.step()
+    lg2, ids2 = d.results()
+    assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
+    st, *_ = _check(w, lg, ids, subset)
+    print(st)
+
+
 def test_mid_shared_prefix():
     ctx = 256 + np.random.default_rng(5).integers(3, 40, size=12)
     w = decode_workload(MID, ctx, seed=4, shared=256, name="mid-shared")
