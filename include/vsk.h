@@ -429,10 +429,12 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  * key 9: the workgroup count the shared-prefix work items of a decode pass
  *        aim for when a group's prefix is split (1..4096, default 192); it
  *        applies to batches built after the call (vsk_batch_build).
- * key 10: 16-row groups per tile of the gate/up and QKV projections of a
- *        row-tiled pass.  0 (the default): 11 where the launch then runs in
- *        fewer rounds x tile height (one workgroup per compute unit, 256 per
- *        round), else 8; 8 or 11 force that height. */
+ * key 10: 16-row groups per tile of the projections of a row-tiled pass
+ *        (lm_head aside).  0 (the default): 6, 7 or 11 (residual
+ *        projections: 6 or 7) where the launch then takes fewer rounds x
+ *        tile height than at 8 (one workgroup per compute unit, 256 per
+ *        round; launches that split K keep 8), else 8; 6, 7, 8 or 11 force
+ *        that height (11 gives 8 for the residual projections). */
 int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value);
 
 /* Inspection: copy the fp32 residual stream x [n_rows][hidden] left in the

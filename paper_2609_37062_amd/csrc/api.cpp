@@ -799,7 +799,8 @@ int vsk_set_tuning(vsk_handle* h, int32_t key, int32_t value) {
       h->xcd_remap = value;
       return VSK_OK;
     case 10:
-      if (value != 0 && value != 8 && value != 11) return fail(h, VSK_E_ARG, "row tile must be 0 (auto), 8 or 11");
+      if (value != 0 && value != 6 && value != 7 && value != 8 && value != 11)
+        return fail(h, VSK_E_ARG, "row tile must be 0 (auto), 6, 7, 8 or 11");
       h->row_tile = value;
       return VSK_OK;
     case 7:
@@ -1105,9 +1106,9 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   GemmPlan p_qkv_split;
   if (h.qkv_target >= 0 && p_qkv.mg >= 4)
     p_qkv_split = plan_gemm(Nq + 2 * Nkv, H, R, EPI_RESID, h.gemm_shape, h.qkv_target > 0 ? h.qkv_target : kQkvTargetWgs);
-  const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape, rt);
+  const GemmPlan p_o = plan_gemm(H, Nq, R, EPI_RESID, h.gemm_shape, rt, h.row_tile);
   const GemmPlan p_gu = plan_gemm(2 * F, H, R, EPI_SWIGLU, h.gemm_shape, 0, h.row_tile);
-  const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape, rt);
+  const GemmPlan p_d = plan_gemm(H, F, R, EPI_RESID, h.gemm_shape, rt, h.row_tile);
   float* ypart = reinterpret_cast<float*>(ws + wl.ypart);
 
   // routed pass (Algorithm 1): the maps of every routed layer, built on the
@@ -1128,7 +1129,7 @@ hipError_t run_pass(Handle& h, const PassArgs& pa, hipStream_t s) {
   GemmPlan p_pgu, p_pd;
   if (routed_pass) {
     p_pgu = plan_gemm(2 * Fp, H, R, EPI_SWIGLU, h.gemm_shape, 0, h.row_tile);
-    p_pd = plan_gemm(H, Fp, R, EPI_RESID, h.gemm_shape, rt);
+    p_pd = plan_gemm(H, Fp, R, EPI_RESID, h.gemm_shape, rt, h.row_tile);
   }
   CohortOut cohort{};  // set for the MLP input of a routed layer
 

@@ -52,8 +52,8 @@ constexpr int kComputeUnits = 256;        // MI355X: 8 XCDs x 32 compute units
 // split; 0: the layout's default -- 192 or 384 with X in LDS, 192 for the
 // two-tile layout of the down projection at <= 16 rows, else
 // kResidTargetWgs)
-// row_tile: 16-row groups per tile of a row-tiled gate/up or QKV (0: chosen
-// from the launch rounds, 8 or 11: that height)
+// row_tile: 16-row groups per tile of a row-tiled projection other than the
+// lm_head (0: chosen from the launch rounds; 6, 7, 8 or 11: that height)
 GemmPlan plan_gemm(int N, int K, int R, int epi, int shape = 0, int resid_target = 0, int row_tile = 0);
 hipError_t launch_gemm(GemmArgs a, const GemmPlan& p, int epi, hipStream_t s, LaunchEvents ev = {});
 // QKV with K split: add the `splits` products in a.ypart and apply the QKV

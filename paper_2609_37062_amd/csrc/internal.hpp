@@ -171,7 +171,7 @@ struct Handle {
   int qkv_target = 0;     // QKV at 4..8 row groups: split-K workgroup target (0 default, -1 no split)
   int prefill_attn = 1;   // prefill rows through the causal multi-row kernel (0: one row per work item)
   int xcd_remap = 1;      // row-tiled projections: XCD-aware workgroup order (0: dispatch order)
-  int row_tile = 0;       // row-tiled gate/up and QKV: 16-row groups per tile (0 auto, 8 or 11)
+  int row_tile = 0;       // row-tiled projections: 16-row groups per tile (0 auto; 6, 7, 8 or 11)
   int step_wgs = -1;   // workgroups of a persistent launch on this device (0: not runnable; -1: not queried)
   uint64_t* step_trace = nullptr;  // measurement: timestamp buffer of the persistent kernel
   size_t step_trace_cap = 0;       // its capacity in uint64

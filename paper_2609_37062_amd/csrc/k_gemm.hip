@@ -560,6 +560,18 @@ static hipError_t launch_cfg(const GemmArgs& a_in, int m_tiles, int ksplit, hipS
 // groups with QKV and 4 row groups on the 2 x 2 grid, shape 6 the default's
 // LDS layouts for every projection but the residual ones, whatever the row
 // tiling.
+// Row-tiled passes whose launch rounds another tile height fills better
+// than 8 row groups (see plan_gemm): staged X, the eight waves side by side,
+// as at 8 (QKV keeps one N tile per wave: two spill 147 registers in its
+// rotary epilogue at 11 row groups; the residual epilogue, holding the
+// residual beside the sums, spills 53 at 11 and stays at 8 or below).
+template <int MG, int EPI>
+static hipError_t launch_row_tiled(const GemmArgs& a, const GemmPlan& p, hipStream_t s, const LaunchEvents& ev) {
+  if constexpr (EPI == EPI_QKV) return launch_cfg<MG, 1, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+  else if constexpr (EPI == EPI_LOGITS || (EPI == EPI_RESID && MG > 8)) return hipErrorInvalidValue;
+  else return launch_cfg<MG, 2, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
+}
+
 template <int EPI>
 static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s, const LaunchEvents& ev) {
   switch (p.mg) {
@@ -579,14 +591,9 @@ static hipError_t launch_epi(const GemmArgs& a, const GemmPlan& p, hipStream_t s
       if (p.wn == 2) return launch_cfg<4, 2, 2, 2, 2, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       if (p.nt == 2) return launch_cfg<4, 2, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
       return launch_cfg<4, 1, 1, 8, 4, EPI>(a, p.m_tiles, p.ksplit, s, ev);
-    case 11:
-      // 11 row groups per tile: row-tiled gate/up and QKV whose launch
-      // rounds that height fills better (see plan_gemm); staged X, the
-      // eight waves side by side (QKV with two N tiles per wave spills
-      // 147 registers in its rotary epilogue at this height)
-      if constexpr (EPI == EPI_QKV) return launch_cfg<11, 1, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
-      else if constexpr (EPI == EPI_SWIGLU) return launch_cfg<11, 2, 8, 1, 4, EPI, true>(a, p.m_tiles, p.ksplit, s, ev);
-      else return hipErrorInvalidValue;
+    case 6: return launch_row_tiled<6, EPI>(a, p, s, ev);
+    case 7: return launch_row_tiled<7, EPI>(a, p, s, ev);
+    case 11: return launch_row_tiled<11, EPI>(a, p, s, ev);
     default:
       if (p.xl) {
         // (QKV takes one N tile per wave: see plan_gemm)
@@ -682,21 +689,34 @@ GemmPlan plan_gemm(int N, int K, int R, int epi, int shape, int resid_target, in
   }
   const int cols_per_group = 16 * p.nt * p.wn;
   p.n_groups = (N / 16 * 16 + cols_per_group - 1) / cols_per_group;
-  // Tile height of a row-tiled gate/up or QKV.  One staged workgroup fills
-  // a compute unit (LDS), so a launch runs in rounds of kComputeUnits
-  // workgroups and a partly filled last round costs a whole one; a tile of
-  // mg row groups costs about mg.  11 row groups replace 8 where rounds x mg
-  // comes out lower: at 2,080 rows (130 groups) 12 tiles instead of 17, the
-  // gate/up launch 3 rounds instead of 5 (33 against 40), QKV 2 instead of 3.
-  if (p.xl && p.wn == 8 && p.m_tiles > 1 && (epi == EPI_SWIGLU || epi == EPI_QKV) && row_tile != 8) {
+  // Tile height of a row-tiled projection.  One staged workgroup fills a
+  // compute unit (LDS), so a launch runs in rounds of kComputeUnits
+  // workgroups and a partly filled last round costs a whole one.  A round
+  // of mg-row-group tiles costs, relative to 8 (measured per round on the
+  // 3B and 8B projections at 768-2,080 rows): 6 groups 0.85, 7 0.94, 11
+  // 1.40 -- a shorter tile keeps its weight stream and epilogue, a taller
+  // one reads its X fragments in batches.  6, 7 or 11 row groups replace 8
+  // where rounds x that cost comes out lower, e.g. at 2,080 rows (130
+  // groups): gate/up 12 tiles of 11 (3 rounds, 4.2) instead of 17 of 8 (5
+  // rounds), QKV 12 of 11 (2 rounds, 2.8; 3 at 8), O and down 19 tiles of 7
+  // in one round (0.94).  Launches that split K (at most
+  // kRowTiledSplitBelow workgroups, below) keep 8.
+  if (p.xl && p.wn == 8 && p.m_tiles > 1 && epi != EPI_LOGITS && row_tile != 8) {
+    auto tiles_at = [&](int mg) { return (Rg + mg - 1) / mg * p.n_groups; };
     auto cost = [&](int mg) {
-      const int t = (Rg + mg - 1) / mg;
-      return (t * p.n_groups + kComputeUnits - 1) / kComputeUnits * mg;
+      const int per_round = mg == 6 ? 85 : mg == 7 ? 94 : mg == 11 ? 140 : 100;
+      return (tiles_at(mg) + kComputeUnits - 1) / kComputeUnits * per_round;
     };
-    if (row_tile == 11 || cost(11) < cost(8)) {
-      p.mg = 11;
-      p.m_tiles = (Rg + 10) / 11;
+    const int tallest = epi == EPI_RESID ? 7 : 11;  // the residual epilogue spills at 11
+    int best = 8;
+    if (row_tile != 0) {
+      best = row_tile <= tallest ? row_tile : 8;
+    } else if (tiles_at(8) > kRowTiledSplitBelow) {
+      for (const int mg : {6, 7, 11})
+        if (mg <= tallest && tiles_at(mg) > kRowTiledSplitBelow && cost(mg) < cost(best)) best = mg;
     }
+    p.mg = best;
+    p.m_tiles = (Rg + best - 1) / best;
   }
   // a residual projection of one row tile splits K until the workgroups
   // reach resid_target, keeping at least 4 K steps per wave; k_resid_norm

@@ -163,15 +163,17 @@ def test_mid_qkv_k_splits(cfg, B, target):
 
 
 @pytest.mark.parametrize("cfg,B,row_tile", [("mid", 130, 11), ("mid", 200, 11), ("mid", 300, 11), ("mid", 300, 8),
-                                            ("wide", 200, 11)])
+                                            ("mid", 300, 7), ("mid", 200, 6), ("wide", 200, 11), ("wide", 300, 7),
+                                            ("wide", 130, 6)])
 def test_row_tile_heights(cfg, B, row_tile):
-    """Gate/up and QKV of a row-tiled pass with 11 row groups per tile
-    (tuning key 10): one padded tile (130 rows: 9 groups), a tile of 2
-    groups after a full one (200 rows), 11 + 8 groups (300 rows), and the
-    8-group tiles at 300 rows for comparison.  MID: logits end to end and a
-    replay bit-exact; WIDE: the layer-local checks of the full-size tests
-    (each layer's new K,V within one bf16 ulp, the residual, the 2e-2 head
-    bar)."""
+    """Projections of a row-tiled pass at each tile height (tuning key 10;
+    11 applies to gate/up and QKV, the residual projections then keep 8):
+    one padded tile (130 rows: 9 groups in one tile of 11, two of 6), a
+    2-group tail (200 rows at 11, 13 = 6 + 6 + 1), 11 + 8 and 7 x 2 + 5
+    groups (300 rows), and the 8-group tiles at 300 rows for comparison.
+    MID: logits end to end and a replay bit-exact; WIDE: the layer-local
+    checks of the full-size tests (each layer's new K,V within one bf16 ulp,
+    the residual, the 2e-2 head bar)."""
     from paper_2609_37062_amd.runner import DeviceRun
     model = MID if cfg == "mid" else WIDE
     ctx = np.random.default_rng(400 + B).integers(0, 400, size=B)
