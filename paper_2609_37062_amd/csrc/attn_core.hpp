@@ -23,8 +23,6 @@
 #pragma once
 
 #include <cmath>
-#include <type_traits>
-#include <utility>
 
 #include "attn.hpp"
 #include "dev.hpp"
@@ -47,36 +45,6 @@ struct AttnLds {
 // agent-scope (all XCDs) coherent loads of the split partials
 __device__ __forceinline__ float ld_agent(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// The walk's K and V loads are issued from inline asm, so the compiler does
-// not track them, and the walk waits for exactly the loads a step needs
-// (s_waitcnt vmcnt(N): loads return in issue order).  When the compiler
-// tracked them it waited for every outstanding load at the top of each step
-// (vmcnt(0) at the loop header), so the next pair's V loads, issued just
-// before, were waited for in full before the scores could start.  A register
-// written by one of these loads is read only through a wait that names it
-// ("+v" on an asm statement after the s_waitcnt), so no copy of it is
-// scheduled before its data has landed.  Extra loads issued after the ones
-// waited for only make a wait longer, never too short.
-// (OFF: a byte offset in the instruction, below 4096)
-template <int OFF = 0>
-__device__ __forceinline__ void walk_load16(u32x4& r, const void* p) {
-  static_assert(OFF >= 0 && OFF < 4096, "instruction offset");
-  asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(r) : "v"(p), "n"(OFF) : "memory");
-}
-template <int OFF = 0>
-__device__ __forceinline__ void walk_load8(u32x2& r, const void* p) {
-  static_assert(OFF >= 0 && OFF < 4096, "instruction offset");
-  asm volatile("global_load_dwordx2 %0, %1, off offset:%2" : "=v"(r) : "v"(p), "n"(OFF) : "memory");
-}
-template <int N>
-__device__ __forceinline__ void walk_wait() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-template <typename T>
-__device__ __forceinline__ void walk_pin(T& r) {
-  asm volatile("" : "+v"(r));
 }
 
 // Splits of a row: n_splits(kv_len) for the row's kv_len = pos + 1.
@@ -255,19 +223,13 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   for (int i = tid; i < b_hi - b_lo; i += blockDim.x) sm.tbl[i] = table[b_lo + i];
   const int h = lane & 15;       // query head within the group (valid if h < G)
   const int quad = lane >> 4;    // token quarter / k sub-range
-  // q as the B operand of S = K q: lane holds q[h][32c + 8*quad .. +7].
-  // Loaded like the walk's K and V (a load the compiler tracked would have
-  // it wait for every outstanding load at its first use, inside the walk);
-  // columns h >= G take head G - 1's q: a column's scores, softmax and
-  // output involve that column alone, and those columns are never stored.
+  // q as the B operand of S = K q: lane holds q[h][32c + 8*quad .. +7]
   u32x4 qf[KC];
   {
-    const int hq = min(h, G - 1);
-    const u32x4* qrow = reinterpret_cast<const u32x4*>(a.q + static_cast<size_t>(row) * a.Nq +
-                                                       static_cast<size_t>(hk * G + hq) * D) + quad;
-    [&]<int... C>(std::integer_sequence<int, C...>) {
-      (walk_load16<C * 64>(qf[C], qrow), ...);
-    }(std::make_integer_sequence<int, KC>{});
+    const uint16_t* qrow = a.q + static_cast<size_t>(row) * a.Nq + static_cast<size_t>(hk * G + h) * D;
+#pragma unroll
+    for (int c = 0; c < KC; ++c)
+      qf[c] = (h < G) ? *reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * quad) : u32x4{0u, 0u, 0u, 0u};
   }
   const float sc = a.scale_log2;  // log2(e) / sqrt(D)
   float m = -INFINITY, l = 0.f;
@@ -287,45 +249,26 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
     bA = static_cast<size_t>(sm.tbl[w_lo + min(2 * p, cnt - 1)]);
     bB = static_cast<size_t>(sm.tbl[w_lo + min(2 * p + 1, cnt - 1)]);
   };
-  // (2 KC loads; see walk_load16)
   auto load_k = [&](u32x4 (&kg)[2][KC], int p, int cnt, int w_lo) {
     size_t bA, bB;
     pair_blocks(p, cnt, w_lo, bA, bB);
     const u32x4* kp = reinterpret_cast<const u32x4*>(kbase + (pair_k_block(lane) ? bB : bA) * kv_stride);
     const int k0 = pair_k_index(lane, 0), k1 = pair_k_index(lane, 1);
-    [&]<int... C>(std::integer_sequence<int, C...>) {
-      ((walk_load16<C * 1024>(kg[0][C], kp + k0), walk_load16<C * 1024>(kg[1][C], kp + k1)), ...);
-    }(std::make_integer_sequence<int, KC>{});
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      kg[0][c] = kp[c * 64 + k0];
+      kg[1][c] = kp[c * 64 + k1];
+    }
   };
-  // (2 VC loads: two 8-byte pieces per V^T operand)
-  auto load_v = [&](u32x2 (&vlo)[VC], u32x2 (&vhi)[VC], int p, int cnt, int w_lo) {
+  auto load_v = [&](u32x4 (&vt)[VC], int p, int cnt, int w_lo) {
     size_t bA, bB;
     pair_blocks(p, cnt, w_lo, bA, bB);
     const u32x2* vp =
         reinterpret_cast<const u32x2*>(vbase + (pair_v_block(lane) ? bB : bA) * kv_stride) + pair_v_index(lane);
-    [&]<int... C>(std::integer_sequence<int, C...>) {
-      ((walk_load8<C * 512>(vlo[C], vp), walk_load8<C * 512 + 128>(vhi[C], vp)), ...);
-    }(std::make_integer_sequence<int, VC>{});
-  };
-  // wait until at most N walk loads are outstanding, then release the
-  // registers (q was loaded before the first pair's K: every wait for a K
-  // covers it)
-  auto wait_k = [&](auto n_c, u32x4 (&kg)[2][KC]) {
-    walk_wait<decltype(n_c)::value>();
-#pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      walk_pin(qf[c]);
-      walk_pin(kg[0][c]);
-      walk_pin(kg[1][c]);
-    }
-  };
-  auto wait_v = [&](auto n_c, u32x2 (&vlo)[VC], u32x2 (&vhi)[VC], u32x4 (&vt)[VC]) {
-    walk_wait<decltype(n_c)::value>();
 #pragma unroll
     for (int c = 0; c < VC; ++c) {
-      walk_pin(vlo[c]);
-      walk_pin(vhi[c]);
-      vt[c] = u32x4{vlo[c][0], vlo[c][1], vhi[c][0], vhi[c][1]};
+      const u32x2 lo = vp[c * 64], hi = vp[c * 64 + 16];
+      vt[c] = u32x4{lo[0], lo[1], hi[0], hi[1]};
     }
   };
 
@@ -342,10 +285,10 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   const int t_first = kBlock * (b_lo + w_lo);                   // first key of the range
   const int t_end = min(kv_len, kBlock * (b_lo + w_lo + cnt));  // keys past it belong to others
   u32x4 kg[2][KC];
-  u32x2 vlo[VC], vhi[VC];
+  u32x4 vt[VC];
   if (cnt > 0) {
     load_k(kg, 0, cnt, w_lo);
-    load_v(vlo, vhi, 0, cnt, w_lo);
+    load_v(vt, 0, cnt, w_lo);
   }
   // the first split starts from the group's shared-prefix partials: wave w
   // folds in partials w, w + NW, ... (their loads wait behind the K/V loads
@@ -379,30 +322,21 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
         if (two) fold(op1, ml1);
     }
   }
-  // (the last pair is peeled so that the loop's loads are unconditional).
-  // Issue order per step: K(p + 1) after the scores of pair p, V(p + 1)
-  // after its P V; so pair p's K has V(p)'s 2 VC loads behind it, and V(p)
-  // has K(p + 1)'s 2 KC.
+  // (the last pair is peeled so that the loop's loads are unconditional)
   for (int p = 0; p + 1 < n_pairs; ++p) {
     const int t0 = t_first + 2 * kBlock * p;
     PTerms pp;
     float alpha;
-    wait_k(std::integral_constant<int, 2 * VC>{}, kg);
     pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, pp, alpha);
     load_k(kg, p + 1, cnt, w_lo);
-    u32x4 vt[VC];
-    wait_v(std::integral_constant<int, 2 * KC>{}, vlo, vhi, vt);
     pair_pv<D>(vt, t0, t_end, pp, alpha, o);
-    load_v(vlo, vhi, p + 1, cnt, w_lo);
+    load_v(vt, p + 1, cnt, w_lo);
   }
   if (n_pairs > 0) {
     const int t0 = t_first + 2 * kBlock * (n_pairs - 1);
     PTerms pp;
     float alpha;
-    wait_k(std::integral_constant<int, 2 * VC>{}, kg);
     pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, pp, alpha);
-    u32x4 vt[VC];
-    wait_v(std::integral_constant<int, 0>{}, vlo, vhi, vt);
     pair_pv<D>(vt, t0, t_end, pp, alpha, o);
   }
 
