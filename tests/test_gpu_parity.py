@@ -162,6 +162,27 @@ def test_mid_qkv_k_splits(cfg, B, target):
     print(st)
 
 
+@pytest.mark.parametrize("lo,hi", [(900, 1000), (300, 1000)])
+def test_mid_auto_split_balance(lo, hi):
+    """The automatic attention split at 80 rows x 2 KV heads (160 pairs, fewer
+    than the compute units): contexts within 20% of each other take one split
+    per pair (no merge), a threefold spread keeps 32-block splits merged in
+    split order; both against the oracle, with stale slots NaN-poisoned."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    B = 80
+    ctx = np.random.default_rng(500 + lo).integers(lo, hi, size=B)
+    w = decode_workload(MID, ctx, seed=29, name=f"mid-autosplit-{lo}-{hi}")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    d.step()
+    lg, ids = d.results()
+    d.step()
+    lg2, ids2 = d.results()
+    assert np.array_equal(lg, lg2) and np.array_equal(ids, ids2)
+    st, *_ = _check(w, lg, ids, list(range(0, B, 7)))
+    print(st)
+
+
 @pytest.mark.parametrize("cfg,B,row_tile", [("mid", 130, 11), ("mid", 200, 11), ("mid", 300, 11), ("mid", 300, 8),
                                             ("mid", 300, 7), ("mid", 200, 6), ("wide", 200, 11), ("wide", 300, 7),
                                             ("wide", 130, 6)])
