@@ -285,7 +285,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   const int t_first = kBlock * (b_lo + w_lo);                   // first key of the range
   const int t_end = min(kv_len, kBlock * (b_lo + w_lo + cnt));  // keys past it belong to others
   u32x4 kg[2][KC];
-  u32x4 vt[VC];
+  u32x4 vt[VC], vt2[VC];  // V of the even and the odd pairs
   if (cnt > 0) {
     load_k(kg, 0, cnt, w_lo);
     load_v(vt, 0, cnt, w_lo);
@@ -322,22 +322,31 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
         if (two) fold(op1, ml1);
     }
   }
-  // (the last pair is peeled so that the loop's loads are unconditional)
-  for (int p = 0; p + 1 < n_pairs; ++p) {
+  // Pair p + 1's K and V are both issued right after the scores of pair p
+  // (its V into the other of two V buffers), so both have pair p's P V to
+  // land in: the compiler waits for every outstanding load at the top of
+  // the walk loop, and a V issued after P V, as before, was waited for in
+  // full there.  Two pairs per iteration keep the buffers compile-time; the
+  // loop's loads are unconditional, the last one or two pairs are peeled.
+  auto step = [&](u32x4 (&vc)[VC], u32x4 (&vn)[VC], int p, bool more) {
     const int t0 = t_first + 2 * kBlock * p;
     PTerms pp;
     float alpha;
     pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, pp, alpha);
-    load_k(kg, p + 1, cnt, w_lo);
-    pair_pv<D>(vt, t0, t_end, pp, alpha, o);
-    load_v(vt, p + 1, cnt, w_lo);
+    if (more) {
+      load_k(kg, p + 1, cnt, w_lo);
+      load_v(vn, p + 1, cnt, w_lo);
+    }
+    pair_pv<D>(vc, t0, t_end, pp, alpha, o);
+  };
+  int p = 0;
+  for (; p + 2 < n_pairs; p += 2) {
+    step(vt, vt2, p, true);
+    step(vt2, vt, p + 1, true);
   }
-  if (n_pairs > 0) {
-    const int t0 = t_first + 2 * kBlock * (n_pairs - 1);
-    PTerms pp;
-    float alpha;
-    pair_scores<D, false>(qf, kg, t0, t_end, 0, sc, m, l, pp, alpha);
-    pair_pv<D>(vt, t0, t_end, pp, alpha, o);
+  if (p < n_pairs) {
+    step(vt, vt2, p, p + 1 < n_pairs);
+    if (p + 1 < n_pairs) step(vt2, vt, p + 1, false);
   }
 
   // ---- merge the waves of this workgroup
