@@ -244,6 +244,20 @@ void plan_prefill_items(BatchHost& b, int32_t group_size, int32_t block) {
       b.pre_items.insert(b.pre_items.end(), it, it + 3);
     }
   }
+  // prefill items too in order of their walks (the blocks up to their last
+  // row), longest first, ties in build order: the launch dispatches an
+  // item's KV heads together, so the longest items start in the first round
+  {
+    const int32_t n = b.n_pre_items();
+    std::vector<int32_t> order(n);
+    for (int32_t k = 0; k < n; ++k) order[k] = k;
+    auto blocks = [&](int32_t k) { return b.pos[b.pre_items[3 * k + 1] + b.pre_items[3 * k + 2] - 1] / block + 1; };
+    std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) { return blocks(x) > blocks(y); });
+    std::vector<int32_t> sorted(b.pre_items.size());
+    for (int32_t k = 0; k < n; ++k)
+      for (int32_t j = 0; j < 3; ++j) sorted[3 * k + j] = b.pre_items[3 * order[k] + j];
+    b.pre_items.swap(sorted);
+  }
   // longest remaining walk first, ties in row order
   auto walk = [&](int32_t r) { return (b.pos[r] + block) / block - b.pfx_blocks[r]; };
   std::stable_sort(b.dec_rows.begin(), b.dec_rows.end(), [&](int32_t x, int32_t y) { return walk(x) > walk(y); });

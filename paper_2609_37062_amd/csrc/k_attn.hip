@@ -274,8 +274,10 @@ __global__ __launch_bounds__(64 * (kPreTiles + 1)) void k_attn_prefill(AttnPrefi
   __shared__ int32_t tbl[kMaxPrefillBlocks];
   __shared__ WalkLds<D, 1> ring;
 
-  const int hk = blockIdx.y;
-  const int32_t* it = a.items + static_cast<size_t>(blockIdx.x) * 3;
+  // one-dimensional grid, an item's KV heads consecutive (items come
+  // longest walk first)
+  const int hk = blockIdx.x % a.Hkv;
+  const int32_t* it = a.items + static_cast<size_t>(blockIdx.x / a.Hkv) * 3;
   const int seq = it[0], row0 = it[1], n_rows = it[2];
   const int G = a.G;
   const int n_cols = n_rows * G;
@@ -339,7 +341,7 @@ __global__ __launch_bounds__(64 * (kPreTiles + 1)) void k_attn_prefill(AttnPrefi
 
 hipError_t launch_attn_prefill(const AttnPrefillArgs& a, int n_items, int head_dim, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  dim3 grid(n_items, a.Hkv);
+  dim3 grid(n_items * a.Hkv);
   if (head_dim == 128) {
     hipLaunchKernelGGL((k_attn_prefill<128>), grid, dim3(64 * (kPreTiles + 1)), 0, s, a);
   } else if (head_dim == 64) {
