@@ -175,6 +175,28 @@ def test_routed_prefill_matches_oracle(policy):
     d.release()
 
 
+@pytest.mark.parametrize("row_tile", [0, 7, 11])
+def test_routed_prefill_row_tiled(row_tile):
+    """Routed prefill of 405 rows (two 200-row prompts beside 5 decoding
+    sequences): the cohort-bounded projections of a row-tiled pass at the
+    default tile heights and with 7 and 11 row groups per tile (tuning key
+    10; a tile starting at or past its cohort's count exits), end to end
+    against the oracle and the first routed layer's K,V within one ulp."""
+    m = MIDR
+    ctx = np.random.default_rng(43).integers(10, 200, size=5)
+    w = mixed_workload(m, n_pre=2, plen=200, ctx=ctx, seed=44, name=f"routed-prefill-rt{row_tile}")
+    tape = _tape("random", m, w, seed=45)
+    d = _device(w)
+    d.eng.set_tuning(10, row_tile)
+    d.set_route(*tape)
+    d.step_routed()
+    lg, ids = d.results()
+    st, *_ = e2e_compare(w, lg, ids, route=tape)
+    print(f"[gpu] routed prefill rows={w.n_rows} row_tile={row_tile}: {st}", flush=True)
+    _first_routed_kv(d, w, tape, [0, 1, 2, 6])
+    d.release()
+
+
 @pytest.mark.parametrize("cfg,subset", [(2, [0, 15]), (5, [0, 77])])
 def test_routed_full_size(cfg, subset):
     """Random skip (r = 1, d = 0.5: half the routed decisions project) over
