@@ -368,7 +368,9 @@ int vsk_set_probe(vsk_handle* h, int32_t which, void* const* begin_events,
  * do not depend on it beyond floating-point summation order.
  * key 0: attention 16-token blocks per split-K work item (multiple of 8 in
  *        8..512), or 0 (the default) for automatic: 32 when fewer than 256
- *        (row, KV head) pairs are in the pass, else 96.
+ *        (row, KV head) pairs are in the pass, else 96; with 128..255 pairs
+ *        whose walks are within 20% of each other, one split per pair (the
+ *        longest walk rounded up to a multiple of 8 blocks).
  * key 1: inspection only -- run just the first `value` layers before the
  *        final norm and lm_head (0 = all layers), for layer-local checks.
  * key 2: execution path.  0 (default) and 1: one kernel per operation.
