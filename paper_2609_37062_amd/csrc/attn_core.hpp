@@ -325,8 +325,8 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int row, int hk, in
   // Pair p + 1's K and V are both issued right after the scores of pair p
   // (its V into the other of two V buffers), so both have pair p's P V to
   // land in: the compiler waits for every outstanding load at the top of
-  // the walk loop, and a V issued after P V, as before, was waited for in
-  // full there.  Two pairs per iteration keep the buffers compile-time; the
+  // the walk loop, so a V issued after P V would be waited for in full
+  // there.  Two pairs per iteration keep the buffers compile-time; the
   // loop's loads are unconditional, the last one or two pairs are peeled.
   auto step = [&](u32x4 (&vc)[VC], u32x4 (&vn)[VC], int p, bool more) {
     const int t0 = t_first + 2 * kBlock * p;
