@@ -251,6 +251,52 @@ def test_mid_prefix_groups(shared, bps):
     print(st)
 
 
+def _graph_replays_match(d, step, n=3):
+    """Capture `step` in a graph and replay it n times, with an eager pass
+    between replays: every replay reproduces the eager pass bit for bit."""
+    import torch
+    step()
+    lg1, ids1 = d.results()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(stream=s.cuda_stream)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step(stream=torch.cuda.current_stream().cuda_stream)
+    for _ in range(n):
+        d.logits.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        lg, ids = d.results()
+        np.testing.assert_array_equal(lg, lg1)
+        np.testing.assert_array_equal(ids, ids1)
+        step()
+        lg, ids = d.results()
+        np.testing.assert_array_equal(lg, lg1)
+    del g
+    return lg1, ids1
+
+
+def test_mixed_pass_graph_replay():
+    """A row-tiled mixed pass (two 200-row prompts prefilled beside 6
+    decodes: 406 rows, tile heights chosen by the launch rounds, prefill
+    items longest first) captured in a graph: every replay, with eager
+    passes between, reproduces the eager pass bit for bit, and the eager
+    pass matches the oracle."""
+    from paper_2609_37062_amd.runner import DeviceRun
+    ctx = np.random.default_rng(71).integers(20, 300, size=6)
+    w = mixed_workload(MID, n_pre=2, plen=200, ctx=ctx, seed=71, name="mid-mixed-graph")
+    print(f"[gpu] {w.name}", flush=True)
+    d = DeviceRun(w, poison_pool=True)
+    lg, ids = _graph_replays_match(d, d.step)
+    st, *_ = _check(w, lg, ids)
+    print(st)
+    d.release()
+
+
 def test_shared_prefix_graph_replay():
     """A decode pass with shared-prefix groups captured in a graph: every
     replay, with eager passes between, reproduces the eager pass bit for bit

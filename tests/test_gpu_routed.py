@@ -175,6 +175,23 @@ def test_routed_prefill_matches_oracle(policy):
     d.release()
 
 
+def test_routed_decode_graph_replay():
+    """A routed decode pass (random skip, 70 rows; cohort counts read on the
+    device by the count-bounded launches) captured in a graph: every replay,
+    with eager passes between, reproduces the eager pass bit for bit."""
+    from test_gpu_parity import _graph_replays_match
+    m = MIDR
+    ctx = np.random.default_rng(81).integers(0, 400, size=70)
+    w = decode_workload(m, ctx, seed=81, name="routed-graph")
+    tape = _tape("random", m, w, seed=82)
+    d = _device(w)
+    d.set_route(*tape)
+    lg, ids = _graph_replays_match(d, d.step_routed)
+    st, *_ = e2e_compare(w, lg, ids, list(range(0, 70, 7)), route=tape)
+    print(f"[gpu] routed graph: {st}", flush=True)
+    d.release()
+
+
 @pytest.mark.parametrize("row_tile", [0, 7, 11])
 def test_routed_prefill_row_tiled(row_tile):
     """Routed prefill of 405 rows (two 200-row prompts beside 5 decoding
